@@ -1,0 +1,196 @@
+"""Benchmark of the mixed-precision training step on one MI355X.
+
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--config NAME] [--no-cpu-baseline]
+
+A step is one pass of the whole hot path over one synthetic batch: cast the
+inputs, half forward, loss with the scale seed, half backward, unscale +
+finite check, masked AdamW with the fused half copy, loss-scale update.
+Inputs and parameters are resident in HBM before the timed region starts.
+
+Prints ONE JSON line.  `value` is train steps/s for the model workloads (or
+unscale+AdamW GB/s for the optimizer sweep); `roofline` covers the dominant
+kernel, timed with HIP events around each of its launches inside the timed
+steps; `cpu_baseline` times the CPU oracle on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+import workloads
+
+PEAK_MFMA_TFLOPS = {"f16": 2500.0, "bf16": 2500.0}   # dense, MI355X
+PEAK_HBM_GBS = 8000.0
+DEFAULT_CONFIG = "vit_block"
+
+# Measured FETCH_SIZE/WRITE_SIZE results for the dominant kernels (KiB per
+# dispatch scaled by the copy-kernel calibration factor), or None when the
+# kernel changed since the counters were taken.
+TRAFFIC = {}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--config", default=DEFAULT_CONFIG, choices=workloads.CONFIG_ORDER)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    return ap.parse_args()
+
+
+def cpu_threads() -> int:
+    try:
+        from threadpoolctl import threadpool_info
+        n = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+        return int(max(n)) if n else 1
+    except Exception:
+        return 1
+
+
+def cpu_baseline_train(cfg, budget_s):
+    """Oracle training steps on the host, as many as fit the time budget (>= 1)."""
+    from oracle import step as ostep
+    st = ostep.init_state(cfg)
+    batch = workloads.make_batch(cfg)
+    t0 = time.perf_counter()
+    n = 0
+    while True:
+        st, _ = ostep.train_step(cfg, st, batch, n)
+        n += 1
+        if time.perf_counter() - t0 >= budget_s or n >= cfg.steps:
+            break
+    dt = time.perf_counter() - t0
+    return {"value": n / dt, "unit": "steps/s", "cores": cpu_threads(), "kind": "oracle",
+            "sample": f"{n} full oracle training step(s) of the '{cfg.name}' workload, "
+                      f"{dt:.1f} s"}
+
+
+def cpu_baseline_sweep(cfg, budget_s):
+    """Oracle unscale + check + adjust + AdamW over a prefix of the tensor list."""
+    from oracle import step as ostep
+    sizes = workloads.sweep_sizes(cfg)
+    take, tot = [], 0
+    for i, n in enumerate(sizes):               # about 1e7 elements
+        take.append(int(n))
+        tot += int(n)
+        if tot >= 10_000_000:
+            break
+    cfg_s = workloads.SweepConfig(**{**cfg.__dict__, "n_tensors": len(take), "total": tot,
+                                     "injections": ()})
+    gf, params = workloads.sweep_tensors(cfg_s, np.array(take, np.int64))
+    gh, st = ostep.sweep_init(cfg_s, gf, params)
+    t0 = time.perf_counter()
+    n = 0
+    while True:
+        st, _, _ = ostep.sweep_step(cfg_s, st, gh, n)
+        n += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    gbs = n * tot * 28 / dt / 1e9
+    return {"value": gbs, "unit": "GB/s", "cores": cpu_threads(), "kind": "oracle",
+            "sample": f"{n} applied sweep step(s) over the first {len(take)} tensors "
+                      f"({tot} elements) of the sweep workload, {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(data-parallel sharding is described in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2507_03312_amd.train import make_step
+    from paper_2507_03312_amd.sweep import SweepStep
+
+    cfg = workloads.get(args.config)
+    torch.cuda.set_device(0)
+    dev = torch.device("cuda:0")
+
+    if args.config == "sweep":
+        steps = args.steps or 50
+        warm = args.warmup if args.warmup is not None else 5
+        sw = SweepStep(cfg, device=dev)
+        gf, params = workloads.sweep_tensors(cfg, sw.sizes)
+        sw.load(gf, params)
+        del gf, params
+        torch.cuda.synchronize()
+        for _ in range(warm):
+            sw.step()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * steps)]
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for i in range(steps):
+            ev[2 * i].record()
+            sw.step()
+            ev[2 * i + 1].record()
+        t1.record()
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / steps
+        per = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(steps)]
+        avg = float(np.mean(per))
+        bytes_per = sw.numel * 28            # g 2 + p,m,v 12 read; p,m,v 12 + half copy 2 written
+        gbs = bytes_per / (avg * 1e-3) / 1e9
+        line = {"metric": "unscale+AdamW GB/s", "value": round(gbs, 1), "unit": "GB/s",
+                "n_gpus": 1, "steps": steps, "warmup": warm, "ms_per_step": round(ms, 4),
+                "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+                "dtype": "f32 (f16 gradients)", "data": "synthetic",
+                "config": {"workload": "sweep: 200 fp16 gradient tensors, lognormal sizes, "
+                                       "1e8 elements, masked AdamW + half copy",
+                           "elements": sw.numel, "parallelism": "none"},
+                "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
+                             "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
+                             "traffic": TRAFFIC.get("sweep")}}
+        if not args.no_cpu_baseline:
+            line["cpu_baseline"] = cpu_baseline_sweep(cfg, args.cpu_seconds)
+        print(json.dumps(line))
+        return
+
+    steps = args.steps or {"mlp": 200, "vit_block": 100, "vit_s": 30, "vit_b": 20}[args.config]
+    warm = args.warmup if args.warmup is not None else 5
+    st = make_step(cfg, dev)
+    st.set_batch(workloads.make_batch(cfg))
+    site = st.dominant_site()
+    st.enable_site(site["name"], steps)
+    torch.cuda.synchronize()
+    for _ in range(warm):
+        st.step()
+    st.reset_site()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        st.step()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / steps
+    k_ms = st.site_mean_ms()
+    achieved = site["flops"] / (k_ms * 1e-3) / 1e12
+    peak = PEAK_MFMA_TFLOPS[cfg.half]
+    line = {"metric": "train steps/s", "value": round(1000.0 / ms, 3), "unit": "steps/s",
+            "n_gpus": 1, "steps": steps, "warmup": warm, "ms_per_step": round(ms, 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": cfg.half, "data": "synthetic",
+            "config": {"workload": st.describe(), "global_batch": cfg.batch,
+                       "seq_len": cfg.tokens or None, "parallelism": "none"},
+            "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak,
+                         "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                         "traffic": TRAFFIC.get(site["name"]),
+                         "kernel": site["desc"], "avg_launch_ms": round(k_ms, 5)}}
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline_train(cfg, args.cpu_seconds)
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

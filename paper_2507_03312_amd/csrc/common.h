@@ -1,0 +1,103 @@
+// Internal helpers shared by the HIP sources of libmpx (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <string>
+
+#include "mpx.h"
+
+namespace mpx {
+
+// ---------------------------------------------------------------- errors --
+
+// Per-thread message of the last failing call (mpx_last_error).
+void set_error(const std::string& msg);
+void clear_error();
+
+#define MPX_REQUIRE(cond, msg)                                  \
+  do {                                                          \
+    if (!(cond)) {                                              \
+      ::mpx::set_error(std::string(__func__) + ": " + (msg));   \
+      return MPX_ERR_INVALID;                                   \
+    }                                                           \
+  } while (0)
+
+#define MPX_HIP(call)                                                              \
+  do {                                                                             \
+    hipError_t e_ = (call);                                                        \
+    if (e_ != hipSuccess) {                                                        \
+      ::mpx::set_error(std::string(__func__) + ": " #call ": " + hipGetErrorString(e_)); \
+      return MPX_ERR_HIP;                                                          \
+    }                                                                              \
+  } while (0)
+
+// Check the launch that was just enqueued.
+#define MPX_LAUNCHED() MPX_HIP(hipGetLastError())
+
+inline bool is_half(mpx_dtype d) { return d == MPX_F16 || d == MPX_BF16; }
+
+// ------------------------------------------------------- 16-bit formats --
+
+// Round-to-nearest-even float32 -> half bits, via the hardware conversions
+// (v_cvt_f16_f32 in the default round-to-nearest-even mode; v_cvt_pk_bf16_f32,
+// which rounds to nearest even and keeps NaN a NaN).
+template <int DT> __device__ __forceinline__ uint16_t f2h(float x);
+template <> __device__ __forceinline__ uint16_t f2h<MPX_F16>(float x) {
+  return __builtin_bit_cast(uint16_t, (_Float16)x);
+}
+template <> __device__ __forceinline__ uint16_t f2h<MPX_BF16>(float x) {
+  return __builtin_bit_cast(uint16_t, (__bf16)x);
+}
+
+// Exact widening half bits -> float32.
+template <int DT> __device__ __forceinline__ float h2f(uint16_t h);
+template <> __device__ __forceinline__ float h2f<MPX_F16>(uint16_t h) {
+  return (float)__builtin_bit_cast(_Float16, h);
+}
+template <> __device__ __forceinline__ float h2f<MPX_BF16>(uint16_t h) {
+  return __builtin_bit_cast(float, (uint32_t)h << 16);
+}
+
+// Exponent field all ones: +-inf or NaN.
+template <int DT> __device__ __forceinline__ bool h_nonfinite(uint16_t h);
+template <> __device__ __forceinline__ bool h_nonfinite<MPX_F16>(uint16_t h) {
+  return (h & 0x7C00u) == 0x7C00u;
+}
+template <> __device__ __forceinline__ bool h_nonfinite<MPX_BF16>(uint16_t h) {
+  return (h & 0x7F80u) == 0x7F80u;
+}
+
+// GELU, tanh form, and its derivative, in float32.
+__device__ __forceinline__ float gelu_tanh(float x) {
+  const float c = 0.7978845608028654f, a = 0.044715f;
+  return 0.5f * x * (1.0f + tanhf(c * (x + a * x * x * x)));
+}
+__device__ __forceinline__ float gelu_tanh_grad(float x) {
+  const float c = 0.7978845608028654f, a = 0.044715f;
+  float t = tanhf(c * (x + a * x * x * x));
+  return 0.5f * (1.0f + t) + 0.5f * x * (1.0f - t * t) * c * (1.0f + 3.0f * a * x * x);
+}
+
+// ------------------------------------------------------------ reductions --
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+}  // namespace mpx

@@ -1,0 +1,463 @@
+"""The mixed-precision training step on the GPU, composed from libmpx calls.
+
+The order of calls follows MPX §3.4 (the transformed gradient function) and
+§3.5 (the masked optimizer update):
+
+  cast masters and inputs to half -> half forward + full-precision loss ->
+  backward seeded with the loss scale -> scaled half gradients ->
+  unscale + all-finite check -> masked AdamW (+ half copy of the new
+  masters) -> loss-scale update.
+
+Every arithmetic step runs in libmpx's HIP kernels.  PyTorch is used only to
+allocate device memory and to name the current stream; this module only
+marshals pointers and sizes.  No call synchronises the host.
+
+Memory layout: all parameters live in one float32 arena (masters), with
+AdamW's m and v in arenas of the same layout, and the half working copy and
+the half gradients in two half arenas of the same element offsets.  Every
+tensor starts at a multiple of 128 elements (256-byte aligned in the half
+arenas).  The multi-tensor sweeps see each arena as a single tensor; the
+padding between tensors stays zero (AdamW maps zero to zero).
+"""
+from __future__ import annotations
+
+import math
+import struct
+from typing import Dict, List, Optional
+
+import numpy as np
+import torch
+
+import workloads
+
+from . import binding as mx
+
+TORCH_HALF = {"f16": torch.float16, "bf16": torch.bfloat16}
+ALIGN = 128
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _off(t: torch.Tensor, elems: int) -> int:
+    """Device address of element ``elems`` of tensor ``t``."""
+    return t.data_ptr() + elems * t.element_size()
+
+
+def _stream() -> int:
+    return torch.cuda.current_stream().cuda_stream
+
+
+def pack_scale_state(scale, counter, period, factor=2.0, min_scale=1.0, max_scale=2.0 ** 127):
+    raw = struct.pack("<fiifff", scale, counter, period, factor, min_scale, max_scale)
+    return np.frombuffer(raw, dtype=np.int32).copy()
+
+
+def unpack_scale_state(words: np.ndarray):
+    scale, counter, period, factor, mn, mxs = struct.unpack("<fiifff", np.asarray(words, np.int32).tobytes())
+    return {"scale": scale, "counter": counter, "period": period, "factor": factor,
+            "min_scale": mn, "max_scale": mxs}
+
+
+class Arena:
+    """Flat arenas for masters (f32), m, v (f32), half copy and half grads."""
+
+    def __init__(self, specs, half: str, device):
+        self.names = [n for n, _, _ in specs]
+        self.shapes = {n: tuple(s) for n, s, _ in specs}
+        self.offsets: Dict[str, int] = {}
+        off = 0
+        for n, s, _ in specs:
+            self.offsets[n] = off
+            off += -(-int(np.prod(s)) // ALIGN) * ALIGN
+        self.total = off
+        hdt = TORCH_HALF[half]
+        self.p32 = torch.zeros(off, dtype=torch.float32, device=device)
+        self.m32 = torch.zeros_like(self.p32)
+        self.v32 = torch.zeros_like(self.p32)
+        self.h = torch.zeros(off, dtype=hdt, device=device)
+        self.g = torch.zeros(off, dtype=hdt, device=device)
+        self.L_p = mx.TensorList([self.p32])
+        self.L_m = mx.TensorList([self.m32])
+        self.L_v = mx.TensorList([self.v32])
+        self.L_h = mx.TensorList([self.h])
+        self.L_g = mx.TensorList([self.g])
+
+    def view(self, arena: torch.Tensor, name: str) -> torch.Tensor:
+        n = int(np.prod(self.shapes[name]))
+        return arena.narrow(0, self.offsets[name], n).view(self.shapes[name])
+
+    def w(self, name):        # half working copy
+        return self.view(self.h, name)
+
+    def gr(self, name):       # half gradient
+        return self.view(self.g, name)
+
+    def load_masters(self, masters: Dict[str, np.ndarray]):
+        host = np.zeros(self.total, np.float32)
+        for n in self.names:
+            o = self.offsets[n]
+            a = np.asarray(masters[n], np.float32).reshape(-1)
+            host[o:o + a.size] = a
+        self.p32.copy_(torch.from_numpy(host))
+        self.m32.zero_()
+        self.v32.zero_()
+
+    def read(self, arena: torch.Tensor) -> List[np.ndarray]:
+        """Host copies (float32) of every tensor of an arena, in spec order."""
+        a = arena.detach().float().cpu().numpy()
+        return [a[self.offsets[n]:self.offsets[n] + int(np.prod(self.shapes[n]))]
+                .reshape(self.shapes[n]).copy() for n in self.names]
+
+
+class TrainStep:
+    """Device state and the call sequence common to both model families."""
+
+    def __init__(self, cfg, device="cuda"):
+        self.cfg = cfg
+        self.device = torch.device(device)
+        self.half = cfg.half
+        self.dt = mx.DTYPES[cfg.half]
+        self.hdt = TORCH_HALF[cfg.half]
+        self.arena = Arena(workloads.param_specs(cfg), cfg.half, self.device)
+        self.d_state = torch.from_numpy(
+            pack_scale_state(cfg.scale_init, 0, cfg.period, cfg.factor, cfg.min_scale,
+                             cfg.max_scale)).to(self.device)
+        self.d_nonfinite = torch.zeros(1, dtype=torch.int32, device=self.device)
+        self.d_step = torch.zeros(1, dtype=torch.int32, device=self.device)
+        self.d_loss = torch.zeros(1, dtype=torch.float32, device=self.device)
+        self.hp = mx.AdamWHP(cfg.lr, cfg.beta1, cfg.beta2, cfg.eps, cfg.weight_decay)
+        self.half_copy_fresh = False
+        self.arena.load_masters(workloads.init_params(cfg))
+
+    # ---- state access (harness only; each of these synchronises) ----
+    def scale_state(self):
+        return unpack_scale_state(self.d_state.cpu().numpy())
+
+    def nonfinite(self) -> int:
+        return int(self.d_nonfinite.item())
+
+    def loss(self) -> float:
+        return float(self.d_loss.item())
+
+    def grads(self) -> List[np.ndarray]:
+        return self.arena.read(self.arena.g)
+
+    def masters(self) -> List[np.ndarray]:
+        return self.arena.read(self.arena.p32)
+
+    # ---- the step ----
+    def cast_params(self):
+        """MPX §3.1: half working copy of every master (first step only; later
+        steps get it from the AdamW kernel's fused half-copy write)."""
+        mx.mpx_cast_to_half(self.arena.L_p, self.arena.L_h, self.dt, _stream())
+        self.half_copy_fresh = True
+
+    def forward_backward(self):
+        if not self.half_copy_fresh:
+            self.cast_params()
+        self._forward_backward(_stream())
+
+    def finish(self):
+        """Unscale + finite check, masked AdamW (+ half copy), scale update."""
+        s = _stream()
+        a = self.arena
+        mx.mpx_unscale_check(a.L_g, self.dt, _ptr(self.d_state), _ptr(self.d_nonfinite), None, s)
+        mx.mpx_adamw_masked(a.L_p, a.L_m, a.L_v, a.L_g, self.dt, self.hp, _ptr(self.d_step),
+                            _ptr(self.d_state), _ptr(self.d_nonfinite), a.L_h, self.dt, s)
+        mx.mpx_scale_update(_ptr(self.d_state), _ptr(self.d_nonfinite), s)
+
+    def step(self):
+        self.forward_backward()
+        self.finish()
+
+    # ---- timing of one launch site with events on the current stream ----
+    _site = None
+
+    def enable_site(self, name: str, capacity: int):
+        self._site = name
+        self._ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                    for _ in range(capacity)]
+        self._n = 0
+
+    def reset_site(self):
+        self._n = 0
+
+    def _begin(self, name: str):
+        if self._site != name or self._n >= len(self._ev):
+            return None
+        pair = self._ev[self._n]
+        self._n += 1
+        pair[0].record()
+        return pair
+
+    @staticmethod
+    def _end(pair):
+        if pair is not None:
+            pair[1].record()
+
+    def site_mean_ms(self) -> float:
+        torch.cuda.synchronize()
+        return float(np.mean([a.elapsed_time(b) for a, b in self._ev[:self._n]]))
+
+    def inject(self, tensor: int, element: int, value: float):
+        """Harness fault injection: overwrite one gradient element (after the
+        backward pass, before the finite check)."""
+        name = self.arena.names[tensor]
+        flat = self.arena.gr(name).reshape(-1)
+        flat[element % flat.numel()] = value
+
+
+class MLPStep(TrainStep):
+    """2-layer MLP with GELU and an MSE loss."""
+
+    def __init__(self, cfg, device="cuda"):
+        super().__init__(cfg, device)
+        B, D, Dh = cfg.batch, cfg.d_in, cfg.d_hidden
+        dev, h = self.device, self.hdt
+        self.x32 = torch.zeros(B, D, dtype=torch.float32, device=dev)
+        self.t32 = torch.zeros(B, D, dtype=torch.float32, device=dev)
+        self.x16 = torch.zeros(B, D, dtype=h, device=dev)
+        self.t16 = torch.zeros(B, D, dtype=h, device=dev)
+        self.L_in = mx.TensorList([self.x32, self.t32])
+        self.L_in16 = mx.TensorList([self.x16, self.t16])
+        self.h_pre = torch.zeros(B, Dh, dtype=h, device=dev)
+        self.hid = torch.zeros(B, Dh, dtype=h, device=dev)
+        self.y = torch.zeros(B, D, dtype=h, device=dev)
+        self.dy = torch.zeros(B, D, dtype=h, device=dev)
+        self.dh_pre = torch.zeros(B, Dh, dtype=h, device=dev)
+        ws = max(mx.mpx_linear_bwd_workspace(B, D, Dh), mx.mpx_linear_bwd_workspace(B, Dh, D))
+        self.ws = torch.zeros(ws, dtype=torch.uint8, device=dev)
+
+    def dominant_site(self):
+        c = self.cfg
+        return {"name": "fc1.fwd", "flops": 2.0 * c.batch * c.d_hidden * c.d_in,
+                "desc": f"linear_fwd+GELU M={c.batch} N={c.d_hidden} K={c.d_in} ({c.half})"}
+
+    def describe(self):
+        c = self.cfg
+        return f"MLP {c.d_in}->{c.d_hidden}->{c.d_in} GELU, MSE, batch {c.batch}, {c.half}"
+
+    def set_batch(self, batch):
+        self.x32.copy_(torch.from_numpy(batch["x"]))
+        self.t32.copy_(torch.from_numpy(batch["target"]))
+
+    def _forward_backward(self, s):
+        c, a, dt = self.cfg, self.arena, self.dt
+        B, D, Dh = c.batch, c.d_in, c.d_hidden
+        mx.mpx_cast_to_half(self.L_in, self.L_in16, dt, s)
+        ev = self._begin("fc1.fwd")
+        mx.mpx_linear_fwd(_ptr(self.x16), _ptr(a.w("fc1.w")), _ptr(a.w("fc1.b")), None,
+                          _ptr(self.hid), _ptr(self.h_pre), B, Dh, D, dt, mx.MPX_ACT_GELU_TANH, s)
+        self._end(ev)
+        mx.mpx_linear_fwd(_ptr(self.hid), _ptr(a.w("fc2.w")), _ptr(a.w("fc2.b")), None,
+                          _ptr(self.y), None, B, D, Dh, dt, mx.MPX_ACT_NONE, s)
+        mx.mpx_mse(_ptr(self.y), _ptr(self.t16), B * D, _ptr(self.d_state), _ptr(self.d_loss),
+                   _ptr(self.dy), dt, s)
+        wsb = self.ws.numel()
+        mx.mpx_linear_bwd(_ptr(self.hid), _ptr(a.w("fc2.w")), _ptr(self.dy), _ptr(self.h_pre),
+                          mx.MPX_ACT_GELU_TANH, _ptr(self.dh_pre), _ptr(a.gr("fc2.w")),
+                          _ptr(a.gr("fc2.b")), B, D, Dh, dt, _ptr(self.ws), wsb, s)
+        mx.mpx_linear_bwd(_ptr(self.x16), _ptr(a.w("fc1.w")), _ptr(self.dh_pre), None,
+                          mx.MPX_ACT_NONE, None, _ptr(a.gr("fc1.w")), _ptr(a.gr("fc1.b")),
+                          B, Dh, D, dt, _ptr(self.ws), wsb, s)
+
+
+class ViTStep(TrainStep):
+    """Pre-LayerNorm ViT (token or image input), CLS pooling, CE loss."""
+
+    def __init__(self, cfg, device="cuda"):
+        super().__init__(cfg, device)
+        B, T, d, H, F, Cn = cfg.batch, cfg.tokens, cfg.d_model, cfg.heads, cfg.d_mlp, cfg.classes
+        self.ldT = -(-T // 8) * 8
+        M = B * T
+        dev, h = self.device, self.hdt
+        z = lambda *shape: torch.zeros(*shape, dtype=h, device=dev)
+        if cfg.image:
+            G, Pd = cfg.n_patches, cfg.patch_dim
+            self.img = torch.zeros(B, cfg.image, cfg.image, cfg.channels, dtype=torch.float32,
+                                   device=dev)
+            self.patches = z(B * G, Pd)
+            self.E = z(B * G, d)
+            self.dE = z(B * G, d)
+        else:
+            self.tok32 = torch.zeros(M, d, dtype=torch.float32, device=dev)
+            self.L_tok32 = mx.TensorList([self.tok32])
+        self.x0 = z(M, d)
+        self.L_x0 = mx.TensorList([self.x0])
+        self.blocks = []
+        for _ in range(cfg.depth):
+            self.blocks.append({
+                "a": z(M, d), "qkv": z(M, 3 * d), "P": z(B * H * T, self.ldT), "O": z(M, d),
+                "x1": z(M, d), "c": z(M, d), "u_pre": z(M, F), "u": z(M, F), "x2": z(M, d)})
+        self.S = z(B * H * T, self.ldT)
+        self.dP = z(B * H * T, self.ldT)
+        self.dS = z(B * H * T, self.ldT)
+        self.zf = z(B, d)
+        self.logits = z(B, Cn)
+        self.dlogits = z(B, Cn)
+        self.dz = z(B, d)
+        self.dxa = z(M, d)
+        self.dxb = z(M, d)
+        self.du_pre = z(M, F)
+        self.dc = z(M, d)
+        self.dx1 = z(M, d)
+        self.dO = z(M, d)
+        self.dqkv = z(M, 3 * d)
+        self.da = z(M, d)
+        self.labels = torch.zeros(B, dtype=torch.int32, device=dev)
+        shapes = [(M, 3 * d, d), (M, d, d), (M, F, d), (M, d, F), (B, Cn, d)]
+        if cfg.image:
+            shapes.append((B * cfg.n_patches, d, cfg.patch_dim))
+        ws = max(mx.mpx_linear_bwd_workspace(*s) for s in shapes)
+        ws = max(ws, mx.mpx_layernorm_bwd_workspace(M, d))
+        self.ws = torch.zeros(ws, dtype=torch.uint8, device=dev)
+
+    def dominant_site(self):
+        c = self.cfg
+        M = c.batch * c.tokens
+        return {"name": "blk0.up.fwd", "flops": 2.0 * M * c.d_mlp * c.d_model,
+                "desc": f"linear_fwd+GELU (MLP up-projection) M={M} N={c.d_mlp} K={c.d_model} ({c.half})"}
+
+    def describe(self):
+        c = self.cfg
+        inp = (f"{c.image}x{c.image}x{c.channels} images, patch {c.patch}" if c.image
+               else f"{c.tokens}x{c.d_model} token inputs")
+        return (f"ViT pre-LN, {c.depth} block(s), d={c.d_model}, {c.heads} heads, MLP {c.d_mlp}, "
+                f"{c.tokens} tokens, {inp}, {c.classes} classes, batch {c.batch}, {c.half}, "
+                f"fp32 masters + masked AdamW, dynamic loss scaling")
+
+    def set_batch(self, batch):
+        c = self.cfg
+        if c.image:
+            self.img.copy_(torch.from_numpy(batch["x"]))
+        else:
+            self.tok32.copy_(torch.from_numpy(batch["x"].reshape(c.batch * c.tokens, c.d_model)))
+        self.labels.copy_(torch.from_numpy(batch["labels"].astype(np.int32)))
+
+    # attention core of one block: S = Q K^T, P = softmax, O = P V
+    def _attn_fwd(self, blk, s):
+        c, dt = self.cfg, self.dt
+        B, T, d, H, hd, ldT = c.batch, c.tokens, c.d_model, c.heads, c.head_dim, self.ldT
+        qkv, P, O = blk["qkv"], blk["P"], blk["O"]
+        mx.mpx_gemm_batched(0, 1, T, T, hd, B, H,
+                            _ptr(qkv), 3 * d, T * 3 * d, hd,
+                            _off(qkv, d), 3 * d, T * 3 * d, hd,
+                            _ptr(self.S), ldT, H * T * ldT, T * ldT, dt, s)
+        mx.mpx_softmax_fwd(_ptr(self.S), _ptr(P), B * H * T, T, ldT, 1.0 / math.sqrt(hd), dt, s)
+        mx.mpx_gemm_batched(0, 0, T, hd, T, B, H,
+                            _ptr(P), ldT, H * T * ldT, T * ldT,
+                            _off(qkv, 2 * d), 3 * d, T * 3 * d, hd,
+                            _ptr(O), d, T * d, hd, dt, s)
+
+    def _attn_bwd(self, blk, s):
+        c, dt = self.cfg, self.dt
+        B, T, d, H, hd, ldT = c.batch, c.tokens, c.d_model, c.heads, c.head_dim, self.ldT
+        qkv, P, dO, dqkv = blk["qkv"], blk["P"], self.dO, self.dqkv
+        # dP = dO V^T
+        mx.mpx_gemm_batched(0, 1, T, T, hd, B, H, _ptr(dO), d, T * d, hd,
+                            _off(qkv, 2 * d), 3 * d, T * 3 * d, hd,
+                            _ptr(self.dP), ldT, H * T * ldT, T * ldT, dt, s)
+        # dV = P^T dO
+        mx.mpx_gemm_batched(1, 0, T, hd, T, B, H, _ptr(P), ldT, H * T * ldT, T * ldT,
+                            _ptr(dO), d, T * d, hd,
+                            _off(dqkv, 2 * d), 3 * d, T * 3 * d, hd, dt, s)
+        mx.mpx_softmax_bwd(_ptr(P), _ptr(self.dP), _ptr(self.dS), B * H * T, T, ldT,
+                           1.0 / math.sqrt(hd), dt, s)
+        # dQ = dS K
+        mx.mpx_gemm_batched(0, 0, T, hd, T, B, H, _ptr(self.dS), ldT, H * T * ldT, T * ldT,
+                            _off(qkv, d), 3 * d, T * 3 * d, hd,
+                            _ptr(dqkv), 3 * d, T * 3 * d, hd, dt, s)
+        # dK = dS^T Q
+        mx.mpx_gemm_batched(1, 0, T, hd, T, B, H, _ptr(self.dS), ldT, H * T * ldT, T * ldT,
+                            _ptr(qkv), 3 * d, T * 3 * d, hd,
+                            _off(dqkv, d), 3 * d, T * 3 * d, hd, dt, s)
+
+    def _forward_backward(self, s):
+        c, a, dt = self.cfg, self.arena, self.dt
+        B, T, d, F, Cn = c.batch, c.tokens, c.d_model, c.d_mlp, c.classes
+        M = B * T
+        W, G = a.w, a.gr
+        wsp, wsb = _ptr(self.ws), self.ws.numel()
+        GELU, NONE = mx.MPX_ACT_GELU_TANH, mx.MPX_ACT_NONE
+        # ---- inputs (MPX §3.4: cast inputs to half) and embedding ----
+        if c.image:
+            mx.mpx_patchify_cast(_ptr(self.img), _ptr(self.patches), B, c.image, c.image,
+                                 c.channels, c.patch, dt, s)
+            mx.mpx_linear_fwd(_ptr(self.patches), _ptr(W("patch.w")), _ptr(W("patch.b")), None,
+                              _ptr(self.E), None, B * c.n_patches, d, c.patch_dim, dt, NONE, s)
+            mx.mpx_embed_assemble(_ptr(self.E), _ptr(W("cls")), _ptr(W("pos")), _ptr(self.x0),
+                                  B, T, d, dt, s)
+        else:
+            mx.mpx_cast_to_half(self.L_tok32, self.L_x0, dt, s)
+        # ---- blocks ----
+        x = self.x0
+        for i, blk in enumerate(self.blocks):
+            p = f"blk{i}."
+            mx.mpx_layernorm_fwd(_ptr(x), d, _ptr(W(p + "ln1.g")), _ptr(W(p + "ln1.b")),
+                                 _ptr(blk["a"]), None, M, d, dt, s)
+            mx.mpx_linear_fwd(_ptr(blk["a"]), _ptr(W(p + "qkv.w")), _ptr(W(p + "qkv.b")), None,
+                              _ptr(blk["qkv"]), None, M, 3 * d, d, dt, NONE, s)
+            self._attn_fwd(blk, s)
+            mx.mpx_linear_fwd(_ptr(blk["O"]), _ptr(W(p + "proj.w")), _ptr(W(p + "proj.b")),
+                              _ptr(x), _ptr(blk["x1"]), None, M, d, d, dt, NONE, s)
+            mx.mpx_layernorm_fwd(_ptr(blk["x1"]), d, _ptr(W(p + "ln2.g")), _ptr(W(p + "ln2.b")),
+                                 _ptr(blk["c"]), None, M, d, dt, s)
+            ev = self._begin(f"blk{i}.up.fwd")
+            mx.mpx_linear_fwd(_ptr(blk["c"]), _ptr(W(p + "up.w")), _ptr(W(p + "up.b")), None,
+                              _ptr(blk["u"]), _ptr(blk["u_pre"]), M, F, d, dt, GELU, s)
+            self._end(ev)
+            mx.mpx_linear_fwd(_ptr(blk["u"]), _ptr(W(p + "down.w")), _ptr(W(p + "down.b")),
+                              _ptr(blk["x1"]), _ptr(blk["x2"]), None, M, d, F, dt, NONE, s)
+            x = blk["x2"]
+        # ---- head: LN on the CLS rows, linear, cross-entropy seeded with the scale ----
+        mx.mpx_layernorm_fwd(_ptr(x), T * d, _ptr(W("lnf.g")), _ptr(W("lnf.b")), _ptr(self.zf),
+                             None, B, d, dt, s)
+        mx.mpx_linear_fwd(_ptr(self.zf), _ptr(W("head.w")), _ptr(W("head.b")), None,
+                          _ptr(self.logits), None, B, Cn, d, dt, NONE, s)
+        mx.mpx_cross_entropy(_ptr(self.logits), Cn, _ptr(self.labels), B, Cn, _ptr(self.d_state),
+                             _ptr(self.d_loss), _ptr(self.dlogits), dt, s)
+        # ---- backward ----
+        mx.mpx_linear_bwd(_ptr(self.zf), _ptr(W("head.w")), _ptr(self.dlogits), None, NONE,
+                          _ptr(self.dz), _ptr(G("head.w")), _ptr(G("head.b")), B, Cn, d, dt,
+                          wsp, wsb, s)
+        dx = self.dxa
+        mx.mpx_zero(_ptr(dx), dx.numel() * 2, s)
+        mx.mpx_layernorm_bwd(_ptr(x), T * d, _ptr(W("lnf.g")), _ptr(self.dz), None, _ptr(dx),
+                             T * d, _ptr(G("lnf.g")), _ptr(G("lnf.b")), B, d, dt, wsp, wsb, s)
+        for i in reversed(range(c.depth)):
+            blk = self.blocks[i]
+            p = f"blk{i}."
+            xin = self.x0 if i == 0 else self.blocks[i - 1]["x2"]
+            dx_out = self.dxb if dx is self.dxa else self.dxa
+            mx.mpx_linear_bwd(_ptr(blk["u"]), _ptr(W(p + "down.w")), _ptr(dx), _ptr(blk["u_pre"]),
+                              GELU, _ptr(self.du_pre), _ptr(G(p + "down.w")), _ptr(G(p + "down.b")),
+                              M, d, F, dt, wsp, wsb, s)
+            mx.mpx_linear_bwd(_ptr(blk["c"]), _ptr(W(p + "up.w")), _ptr(self.du_pre), None, NONE,
+                              _ptr(self.dc), _ptr(G(p + "up.w")), _ptr(G(p + "up.b")),
+                              M, F, d, dt, wsp, wsb, s)
+            mx.mpx_layernorm_bwd(_ptr(blk["x1"]), d, _ptr(W(p + "ln2.g")), _ptr(self.dc), _ptr(dx),
+                                 _ptr(self.dx1), d, _ptr(G(p + "ln2.g")), _ptr(G(p + "ln2.b")),
+                                 M, d, dt, wsp, wsb, s)
+            mx.mpx_linear_bwd(_ptr(blk["O"]), _ptr(W(p + "proj.w")), _ptr(self.dx1), None, NONE,
+                              _ptr(self.dO), _ptr(G(p + "proj.w")), _ptr(G(p + "proj.b")),
+                              M, d, d, dt, wsp, wsb, s)
+            self._attn_bwd(blk, s)
+            mx.mpx_linear_bwd(_ptr(blk["a"]), _ptr(W(p + "qkv.w")), _ptr(self.dqkv), None, NONE,
+                              _ptr(self.da), _ptr(G(p + "qkv.w")), _ptr(G(p + "qkv.b")),
+                              M, 3 * d, d, dt, wsp, wsb, s)
+            mx.mpx_layernorm_bwd(_ptr(xin), d, _ptr(W(p + "ln1.g")), _ptr(self.da), _ptr(self.dx1),
+                                 _ptr(dx_out), d, _ptr(G(p + "ln1.g")), _ptr(G(p + "ln1.b")),
+                                 M, d, dt, wsp, wsb, s)
+            dx = dx_out
+        if c.image:
+            mx.mpx_embed_assemble_bwd(_ptr(dx), _ptr(self.dE), _ptr(G("cls")), _ptr(G("pos")),
+                                      B, T, d, dt, s)
+            mx.mpx_linear_bwd(_ptr(self.patches), _ptr(W("patch.w")), _ptr(self.dE), None, NONE,
+                              None, _ptr(G("patch.w")), _ptr(G("patch.b")), B * c.n_patches, d,
+                              c.patch_dim, dt, wsp, wsb, s)
+
+
+def make_step(cfg, device="cuda") -> TrainStep:
+    return MLPStep(cfg, device) if cfg.kind == "mlp" else ViTStep(cfg, device)

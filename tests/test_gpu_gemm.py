@@ -1,0 +1,219 @@
+"""GPU parity of the half GEMMs (float32 accumulation) against the oracle,
+through the C ABI: linear forward with bias / GELU / residual epilogues,
+linear backward (dX, dX through GELU', split-K dW, db) and the batched GEMM of
+the attention core, in float16 and bfloat16.
+
+Bar (per element): |gpu - oracle| <= ulp(oracle) + 2 K 2^-24 (|A||B|), the
+difference allowed between two float32 summation orders followed by one
+rounding to half.  Epilogues that round again (GELU, residual) are checked
+against the oracle's op applied to the GPU's own pre-activation, within one
+half ulp (float32 vs float64 math inside the op).
+"""
+import numpy as np
+import pytest
+
+from oracle import ops
+from oracle.numfmt import round_to
+from oracle.policy import Policy
+from tests.gpu_util import (HAVE_GPU, assert_within, gemm_bound, to_dev_half, to_host, ulp)
+
+pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not HAVE_GPU, reason="no GPU")]
+
+if HAVE_GPU:
+    import torch
+    from paper_2507_03312_amd import binding as mx
+
+FMTS = ["f16", "bf16"]
+
+
+def _s():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _rand(shape, fmt, seed, std=1.0):
+    return round_to(np.random.default_rng(seed).normal(0, std, size=shape), fmt)
+
+
+def _empty(shape, fmt):
+    return torch.zeros(*shape, dtype=torch.float16 if fmt == "f16" else torch.bfloat16, device="cuda")
+
+
+SHAPES = [
+    (64, 1024, 512),     # MLP fc1
+    (70, 100, 72),       # ragged in M and N, K a multiple of 8
+    (33, 17, 50),        # every dim ragged, K not a multiple of 8 (scalar loads)
+    (300, 200, 1000),
+    (128, 10, 384),      # a 10-class head
+    (1, 8, 8),
+]
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("mnk", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_linear_fwd(fmt, mnk):
+    M, N, K = mnk
+    pol = Policy(fmt)
+    x = _rand((M, K), fmt, 1)
+    w = _rand((N, K), fmt, 2, 0.05)
+    b = _rand((N,), fmt, 3, 0.5)
+    r = _rand((M, N), fmt, 4)
+    dx, dw, db, dr = (to_dev_half(a, fmt) for a in (x, w, b, r))
+    y, pre, y2 = _empty((M, N), fmt), _empty((M, N), fmt), _empty((M, N), fmt)
+    dt = mx.DTYPES[fmt]
+    # plain + bias
+    mx.mpx_linear_fwd(dx.data_ptr(), dw.data_ptr(), db.data_ptr(), None, y.data_ptr(), None,
+                      M, N, K, dt, mx.MPX_ACT_NONE, _s())
+    ref = ops.linear_fwd(pol, x, w, b)
+    bound = gemm_bound(x, w.T, ref, fmt, K)
+    assert_within(to_host(y), ref, bound, "linear")
+    # GELU epilogue: pre-activation within the GEMM bound, output = gelu(own pre)
+    mx.mpx_linear_fwd(dx.data_ptr(), dw.data_ptr(), db.data_ptr(), None, y.data_ptr(),
+                      pre.data_ptr(), M, N, K, dt, mx.MPX_ACT_GELU_TANH, _s())
+    gpre = to_host(pre)
+    assert_within(gpre, ref, bound, "pre-activation")
+    g_ref = ops.gelu_fwd(pol, gpre)
+    assert_within(to_host(y), g_ref, ulp(g_ref, fmt), "gelu epilogue")
+    # residual epilogue, no bias
+    mx.mpx_linear_fwd(dx.data_ptr(), dw.data_ptr(), None, dr.data_ptr(), y2.data_ptr(), None,
+                      M, N, K, dt, mx.MPX_ACT_NONE, _s())
+    mx.mpx_linear_fwd(dx.data_ptr(), dw.data_ptr(), None, None, y.data_ptr(), None,
+                      M, N, K, dt, mx.MPX_ACT_NONE, _s())
+    own = to_host(y)
+    ref0 = ops.linear_fwd(pol, x, w, None)
+    assert_within(own, ref0, gemm_bound(x, w.T, ref0, fmt, K), "linear no bias")
+    assert_within(to_host(y2), ops.add(pol, own, r), 0.0, "residual epilogue")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("mnk", SHAPES + [(4096, 384, 384), (2500, 96, 40)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_linear_bwd(fmt, mnk):
+    M, N, K = mnk
+    pol = Policy(fmt)
+    x = _rand((M, K), fmt, 11)
+    w = _rand((N, K), fmt, 12, 0.05)
+    dy = _rand((M, N), fmt, 13)
+    xpre = _rand((M, K), fmt, 14)
+    tx, tw, tdy, txp = (to_dev_half(a, fmt) for a in (x, w, dy, xpre))
+    gdx, gdw, gdb = _empty((M, K), fmt), _empty((N, K), fmt), _empty((N,), fmt)
+    ws_n = mx.mpx_linear_bwd_workspace(M, N, K)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    dt = mx.DTYPES[fmt]
+    mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), None, mx.MPX_ACT_NONE,
+                      gdx.data_ptr(), gdw.data_ptr(), gdb.data_ptr(), M, N, K, dt,
+                      ws.data_ptr(), ws_n, _s())
+    rdx, rdw, rdb = ops.linear_bwd(pol, x, w, dy)
+    assert_within(to_host(gdx), rdx, gemm_bound(dy, w, rdx, fmt, N), "dX")
+    assert_within(to_host(gdw), rdw, gemm_bound(dy.T, x, rdw, fmt, M), "dW")
+    colb = ulp(rdb, fmt) + 2.0 * M * 2.0 ** -24 * np.abs(dy.astype(np.float64)).sum(axis=0)
+    assert_within(to_host(gdb), rdb, colb, "db")
+    # dX through GELU': half(half(dY W) * gelu'(Xpre))
+    mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), txp.data_ptr(),
+                      mx.MPX_ACT_GELU_TANH, gdx.data_ptr(), gdw.data_ptr(), None, M, N, K, dt,
+                      ws.data_ptr(), ws_n, _s())
+    got = to_host(gdx)
+    ref = ops.gelu_bwd(pol, xpre, rdx)
+    # GPU's own dX may differ from rdx by the GEMM bound, scaled by |gelu'| <= 1.13
+    bound = 1.13 * gemm_bound(dy, w, rdx, fmt, N) + ulp(ref, fmt)
+    assert_within(got, ref, bound, "dX through gelu'")
+
+
+def test_linear_bwd_workspace_is_checked():
+    M, N, K = 256, 256, 256
+    t = _empty((M, K), "f16")
+    with pytest.raises(mx.MPXError, match="workspace"):
+        mx.mpx_linear_bwd(t.data_ptr(), t.data_ptr(), t.data_ptr(), None, 0, t.data_ptr(),
+                          t.data_ptr(), None, M, N, K, mx.MPX_F16, None, 0, _s())
+
+
+def test_invalid_arguments_raise_before_launch():
+    t = _empty((8, 8), "f16")
+    with pytest.raises(mx.MPXError):
+        mx.mpx_linear_fwd(t.data_ptr(), None, None, None, t.data_ptr(), None, 8, 8, 8,
+                          mx.MPX_F16, 0, _s())
+    with pytest.raises(mx.MPXError):
+        mx.mpx_linear_fwd(t.data_ptr(), t.data_ptr(), None, None, t.data_ptr(), None, 0, 8, 8,
+                          mx.MPX_F16, 0, _s())
+    with pytest.raises(mx.MPXError):
+        mx.mpx_linear_fwd(t.data_ptr(), t.data_ptr(), None, None, t.data_ptr(), None, 8, 8, 8,
+                          7, 0, _s())
+
+
+ATTN = [(2, 3, 65, 64), (1, 2, 197, 64), (3, 1, 5, 16)]
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("bhtd", ATTN, ids=lambda s: "x".join(map(str, s)))
+def test_gemm_batched_attention_layouts(fmt, bhtd):
+    """The four operand layouts the attention core uses, on the real strides."""
+    B, H, T, hd = bhtd
+    d = H * hd
+    ldT = -(-T // 8) * 8
+    pol = Policy(fmt)
+    qkv = _rand((B * T, 3 * d), fmt, 21)
+    Pm = np.zeros((B, H, T, ldT), np.float32)
+    Pm[..., :T] = _rand((B, H, T, T), fmt, 22, 0.1)
+    tq, tp = to_dev_half(qkv, fmt), to_dev_half(Pm.reshape(B * H * T, ldT), fmt)
+    out_s = _empty((B * H * T, ldT), fmt)
+    out_o = _empty((B * T, d), fmt)
+    dt = mx.DTYPES[fmt]
+    e = tq.element_size()
+    q, k, v = ops.split_heads(qkv, B, T, H, hd)
+    # S = Q K^T
+    mx.mpx_gemm_batched(0, 1, T, T, hd, B, H, tq.data_ptr(), 3 * d, T * 3 * d, hd,
+                        tq.data_ptr() + d * e, 3 * d, T * 3 * d, hd,
+                        out_s.data_ptr(), ldT, H * T * ldT, T * ldT, dt, _s())
+    got = to_host(out_s).reshape(B, H, T, ldT)[..., :T]
+    k_t = np.swapaxes(k, -1, -2)
+    ref = pol.R(pol.mm(q, k_t))
+    bnd = ulp(ref, fmt) + 2 * hd * 2.0 ** -24 * (np.abs(q.astype(np.float64)) @ np.abs(k_t.astype(np.float64)))
+    assert_within(got, ref, bnd, "QK^T")
+    # O = P V  (k-major P with padded rows, V as a K x N slice)
+    mx.mpx_gemm_batched(0, 0, T, hd, T, B, H, tp.data_ptr(), ldT, H * T * ldT, T * ldT,
+                        tq.data_ptr() + 2 * d * e, 3 * d, T * 3 * d, hd,
+                        out_o.data_ptr(), d, T * d, hd, dt, _s())
+    Pv = Pm[..., :T]
+    ref = pol.R(pol.mm(Pv, v))
+    bnd = ulp(ref, fmt) + 2 * T * 2.0 ** -24 * (np.abs(Pv.astype(np.float64)) @ np.abs(v.astype(np.float64)))
+    got = to_host(out_o).reshape(B, T, H, hd).transpose(0, 2, 1, 3)
+    assert_within(got, ref, bnd, "PV")
+    # dV-like: P^T X (trans_a = 1) and dK-like with trans_a = 1, trans_b = 0
+    mx.mpx_gemm_batched(1, 0, T, hd, T, B, H, tp.data_ptr(), ldT, H * T * ldT, T * ldT,
+                        tq.data_ptr(), 3 * d, T * 3 * d, hd,
+                        out_o.data_ptr(), d, T * d, hd, dt, _s())
+    Pt = np.swapaxes(Pv, -1, -2)
+    ref = pol.R(pol.mm(Pt, q))
+    bnd = ulp(ref, fmt) + 2 * T * 2.0 ** -24 * (np.abs(Pt.astype(np.float64)) @ np.abs(q.astype(np.float64)))
+    got = to_host(out_o).reshape(B, T, H, hd).transpose(0, 2, 1, 3)
+    assert_within(got, ref, bnd, "P^T Q")
+
+
+@pytest.mark.parametrize("fmt,mnk", [("bf16", (12608, 2304, 768)), ("bf16", (12608, 768, 3072)),
+                                     ("f16", (16640, 1536, 384)), ("f16", (16384, 384, 48))],
+                         ids=lambda s: str(s))
+def test_full_size_linear_sampled(fmt, mnk):
+    """Full ViT-B / ViT-S layer shapes, forward and backward, in the launch
+    configuration the training step uses; sampled outputs against the oracle."""
+    M, N, K = mnk
+    pol = Policy(fmt)
+    rng = np.random.default_rng(5)
+    x = _rand((M, K), fmt, 31)
+    w = _rand((N, K), fmt, 32, 0.02)
+    dy = _rand((M, N), fmt, 33, 1e-2)
+    tx, tw, tdy = (to_dev_half(a, fmt) for a in (x, w, dy))
+    y, gdx, gdw, gdb = _empty((M, N), fmt), _empty((M, K), fmt), _empty((N, K), fmt), _empty((N,), fmt)
+    dt = mx.DTYPES[fmt]
+    mx.mpx_linear_fwd(tx.data_ptr(), tw.data_ptr(), None, None, y.data_ptr(), None, M, N, K, dt, 0, _s())
+    ws_n = mx.mpx_linear_bwd_workspace(M, N, K)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), None, 0, gdx.data_ptr(),
+                      gdw.data_ptr(), gdb.data_ptr(), M, N, K, dt, ws.data_ptr(), ws_n, _s())
+    rows = np.unique(rng.integers(0, M, 48))
+    cols = np.unique(rng.integers(0, N, 48))
+    ref = pol.gemm(x[rows], w[cols].T)
+    assert_within(to_host(y)[np.ix_(rows, cols)], ref, gemm_bound(x[rows], w[cols].T, ref, fmt, K), "Y")
+    kc = np.unique(rng.integers(0, K, 48))
+    ref = pol.gemm(dy[rows], w[:, kc])
+    assert_within(to_host(gdx)[np.ix_(rows, kc)], ref, gemm_bound(dy[rows], w[:, kc], ref, fmt, N), "dX")
+    ref = pol.gemm(dy[:, cols].T, x[:, kc])
+    assert_within(to_host(gdw)[np.ix_(cols, kc)], ref, gemm_bound(dy[:, cols].T, x[:, kc], ref, fmt, M), "dW")

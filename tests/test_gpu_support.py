@@ -1,0 +1,199 @@
+"""GPU parity of the support ops (full-precision islands and embedding data
+movement) against the oracle, through the C ABI.
+
+The GPU computes these ops in float32, the oracle in float64; both round once
+to half, so outputs agree within one half ulp (exactly, for data movement).
+Column sums (LayerNorm dgamma/dbeta, embedding dpos/dcls) also carry a float32
+summation-order term.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import ops
+from oracle.numfmt import round_to
+from oracle.policy import Policy
+from tests.gpu_util import HAVE_GPU, assert_same_values, assert_within, to_dev_half, to_host, ulp
+
+pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not HAVE_GPU, reason="no GPU")]
+
+if HAVE_GPU:
+    import torch
+    from paper_2507_03312_amd import binding as mx
+
+FMTS = ["f16", "bf16"]
+
+
+def _s():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _rand(shape, fmt, seed, std=1.0, mean=0.0):
+    return round_to(np.random.default_rng(seed).normal(mean, std, size=shape), fmt)
+
+
+def _empty(shape, fmt):
+    return torch.zeros(*shape, dtype=torch.float16 if fmt == "f16" else torch.bfloat16, device="cuda")
+
+
+def _sum_bound(x, fmt, ref):
+    return 2 * ulp(ref, fmt) + 2.0 * x.shape[0] * 2.0 ** -24 * np.abs(x.astype(np.float64)).sum(axis=0)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("rows,d", [(130, 384), (7, 768), (33, 100), (5, 2048)])
+def test_layernorm_fwd_bwd(fmt, rows, d):
+    pol = Policy(fmt)
+    x = _rand((rows, d), fmt, 1, 2.0, 0.5)
+    g = _rand((d,), fmt, 2, 0.2, 1.0)
+    b = _rand((d,), fmt, 3, 0.2)
+    dy = _rand((rows, d), fmt, 4)
+    rg = _rand((rows, d), fmt, 5)
+    tx, tg, tb, tdy, trg = (to_dev_half(a, fmt) for a in (x, g, b, dy, rg))
+    y = _empty((rows, d), fmt)
+    dt = mx.DTYPES[fmt]
+    mx.mpx_layernorm_fwd(tx.data_ptr(), d, tg.data_ptr(), tb.data_ptr(), y.data_ptr(), None,
+                         rows, d, dt, _s())
+    ref = ops.layernorm_fwd(pol, x, g, b)
+    assert_within(to_host(y), ref, ulp(ref, fmt) + 1e-5 * np.abs(ref), "LN fwd")
+    dx, dg, db = _empty((rows, d), fmt), _empty((d,), fmt), _empty((d,), fmt)
+    wsn = mx.mpx_layernorm_bwd_workspace(rows, d)
+    ws = torch.zeros(wsn, dtype=torch.uint8, device="cuda")
+    mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), trg.data_ptr(),
+                         dx.data_ptr(), d, dg.data_ptr(), db.data_ptr(), rows, d, dt,
+                         ws.data_ptr(), wsn, _s())
+    rdx, rdg, rdb = ops.layernorm_bwd(pol, x, g, dy)
+    rtot = ops.add(pol, rg, rdx)
+    assert_within(to_host(dx), rtot, 2 * ulp(rtot, fmt) + ulp(rdx, fmt) + 1e-4 * np.abs(rdx), "LN dX")
+    xhat_abs = np.abs(ops.layernorm_fwd(Policy("f64"), x, np.ones(d), np.zeros(d)))
+    assert_within(to_host(dg), rdg, _sum_bound(dy * xhat_abs, fmt, rdg) + 1e-4 * np.abs(rdg), "LN dgamma")
+    assert_within(to_host(db), rdb, _sum_bound(dy, fmt, rdb), "LN dbeta")
+
+
+def test_layernorm_strided_rows_cls_pooling():
+    """Final LayerNorm on the CLS rows of a [B, T, d] token matrix."""
+    fmt, B, T, d = "bf16", 6, 5, 384
+    pol = Policy(fmt)
+    x = _rand((B, T, d), fmt, 7)
+    g, b = _rand((d,), fmt, 8, 0.1, 1.0), _rand((d,), fmt, 9, 0.1)
+    tx, tg, tb = (to_dev_half(a, fmt) for a in (x, g, b))
+    z = _empty((B, d), fmt)
+    mx.mpx_layernorm_fwd(tx.data_ptr(), T * d, tg.data_ptr(), tb.data_ptr(), z.data_ptr(), None,
+                         B, d, mx.MPX_BF16, _s())
+    ref = ops.layernorm_fwd(pol, x[:, 0, :], g, b)
+    assert_within(to_host(z), ref, ulp(ref, fmt), "LN CLS rows")
+    dz = _rand((B, d), fmt, 10)
+    tdz = to_dev_half(dz, fmt)
+    dx = _empty((B * T, d), fmt)
+    dx.fill_(7.0)
+    dg, db = _empty((d,), fmt), _empty((d,), fmt)
+    wsn = mx.mpx_layernorm_bwd_workspace(B, d)
+    ws = torch.zeros(wsn, dtype=torch.uint8, device="cuda")
+    mx.mpx_layernorm_bwd(tx.data_ptr(), T * d, tg.data_ptr(), tdz.data_ptr(), None, dx.data_ptr(),
+                         T * d, dg.data_ptr(), db.data_ptr(), B, d, mx.MPX_BF16, ws.data_ptr(), wsn, _s())
+    got = to_host(dx).reshape(B, T, d)
+    rdx, _, _ = ops.layernorm_bwd(pol, x[:, 0, :], g, dz)
+    assert_within(got[:, 0, :], rdx, ulp(rdx, fmt) + 1e-4 * np.abs(rdx), "LN dX CLS rows")
+    assert np.all(got[:, 1:, :] == 7.0), "rows outside the CLS rows must not be written"
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("T", [65, 197, 5])
+def test_softmax_fwd_bwd(fmt, T):
+    pol = Policy(fmt)
+    rows = 37
+    ld = -(-T // 8) * 8
+    s = np.zeros((rows, ld), np.float32)
+    s[:, :T] = _rand((rows, T), fmt, 1, 3.0)
+    dp = np.zeros((rows, ld), np.float32)
+    dp[:, :T] = _rand((rows, T), fmt, 2)
+    ts, tdp = to_dev_half(s, fmt), to_dev_half(dp, fmt)
+    p = _empty((rows, ld), fmt)
+    p.fill_(3.0)
+    scale = 1.0 / math.sqrt(64)
+    mx.mpx_softmax_fwd(ts.data_ptr(), p.data_ptr(), rows, T, ld, scale, mx.DTYPES[fmt], _s())
+    gp = to_host(p)
+    ref = ops.softmax_fwd(pol, s[:, :T], scale)
+    assert_within(gp[:, :T], ref, ulp(ref, fmt), "softmax")
+    assert np.all(gp[:, T:] == 0)
+    ds = _empty((rows, ld), fmt)
+    tp = to_dev_half(gp, fmt)
+    mx.mpx_softmax_bwd(tp.data_ptr(), tdp.data_ptr(), ds.data_ptr(), rows, T, ld, scale,
+                       mx.DTYPES[fmt], _s())
+    ref = ops.softmax_bwd(pol, gp[:, :T], dp[:, :T], scale)
+    got = to_host(ds)
+    dot = np.abs((dp[:, :T].astype(np.float64) * gp[:, :T]).sum(axis=1, keepdims=True))
+    bnd = ulp(ref, fmt) + 1e-5 * scale * np.abs(gp[:, :T]) * (np.abs(dp[:, :T]) + dot)
+    assert_within(got[:, :T], ref, bnd, "softmax bwd")
+    assert np.all(got[:, T:] == 0)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("B,C", [(64, 1000), (256, 100), (3, 10)])
+def test_cross_entropy(fmt, B, C):
+    from paper_2507_03312_amd.train import pack_scale_state
+    pol = Policy(fmt)
+    z = _rand((B, C), fmt, 3, 2.0)
+    y = np.random.default_rng(4).integers(0, C, B).astype(np.int32)
+    scale = 2.0 ** 15
+    tz = to_dev_half(z, fmt)
+    ty = torch.from_numpy(y).cuda()
+    st = torch.from_numpy(pack_scale_state(scale, 0, 10)).cuda()
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    dz = _empty((B, C), fmt)
+    mx.mpx_cross_entropy(tz.data_ptr(), C, ty.data_ptr(), B, C, st.data_ptr(), loss.data_ptr(),
+                         dz.data_ptr(), mx.DTYPES[fmt], _s())
+    rl, rdz = ops.ce_fwd_bwd(pol, z, y, scale)
+    assert abs(float(loss.item()) - rl) <= 1e-5 * abs(rl)
+    assert_within(to_host(dz), rdz, ulp(rdz, fmt) + 1e-5 * np.abs(rdz), "CE cotangent")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_mse(fmt):
+    from paper_2507_03312_amd.train import pack_scale_state
+    pol = Policy(fmt)
+    yv, tv = _rand((64, 512), fmt, 5), _rand((64, 512), fmt, 6)
+    st = torch.from_numpy(pack_scale_state(2.0 ** 15, 0, 4)).cuda()
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    dy = _empty((64, 512), fmt)
+    ty, tt = to_dev_half(yv, fmt), to_dev_half(tv, fmt)
+    mx.mpx_mse(ty.data_ptr(), tt.data_ptr(), yv.size, st.data_ptr(), loss.data_ptr(), dy.data_ptr(),
+               mx.DTYPES[fmt], _s())
+    rl, rdy = ops.mse_fwd_bwd(pol, yv, tv, 2.0 ** 15)
+    assert abs(float(loss.item()) - rl) <= 1e-5 * rl
+    assert_within(to_host(dy), rdy, ulp(rdy, fmt), "MSE cotangent")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_patchify_embed_assemble_and_backward(fmt):
+    pol = Policy(fmt)
+    B, Hh, C, p, d = 3, 8, 3, 4, 16
+    G = (Hh // p) ** 2
+    T = G + 1
+    img = np.random.default_rng(1).uniform(0, 1, (B, Hh, Hh, C)).astype(np.float32)
+    timg = torch.from_numpy(img).cuda()
+    pt = _empty((B * G, p * p * C), fmt)
+    mx.mpx_patchify_cast(timg.data_ptr(), pt.data_ptr(), B, Hh, Hh, C, p, mx.DTYPES[fmt], _s())
+    assert_same_values(to_host(pt), pol.R(ops.patchify(img, p)), "patchify")
+    E = _rand((B * G, d), fmt, 2)
+    cls = _rand((d,), fmt, 3)
+    pos = _rand((T, d), fmt, 4)
+    tE, tc, tpos = (to_dev_half(a, fmt) for a in (E, cls, pos))
+    X = _empty((B * T, d), fmt)
+    mx.mpx_embed_assemble(tE.data_ptr(), tc.data_ptr(), tpos.data_ptr(), X.data_ptr(), B, T, d,
+                          mx.DTYPES[fmt], _s())
+    ref = np.empty((B, T, d), np.float32)
+    ref[:, 0] = ops.add(pol, cls, pos[0])
+    ref[:, 1:] = ops.add(pol, E.reshape(B, G, d), pos[None, 1:])
+    assert_same_values(to_host(X).reshape(B, T, d), ref, "embed assemble")
+    dX = _rand((B * T, d), fmt, 5)
+    tdX = to_dev_half(dX, fmt)
+    dE, dcls, dpos = _empty((B * G, d), fmt), _empty((d,), fmt), _empty((T, d), fmt)
+    mx.mpx_embed_assemble_bwd(tdX.data_ptr(), dE.data_ptr(), dcls.data_ptr(), dpos.data_ptr(), B,
+                              T, d, mx.DTYPES[fmt], _s())
+    d3 = dX.reshape(B, T, d)
+    assert_same_values(to_host(dE), d3[:, 1:].reshape(B * G, d), "dE")
+    rpos = pol.R(d3.astype(np.float64).sum(axis=0))
+    assert_within(to_host(dpos), rpos, _sum_bound(d3.reshape(B, -1), fmt, rpos.reshape(-1)).reshape(T, d), "dpos")
+    assert_same_values(to_host(dcls), to_host(dpos)[0], "dcls")

@@ -1,0 +1,121 @@
+"""End-to-end parity of the GPU training step against the oracle (MPX §3.4 and
+§3.5 composed), through the C ABI.
+
+* Lockstep: from the same start-of-step masters, the GPU's scaled half
+  gradients match the oracle's within 2e-2 relative per tensor (and per element
+  within 2e-2 of the tensor's max); then the oracle's unscale/check/adjust/AdamW
+  applied to the GPU's own gradients matches the GPU's post-step state: flag,
+  skip, scale and counter bit-exact, masters within 1e-5.
+* Free-running: the oracle and the GPU each run the steps on their own; the
+  flag / skip / scale trajectories are bit-exact and the masters agree within
+  2e-2 normwise.
+"""
+import numpy as np
+import pytest
+
+import workloads
+from oracle import step as ostep
+from oracle.policy import Policy
+from tests.gpu_util import HAVE_GPU, rel_norm_err
+
+pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not HAVE_GPU, reason="no GPU")]
+
+if HAVE_GPU:
+    import torch
+    from paper_2507_03312_amd.train import make_step
+
+
+def _lockstep(cfg, steps):
+    gpu = make_step(cfg)
+    batch = workloads.make_batch(cfg)
+    gpu.set_batch(batch)
+    ost = ostep.init_state(cfg)
+    pol = Policy(cfg.half)
+    for s in range(steps):
+        # oracle gradients from the GPU's current masters (identical start state)
+        start = ostep.TrainState(ost.names, gpu.masters(), ost.m, ost.v, ost.t, ost.scale)
+        loss_ref, g_ref = ostep.gradients(cfg, start, batch, pol)
+        gpu.forward_backward()
+        for inj in cfg.injections:
+            if inj.step == s:
+                gpu.inject(inj.tensor, inj.element, inj.value)
+        ostep.apply_injections(cfg, s, g_ref)
+        g_gpu = gpu.grads()
+        assert abs(gpu.loss() - loss_ref) <= 1e-2 * abs(loss_ref) + 1e-6
+        for name, a, b in zip(ost.names, g_gpu, g_ref):
+            fin = np.isfinite(b)
+            assert np.array_equal(np.isfinite(a), fin), name
+            if fin.all() and np.any(b):
+                assert rel_norm_err(a, b) <= 2e-2, (s, name, rel_norm_err(a, b))
+                assert np.max(np.abs(a - b)) <= 2e-2 * np.max(np.abs(b)), (s, name)
+        # oracle's steps 5-8 on the GPU's own gradients vs the GPU's update
+        ref_state, nf = ostep.finish_step(cfg, start, g_gpu)
+        gpu.finish()
+        assert gpu.nonfinite() == nf
+        st = gpu.scale_state()
+        assert st["scale"] == float(ref_state.scale.scale) and st["counter"] == ref_state.scale.counter
+        assert int(gpu.d_step.item()) == ref_state.t
+        for name, a, b in zip(ost.names, gpu.masters(), ref_state.masters):
+            assert np.all(np.abs(a - b) <= 1e-5 * np.maximum(np.abs(b), cfg.lr)), (s, name)
+        ost = ostep.TrainState(ost.names, ref_state.masters, ref_state.m, ref_state.v,
+                               ref_state.t, ref_state.scale)
+        # moments: compare once per step too
+        gm = gpu.arena.read(gpu.arena.m32)
+        for name, a, b in zip(ost.names, gm, ref_state.m):
+            assert np.all(np.abs(a - b) <= 1e-5 * max(float(np.max(np.abs(b))), 1e-30)), (s, name)
+
+
+def _free_running(cfg, steps):
+    gpu = make_step(cfg)
+    batch = workloads.make_batch(cfg)
+    gpu.set_batch(batch)
+    ost, results = ostep.run(cfg, steps=steps)
+    flags, scales = [], []
+    for s in range(steps):
+        scales.append(gpu.scale_state()["scale"])
+        gpu.forward_backward()
+        for inj in cfg.injections:
+            if inj.step == s:
+                gpu.inject(inj.tensor, inj.element, inj.value)
+        gpu.finish()
+        flags.append(gpu.nonfinite())
+    assert [f > 0 for f in flags] == [r.nonfinite > 0 for r in results]
+    assert scales == [r.scale_used for r in results]
+    st = gpu.scale_state()
+    assert st["scale"] == float(ost.scale.scale) and st["counter"] == ost.scale.counter
+    for name, a, b in zip(ost.names, gpu.masters(), ost.masters):
+        assert rel_norm_err(a, b) <= 2e-2, name
+
+
+def test_mlp_lockstep_10_steps_with_injection():
+    cfg = workloads.get("mlp")
+    _lockstep(cfg, cfg.steps)
+
+
+def test_mlp_free_running_10_steps():
+    cfg = workloads.get("mlp")
+    _free_running(cfg, cfg.steps)
+
+
+def test_vit_block_lockstep_small_batch():
+    cfg = workloads.scaled_down(workloads.get("vit_block"), batch=8)
+    _lockstep(cfg, 3)
+
+
+def test_vit_block_full_size_lockstep_one_step():
+    _lockstep(workloads.get("vit_block"), 1)
+
+
+def test_vit_s_reduced_lockstep():
+    cfg = workloads.scaled_down(workloads.get("vit_s"), batch=4, depth=2)
+    _lockstep(cfg, 2)
+
+
+def test_vit_b_reduced_lockstep():
+    cfg = workloads.scaled_down(workloads.get("vit_b"), batch=2, depth=1)
+    _lockstep(cfg, 2)
+
+
+def test_vit_block_free_running_small_batch():
+    cfg = workloads.scaled_down(workloads.get("vit_block"), batch=8)
+    _free_running(cfg, 4)
