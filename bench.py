@@ -124,22 +124,19 @@ def main():
         torch.cuda.synchronize()
         for _ in range(warm):
             sw.step()
-        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2 * steps)]
         torch.cuda.synchronize()
         t0 = torch.cuda.Event(enable_timing=True)
         t1 = torch.cuda.Event(enable_timing=True)
         t0.record()
-        for i in range(steps):
-            ev[2 * i].record()
+        for _ in range(steps):
             sw.step()
-            ev[2 * i + 1].record()
         t1.record()
         torch.cuda.synchronize()
         ms = t0.elapsed_time(t1) / steps
-        per = [ev[2 * i].elapsed_time(ev[2 * i + 1]) for i in range(steps)]
-        avg = float(np.mean(per))
         bytes_per = sw.numel * 28            # g 2 + p,m,v 12 read; p,m,v 12 + half copy 2 written
-        gbs = bytes_per / (avg * 1e-3) / 1e9
+        gbs = bytes_per / (ms * 1e-3) / 1e9
+        k_ms = sw.time_graph(sw.adamw)       # the dominant kernel: masked AdamW + half copy
+        k_gbs = bytes_per / (k_ms * 1e-3) / 1e9
         line = {"metric": "unscale+AdamW GB/s", "value": round(gbs, 1), "unit": "GB/s",
                 "n_gpus": 1, "steps": steps, "warmup": warm, "ms_per_step": round(ms, 4),
                 "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
@@ -147,34 +144,37 @@ def main():
                 "config": {"workload": "sweep: 200 fp16 gradient tensors, lognormal sizes, "
                                        "1e8 elements, masked AdamW + half copy",
                            "elements": sw.numel, "parallelism": "none"},
-                "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS,
-                             "unit": "GB/s", "frac": round(gbs / PEAK_HBM_GBS, 4),
-                             "traffic": TRAFFIC.get("sweep")}}
+                "roofline": {"bound": "hbm", "achieved": round(k_gbs, 1), "peak": PEAK_HBM_GBS,
+                             "unit": "GB/s", "frac": round(k_gbs / PEAK_HBM_GBS, 4),
+                             "traffic": TRAFFIC.get("sweep"),
+                             "kernel": "masked AdamW + half copy, 28 B/element",
+                             "avg_launch_ms": round(k_ms, 4)}}
         if not args.no_cpu_baseline:
             line["cpu_baseline"] = cpu_baseline_sweep(cfg, args.cpu_seconds)
         print(json.dumps(line))
         return
 
-    steps = args.steps or {"mlp": 200, "vit_block": 100, "vit_s": 30, "vit_b": 20}[args.config]
+    steps = args.steps or {"mlp": 500, "vit_block": 300, "vit_s": 50, "vit_b": 30}[args.config]
     warm = args.warmup if args.warmup is not None else 5
     st = make_step(cfg, dev)
     st.set_batch(workloads.make_batch(cfg))
     site = st.dominant_site()
-    st.enable_site(site["name"], steps)
     torch.cuda.synchronize()
-    for _ in range(warm):
+    for _ in range(warm):                 # eager steps (also the first cast)
         st.step()
-    st.reset_site()
+    st.capture()                          # the whole step as one HIP graph
+    for _ in range(warm):
+        st.replay()
     torch.cuda.synchronize()
     t0 = torch.cuda.Event(enable_timing=True)
     t1 = torch.cuda.Event(enable_timing=True)
     t0.record()
     for _ in range(steps):
-        st.step()
+        st.replay()
     t1.record()
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps
-    k_ms = st.site_mean_ms()
+    k_ms = st.time_dominant()
     achieved = site["flops"] / (k_ms * 1e-3) / 1e12
     peak = PEAK_MFMA_TFLOPS[cfg.half]
     line = {"metric": "train steps/s", "value": round(1000.0 / ms, 3), "unit": "steps/s",

@@ -56,16 +56,26 @@ def _elementwise(fn, *arrays, chunk=1 << 16):
     return out.reshape(np.shape(arrays[0]))
 
 
+def _sigmoid_2u(z):
+    """1 / (1 + exp(-2u)) with u = c (z + a z^3), i.e. (1 + tanh(u)) / 2."""
+    u = GELU_C * (z + GELU_A * z ** 3)
+    with np.errstate(over="ignore"):
+        return 1.0 / (1.0 + np.exp(-2.0 * u))
+
+
 def _gelu64(x):
+    """0.5 x (1 + tanh(u)), evaluated as x / (1 + exp(-2u)) (the same function;
+    this form has no cancellation for negative x)."""
     z = f64(x)
-    return 0.5 * z * (1.0 + np.tanh(GELU_C * (z + GELU_A * z ** 3)))
+    return z * _sigmoid_2u(z)
 
 
 def gelu_grad(x):
-    """d/dx of the tanh-form GELU, in float64."""
+    """d/dx of the tanh-form GELU, in float64:
+    sigma + 2 x sigma (1 - sigma) c (1 + 3 a x^2), with sigma = (1 + tanh(u)) / 2."""
     z = f64(x)
-    t = np.tanh(GELU_C * (z + GELU_A * z ** 3))
-    return 0.5 * (1.0 + t) + 0.5 * z * (1.0 - t * t) * GELU_C * (1.0 + 3.0 * GELU_A * z * z)
+    sg = _sigmoid_2u(z)
+    return sg + 2.0 * z * sg * (1.0 - sg) * GELU_C * (1.0 + 3.0 * GELU_A * z * z)
 
 
 def gelu_fwd(pol, x):

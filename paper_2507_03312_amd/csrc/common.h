@@ -69,15 +69,20 @@ template <> __device__ __forceinline__ bool h_nonfinite<MPX_BF16>(uint16_t h) {
   return (h & 0x7F80u) == 0x7F80u;
 }
 
-// GELU, tanh form, and its derivative, in float32.
-__device__ __forceinline__ float gelu_tanh(float x) {
+// GELU, tanh form, and its derivative, in float32.  With
+// sigma = (1 + tanh(u)) / 2 = 1 / (1 + exp(-2u)), u = c (x + a x^3):
+//   gelu(x) = x sigma,  gelu'(x) = sigma + 2 x sigma (1 - sigma) c (1 + 3 a x^2).
+// The sigmoid form avoids the cancellation of 1 + tanh(u) for negative x.
+__device__ __forceinline__ float gelu_sigma(float x) {
   const float c = 0.7978845608028654f, a = 0.044715f;
-  return 0.5f * x * (1.0f + tanhf(c * (x + a * x * x * x)));
+  const float u = c * (x + a * x * x * x);
+  return 1.0f / (1.0f + expf(-2.0f * u));
 }
+__device__ __forceinline__ float gelu_tanh(float x) { return x * gelu_sigma(x); }
 __device__ __forceinline__ float gelu_tanh_grad(float x) {
   const float c = 0.7978845608028654f, a = 0.044715f;
-  float t = tanhf(c * (x + a * x * x * x));
-  return 0.5f * (1.0f + t) + 0.5f * x * (1.0f - t * t) * c * (1.0f + 3.0f * a * x * x);
+  const float s = gelu_sigma(x);
+  return s + 2.0f * x * s * (1.0f - s) * c * (1.0f + 3.0f * a * x * x);
 }
 
 // ------------------------------------------------------------ reductions --

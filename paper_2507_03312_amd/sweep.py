@@ -52,13 +52,36 @@ class SweepStep:
             t.zero_()
         mx.mpx_cast_to_half(self.L_g32, self.L_g, self.dt, _stream())
 
-    def step(self):
-        s = _stream()
+    def step(self, s=None):
+        s = _stream() if s is None else s
         mx.mpx_unscale_check(self.L_g, self.dt, _ptr(self.d_state), _ptr(self.d_nonfinite), None, s)
         mx.mpx_adamw_masked(self.L_p, self.L_m, self.L_v, self.L_g, self.dt, self.hp,
                             _ptr(self.d_step), _ptr(self.d_state), _ptr(self.d_nonfinite),
                             self.L_h, self.dt, s)
         mx.mpx_scale_update(_ptr(self.d_state), _ptr(self.d_nonfinite), s)
+
+    def adamw(self, s):
+        mx.mpx_adamw_masked(self.L_p, self.L_m, self.L_v, self.L_g, self.dt, self.hp,
+                            _ptr(self.d_step), _ptr(self.d_state), _ptr(self.d_nonfinite),
+                            self.L_h, self.dt, s)
+
+    def time_graph(self, body, launches: int = 10, reps: int = 3) -> float:
+        """Mean ms per call of ``body(stream)`` from HIP events around a graph
+        of ``launches`` back-to-back calls."""
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(launches):
+                body(_stream())
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (reps * launches)
 
     def injections_at(self, step: int):
         return [inj for inj in self.cfg.injections if inj.step == step]

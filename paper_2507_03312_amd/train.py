@@ -172,34 +172,47 @@ class TrainStep:
         self.forward_backward()
         self.finish()
 
-    # ---- timing of one launch site with events on the current stream ----
-    _site = None
+    # ---- HIP graph of the whole step ----
+    graph = None
 
-    def enable_site(self, name: str, capacity: int):
-        self._site = name
-        self._ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                    for _ in range(capacity)]
-        self._n = 0
-
-    def reset_site(self):
-        self._n = 0
-
-    def _begin(self, name: str):
-        if self._site != name or self._n >= len(self._ev):
-            return None
-        pair = self._ev[self._n]
-        self._n += 1
-        pair[0].record()
-        return pair
-
-    @staticmethod
-    def _end(pair):
-        if pair is not None:
-            pair[1].record()
-
-    def site_mean_ms(self) -> float:
+    def capture(self):
+        """Record one whole step (forward, backward, unscale/check, masked
+        AdamW, scale update) into a HIP graph; ``replay`` then launches it with
+        a single host call.  Every piece of state the step reads (scale, flag,
+        step count, half copy) lives in device memory, so replays advance the
+        training state exactly as eager steps do."""
+        if not self.half_copy_fresh:
+            self.cast_params()
         torch.cuda.synchronize()
-        return float(np.mean([a.elapsed_time(b) for a, b in self._ev[:self._n]]))
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self._forward_backward(_stream())
+            self.finish()
+        torch.cuda.synchronize()
+        self.graph = g
+
+    def replay(self):
+        self.graph.replay()
+
+    # ---- timing of the dominant kernel ----
+    def time_dominant(self, launches: int = 20, reps: int = 5) -> float:
+        """Mean duration (ms) of one launch of the dominant kernel, from HIP
+        events around a graph of ``launches`` back-to-back launches of it with
+        the step's own operands (so no host launch gap is measured)."""
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(launches):
+                self._dominant_call(_stream())
+        g.replay()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            g.replay()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (reps * launches)
 
     def inject(self, tensor: int, element: int, value: float):
         """Harness fault injection: overwrite one gradient element (after the
@@ -230,6 +243,12 @@ class MLPStep(TrainStep):
         ws = max(mx.mpx_linear_bwd_workspace(B, D, Dh), mx.mpx_linear_bwd_workspace(B, Dh, D))
         self.ws = torch.zeros(ws, dtype=torch.uint8, device=dev)
 
+    def _dominant_call(self, s):
+        c, a = self.cfg, self.arena
+        mx.mpx_linear_fwd(_ptr(self.x16), _ptr(a.w("fc1.w")), _ptr(a.w("fc1.b")), None,
+                          _ptr(self.hid), _ptr(self.h_pre), c.batch, c.d_hidden, c.d_in, self.dt,
+                          mx.MPX_ACT_GELU_TANH, s)
+
     def dominant_site(self):
         c = self.cfg
         return {"name": "fc1.fwd", "flops": 2.0 * c.batch * c.d_hidden * c.d_in,
@@ -247,10 +266,7 @@ class MLPStep(TrainStep):
         c, a, dt = self.cfg, self.arena, self.dt
         B, D, Dh = c.batch, c.d_in, c.d_hidden
         mx.mpx_cast_to_half(self.L_in, self.L_in16, dt, s)
-        ev = self._begin("fc1.fwd")
-        mx.mpx_linear_fwd(_ptr(self.x16), _ptr(a.w("fc1.w")), _ptr(a.w("fc1.b")), None,
-                          _ptr(self.hid), _ptr(self.h_pre), B, Dh, D, dt, mx.MPX_ACT_GELU_TANH, s)
-        self._end(ev)
+        self._dominant_call(s)
         mx.mpx_linear_fwd(_ptr(self.hid), _ptr(a.w("fc2.w")), _ptr(a.w("fc2.b")), None,
                           _ptr(self.y), None, B, D, Dh, dt, mx.MPX_ACT_NONE, s)
         mx.mpx_mse(_ptr(self.y), _ptr(self.t16), B * D, _ptr(self.d_state), _ptr(self.d_loss),
@@ -313,6 +329,12 @@ class ViTStep(TrainStep):
         ws = max(mx.mpx_linear_bwd_workspace(*s) for s in shapes)
         ws = max(ws, mx.mpx_layernorm_bwd_workspace(M, d))
         self.ws = torch.zeros(ws, dtype=torch.uint8, device=dev)
+
+    def _dominant_call(self, s):
+        c, a, blk = self.cfg, self.arena, self.blocks[0]
+        mx.mpx_linear_fwd(_ptr(blk["c"]), _ptr(a.w("blk0.up.w")), _ptr(a.w("blk0.up.b")), None,
+                          _ptr(blk["u"]), _ptr(blk["u_pre"]), c.batch * c.tokens, c.d_mlp,
+                          c.d_model, self.dt, mx.MPX_ACT_GELU_TANH, s)
 
     def dominant_site(self):
         c = self.cfg
@@ -404,10 +426,8 @@ class ViTStep(TrainStep):
                               _ptr(x), _ptr(blk["x1"]), None, M, d, d, dt, NONE, s)
             mx.mpx_layernorm_fwd(_ptr(blk["x1"]), d, _ptr(W(p + "ln2.g")), _ptr(W(p + "ln2.b")),
                                  _ptr(blk["c"]), None, M, d, dt, s)
-            ev = self._begin(f"blk{i}.up.fwd")
             mx.mpx_linear_fwd(_ptr(blk["c"]), _ptr(W(p + "up.w")), _ptr(W(p + "up.b")), None,
                               _ptr(blk["u"]), _ptr(blk["u_pre"]), M, F, d, dt, GELU, s)
-            self._end(ev)
             mx.mpx_linear_fwd(_ptr(blk["u"]), _ptr(W(p + "down.w")), _ptr(W(p + "down.b")),
                               _ptr(blk["x1"]), _ptr(blk["x2"]), None, M, d, F, dt, NONE, s)
             x = blk["x2"]

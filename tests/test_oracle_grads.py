@@ -187,3 +187,24 @@ def test_patchify_brute_force():
                     for j in range(2):
                         for c in range(3):
                             assert pt[row, (i * 2 + j) * 3 + c] == img[b, gy * 2 + i, gx * 2 + j, c]
+
+
+def test_gelu_against_high_precision():
+    """The oracle's GELU (and derivative) against 50-digit evaluations of the
+    tanh form 0.5 x (1 + tanh(c (x + a x^3))), including the far negative tail
+    where 1 + tanh cancels in float64."""
+    import mpmath
+    mpmath.mp.dps = 1000   # 1 + tanh(u) cancels down to ~1e-860 at x = -30
+    xs = np.concatenate([np.linspace(-12, 6, 181), [-30.0, -9.5, -0.75, 0.0, 1e-3]])
+    c = mpmath.sqrt(2 / mpmath.pi)
+    for x in xs:
+        X = mpmath.mpf(float(x))
+        u = c * (X + mpmath.mpf("0.044715") * X ** 3)
+        ref = 0.5 * X * (1 + mpmath.tanh(u))
+        got = ops._gelu64(np.array([x]))[0]
+        assert abs(got - float(ref)) <= 1e-13 * abs(float(ref)) + 1e-300, x
+        dref = mpmath.diff(lambda t: 0.5 * t * (1 + mpmath.tanh(c * (t + mpmath.mpf("0.044715") * t ** 3))), X)
+        dgot = ops.gelu_grad(np.array([x]))[0]
+        assert abs(dgot - float(dref)) <= 1e-12 * abs(float(dref)) + 1e-300, x
+    # the bf16 GELU of a far-negative input is a tiny negative number, not zero
+    assert ops.gelu_fwd(Policy("bf16"), np.array([-8.0]))[0] < 0
