@@ -196,8 +196,8 @@ int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, const void*
 size_t mpx_layernorm_bwd_workspace(int64_t rows, int64_t d);
 
 /* Row softmax of scale * S (float32 math): P = half(softmax(scale * S)).
- * rows of length n with row stride ld (S and P); columns n..ld-1 of P are set
- * to zero. */
+ * rows of length n (1 <= n <= 1024) with row stride ld (S and P); columns
+ * n..ld-1 of P are set to zero. */
 int mpx_softmax_fwd(const void* S, void* P, int64_t rows, int64_t n, int64_t ld, float scale,
                     mpx_dtype dt, void* stream);
 
@@ -206,19 +206,27 @@ int mpx_softmax_fwd(const void* S, void* P, int64_t rows, int64_t n, int64_t ld,
 int mpx_softmax_bwd(const void* P, const void* dP, void* dS, int64_t rows, int64_t n,
                     int64_t ld, float scale, mpx_dtype dt, void* stream);
 
+/* Workspace (bytes) for the loss calls over n rows (cross-entropy) or n
+ * elements (MSE): per-row losses or per-block partial sums, overwritten by
+ * every call. */
+size_t mpx_loss_workspace(int64_t n);
+
 /* Mean softmax cross-entropy over B rows of C logits (row stride ldz) with
  * int32 labels, and its cotangent seeded with the loss scale (MPX §3.4: the
  * function output is scaled before differentiation):
  *   *d_loss = mean_b(logsumexp(z_b) - z_b[y_b])          (float32)
- *   dZ = half(scale * (softmax(z) - onehot(y)) / B), scale = d_state->scale. */
+ *   dZ = half(scale * (softmax(z) - onehot(y)) / B), scale = d_state->scale,
+ *   dZ dense [B, C].  The row losses are added in row order (deterministic).
+ * A label outside [0, C) makes the loss NaN (never an out-of-range read). */
 int mpx_cross_entropy(const void* Z, int64_t ldz, const int32_t* labels, int64_t B,
                       int64_t C, const mpx_scale_state* d_state, float* d_loss, void* dZ,
-                      mpx_dtype dt, void* stream);
+                      mpx_dtype dt, void* workspace, size_t ws_bytes, void* stream);
 
 /* Mean squared error over n elements and its scaled cotangent:
  *   *d_loss = mean((y - t)^2);  dY = half(scale * 2 (y - t) / n). */
 int mpx_mse(const void* Y, const void* T, int64_t n, const mpx_scale_state* d_state,
-            float* d_loss, void* dY, mpx_dtype dt, void* stream);
+            float* d_loss, void* dY, mpx_dtype dt, void* workspace, size_t ws_bytes,
+            void* stream);
 
 /* Cast float32 NHWC images [B,H,W,C] to half patch vectors [B*G, p*p*C]
  * (MPX §3.4: inputs cast to half).  Patches row-major over the grid; a

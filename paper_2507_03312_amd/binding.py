@@ -67,8 +67,9 @@ _SIGS = {
     "mpx_layernorm_bwd_workspace": (SZ, [I64, I64]),
     "mpx_softmax_fwd": (C.c_int, [P, P, I64, I64, I64, F, I32, P]),
     "mpx_softmax_bwd": (C.c_int, [P, P, P, I64, I64, I64, F, I32, P]),
-    "mpx_cross_entropy": (C.c_int, [P, I64, P, I64, I64, P, P, P, I32, P]),
-    "mpx_mse": (C.c_int, [P, P, I64, P, P, P, I32, P]),
+    "mpx_loss_workspace": (SZ, [I64]),
+    "mpx_cross_entropy": (C.c_int, [P, I64, P, I64, I64, P, P, P, I32, P, SZ, P]),
+    "mpx_mse": (C.c_int, [P, P, I64, P, P, P, I32, P, SZ, P]),
     "mpx_patchify_cast": (C.c_int, [P, P, I64, I64, I64, I64, I64, I32, P]),
     "mpx_embed_assemble": (C.c_int, [P, P, P, P, I64, I64, I64, I32, P]),
     "mpx_embed_assemble_bwd": (C.c_int, [P, P, P, P, I64, I64, I64, I32, P]),
@@ -172,6 +173,10 @@ mpx_zero = _call("mpx_zero")
 
 def mpx_linear_bwd_workspace(M: int, N: int, K: int) -> int:
     return int(lib.mpx_linear_bwd_workspace(M, N, K))
+
+
+def mpx_loss_workspace(n: int) -> int:
+    return int(lib.mpx_loss_workspace(n))
 
 
 def mpx_layernorm_bwd_workspace(rows: int, d: int) -> int:

@@ -24,7 +24,9 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <utility>
 
+#include "colsum.h"
 #include "common.h"
 
 namespace mpx {
@@ -50,6 +52,18 @@ struct GemmArgs {
   int32_t act;
 };
 
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [0, N).  The
+// accumulator tiles are indexed only with such constants, so they stay in
+// registers (a runtime index would force them into scratch memory).
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
 template <int DT>
 __device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
   if constexpr (DT == MPX_F16) {
@@ -74,9 +88,68 @@ struct TileLoader {
   static_assert(UNITS % NT == 0, "tile does not split evenly over the workgroup");
   uint4 reg[KMAJ ? PER : PER * KR];
 
-  // rows_valid: rows r < rows_valid exist; k_valid: reduction values k < k_valid exist
+  // rows_valid: rows r < rows_valid exist; k_valid: reduction values k < k_valid exist.
+  //
+  // VEC (16-byte aligned base, leading dimension a multiple of 8): every load
+  // is a plain 16-byte load with no branch, so the compiler keeps the next
+  // stage's loads in flight.  A vector that starts inside the matrix lies
+  // wholly inside its row's leading dimension (ld is a multiple of 8 and at
+  // least the row length), so it is loaded whole and its elements past the
+  // end are zeroed; a vector that starts outside is redirected to the tile's
+  // first vector (always inside) and zeroed entirely.
+  __device__ __forceinline__ static uint4 mask_vec(uint4 v, int nvalid) {
+    // keep elements [0, nvalid) of 8, zero the rest
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t lo = 2 * q < nvalid ? 0x0000FFFFu : 0u;
+      const uint32_t hi = 2 * q + 1 < nvalid ? 0xFFFF0000u : 0u;
+      o[q] = w[q] & (lo | hi);
+    }
+    return make_uint4(o[0], o[1], o[2], o[3]);
+  }
+
+  // extent of the tile last loaded (the masking happens in store(), next to
+  // the LDS writes, so that nothing waits on the loads before then)
+  int rv_ = ROWS, kv_ = BK;
+
   __device__ __forceinline__ void load(const uint16_t* __restrict__ base, int64_t ld, int rows_valid,
                                        int k_valid, int tid) {
+    rv_ = rows_valid;
+    kv_ = k_valid;
+    if constexpr (!VEC) {
+      load_guarded(base, ld, rows_valid, k_valid, tid);
+    } else {
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int unit = tid + u * NT;
+        if constexpr (KMAJ) {
+          const int r = unit / (BK / 8);
+          const int k = (unit % (BK / 8)) * 8;
+          const bool inside = r < rows_valid && k < k_valid;
+          const int64_t off = inside ? (int64_t)r * ld + k : 0;
+          reg[u] = *reinterpret_cast<const uint4*>(base + off);
+        } else {
+          const int r = (unit / (BK / KR)) * 8;
+          const int k = (unit % (BK / KR)) * KR;
+#pragma unroll
+          for (int q = 0; q < KR; ++q) {
+            const bool inside = k + q < k_valid && r < rows_valid;
+            const int64_t off = inside ? (int64_t)(k + q) * ld + r : 0;
+            reg[u * KR + q] = *reinterpret_cast<const uint4*>(base + off);
+          }
+        }
+      }
+    }
+  }
+
+  __device__ __forceinline__ void load_guarded(const uint16_t* __restrict__ base, int64_t ld,
+                                               int rows_valid, int k_valid, int tid) {
+    auto pack8 = [](const uint16_t (&h)[8]) {
+      return make_uint4(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16),
+                        h[4] | ((uint32_t)h[5] << 16), h[6] | ((uint32_t)h[7] << 16));
+    };
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int unit = tid + u * NT;
@@ -84,30 +157,20 @@ struct TileLoader {
         const int r = unit / (BK / 8);
         const int k = (unit % (BK / 8)) * 8;
         const uint16_t* p = base + (int64_t)r * ld + k;
-        if (VEC && r < rows_valid && k + 8 <= k_valid) {
-          reg[u] = *reinterpret_cast<const uint4*>(p);
-        } else {
-          uint16_t h[8];
+        uint16_t h[8];
 #pragma unroll
-          for (int j = 0; j < 8; ++j) h[j] = (r < rows_valid && k + j < k_valid) ? p[j] : (uint16_t)0;
-          reg[u] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16),
-                              h[6] | (h[7] << 16));
-        }
+        for (int j = 0; j < 8; ++j) h[j] = (r < rows_valid && k + j < k_valid) ? p[j] : (uint16_t)0;
+        reg[u] = pack8(h);
       } else {
-        const int r = (unit % (ROWS / 8)) * 8;
-        const int k = (unit / (ROWS / 8)) * KR;
+        const int r = (unit / (BK / KR)) * 8;
+        const int k = (unit % (BK / KR)) * KR;
 #pragma unroll
         for (int q = 0; q < KR; ++q) {
           const uint16_t* p = base + (int64_t)(k + q) * ld + r;
-          if (VEC && k + q < k_valid && r + 8 <= rows_valid) {
-            reg[u * KR + q] = *reinterpret_cast<const uint4*>(p);
-          } else {
-            uint16_t h[8];
+          uint16_t h[8];
 #pragma unroll
-            for (int j = 0; j < 8; ++j) h[j] = (k + q < k_valid && r + j < rows_valid) ? p[j] : (uint16_t)0;
-            reg[u * KR + q] = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16),
-                                         h[4] | (h[5] << 16), h[6] | (h[7] << 16));
-          }
+          for (int j = 0; j < 8; ++j) h[j] = (k + q < k_valid && r + j < rows_valid) ? p[j] : (uint16_t)0;
+          reg[u * KR + q] = pack8(h);
         }
       }
     }
@@ -116,25 +179,30 @@ struct TileLoader {
   // LDS tile: ROWS rows of pitch LDSP halves.
   template <int LDSP>
   __device__ __forceinline__ void store(uint16_t* __restrict__ lds, int tid) const {
+    const int rv_ = this->rv_, kv_ = this->kv_;
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
       const int unit = tid + u * NT;
       if constexpr (KMAJ) {
         const int r = unit / (BK / 8);
         const int k = (unit % (BK / 8)) * 8;
-        *reinterpret_cast<uint4*>(lds + r * LDSP + k) = reg[u];
+        uint4 v = reg[u];
+        if (VEC) v = mask_vec(v, r < rv_ && k < kv_ ? min(8, kv_ - k) : 0);
+        *reinterpret_cast<uint4*>(lds + r * LDSP + k) = v;
       } else {
-        const int r = (unit % (ROWS / 8)) * 8;
-        const int k = (unit / (ROWS / 8)) * KR;
+        const int r = (unit / (BK / KR)) * 8;
+        const int k = (unit % (BK / KR)) * KR;
         // register transpose: lane holds rows k..k+KR-1 of 8 consecutive
         // output indices; write output index r+j as KR consecutive k values
         uint32_t w[KR][4];
 #pragma unroll
         for (int q = 0; q < KR; ++q) {
-          w[q][0] = reg[u * KR + q].x;
-          w[q][1] = reg[u * KR + q].y;
-          w[q][2] = reg[u * KR + q].z;
-          w[q][3] = reg[u * KR + q].w;
+          uint4 v = reg[u * KR + q];
+          if (VEC) v = mask_vec(v, k + q < kv_ && r < rv_ ? min(8, rv_ - r) : 0);
+          w[q][0] = v.x;
+          w[q][1] = v.y;
+          w[q][2] = v.z;
+          w[q][3] = v.w;
         }
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
@@ -155,15 +223,21 @@ struct TileLoader {
   }
 };
 
-template <int DT, int BM, int BN, int BK, int WM, int WN, bool AK, bool BKM, bool VEC>
-__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmArgs g) {
+// OCC: waves per SIMD the register budget is sized for.
+template <int DT, int BM, int BN, int BK, int WM, int WN, bool AK, bool BKM, bool VEC, int OCC>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(OCC, OCC)))
+void gemm_kernel(GemmArgs g) {
   constexpr int NW = (BM / WM) * (BN / WN);
   constexpr int NT = NW * 64;
   constexpr int PAD = 8;
   constexpr int LDSP = BK + PAD;
   constexpr int TM = WM / 32, TN = WN / 32;
-  __shared__ __attribute__((aligned(16))) uint16_t sA[2][BM * LDSP];
-  __shared__ __attribute__((aligned(16))) uint16_t sB[2][BN * LDSP];
+  // one LDS block: the double-buffered A and B tiles during the main loop,
+  // then the float32 staging area of the epilogue
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (BM + BN) * LDSP];
+  uint16_t (*sA)[BM * LDSP] = reinterpret_cast<uint16_t (*)[BM * LDSP]>(smem);
+  uint16_t (*sB)[BN * LDSP] = reinterpret_cast<uint16_t (*)[BN * LDSP]>(smem + 2 * BM * LDSP);
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -171,9 +245,14 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   const int wm0 = (wave / (BN / WN)) * WM;
   const int wn0 = (wave % (BN / WN)) * WN;
 
-  // tile coordinates
+  // tile coordinates.  Workgroups are dealt to the 8 XCDs round-robin
+  // (workgroup w runs on XCD w % 8); renumber so that each XCD works through
+  // one contiguous range of row-major tiles, which share A row blocks and the
+  // B operand in that XCD's L2.
   const int64_t tiles_n = (g.N + BN - 1) / BN;
-  const int64_t tile = blockIdx.x;
+  const int64_t ntiles = gridDim.x;
+  const int64_t xcd = blockIdx.x % 8, local = blockIdx.x / 8;
+  const int64_t tile = xcd * (ntiles / 8) + min(xcd, ntiles % 8) + local;
   const int64_t m0 = (tile / tiles_n) * BM;
   const int64_t n0 = (tile % tiles_n) * BN;
   // batch / split
@@ -202,36 +281,37 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
   const int rowsA = (int)min<int64_t>(BM, g.M - m0);
   const int rowsB = (int)min<int64_t>(BN, g.N - n0);
 
+  // One register stage: the loads of k tile kt+1 are issued before the MFMAs
+  // of tile kt and land in LDS (the other buffer) after them.
   TileLoader<BM, BK, NT, AK, VEC> la;
   TileLoader<BN, BK, NT, BKM, VEC> lb;
 
   f32x16 acc[TM][TN];
-#pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j)
+  static_for<TM>([&](auto i) {
+    static_for<TN>([&](auto j) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+    });
+  });
 
+  auto kvalid = [&](int kt) { return (int)min<int64_t>(BK, kend - (kbeg + (int64_t)kt * BK)); };
   if (nk > 0) {
-    la.load(Ab, g.lda, rowsA, (int)min<int64_t>(BK, kend - kbeg), tid);
-    lb.load(Bb, g.ldb, rowsB, (int)min<int64_t>(BK, kend - kbeg), tid);
+    la.load(Ab, g.lda, rowsA, kvalid(0), tid);
+    lb.load(Bb, g.ldb, rowsB, kvalid(0), tid);
     la.template store<LDSP>(sA[0], tid);
     lb.template store<LDSP>(sB[0], tid);
   }
   __syncthreads();
 
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
+    const int c = kt & 1;
     const bool more = kt + 1 < nk;
     if (more) {
-      const int64_t kv = kend - (kbeg + (int64_t)(kt + 1) * BK);
-      const int kval = (int)min<int64_t>(BK, kv);
-      la.load(Ab + (kt + 1) * Astep, g.lda, rowsA, kval, tid);
-      lb.load(Bb + (kt + 1) * Bstep, g.ldb, rowsB, kval, tid);
+      la.load(Ab + (kt + 1) * Astep, g.lda, rowsA, kvalid(kt + 1), tid);
+      lb.load(Bb + (kt + 1) * Bstep, g.ldb, rowsB, kvalid(kt + 1), tid);
     }
-    const uint16_t* a_s = sA[cur];
-    const uint16_t* b_s = sB[cur];
+    const uint16_t* a_s = sA[c];
+    const uint16_t* b_s = sB[c];
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
       const int kofs = kk * 16 + 8 * (lane >> 5);
@@ -242,57 +322,125 @@ __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64) void gemm_kernel(GemmAr
 #pragma unroll
       for (int j = 0; j < TN; ++j)
         bf[j] = *reinterpret_cast<const uint4*>(b_s + (wn0 + j * 32 + (lane & 31)) * LDSP + kofs);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = mfma32<DT>(af[i], bf[j], acc[i][j]);
+      static_for<TM>([&](auto i) {
+        static_for<TN>([&](auto j) { acc[i][j] = mfma32<DT>(af[i], bf[j], acc[i][j]); });
+      });
     }
     if (more) {
-      la.template store<LDSP>(sA[cur ^ 1], tid);
-      lb.template store<LDSP>(sB[cur ^ 1], tid);
+      la.template store<LDSP>(sA[c ^ 1], tid);
+      lb.template store<LDSP>(sB[c ^ 1], tid);
     }
     __syncthreads();
   }
 
   // ---- epilogue ----
-  const int col_l = lane & 31;
-  const int row_l = 4 * (lane >> 5);
+  // The accumulators of a 32x32 block hold, per lane, one column and 4 runs
+  // of 4 consecutive rows.  A 4x4 transpose across each group of 4 lanes
+  // (two butterfly exchanges) turns every run into 4 consecutive columns of
+  // one row, so bias / residual / activation inputs are read and outputs
+  // written 4 elements (8 bytes; 16 for float partials) at a time.
+  const int q4 = lane & 3;
+  const int row_l = 4 * (lane >> 5) + q4;        // row within an 8-row group
+  const int col_l = 4 * ((lane & 31) >> 2);      // first of the lane's 4 columns
+  // exchange (p, p + st) pairs with the lane st apart (st = 1 or 2) through a
+  // DPP quad permutation (lane ^ 1: quad_perm [1,0,3,2]; lane ^ 2: [2,3,0,1])
+  auto xchg = [&](float& lo, float& hi_v, int st) {
+    const bool hi = (q4 & st) != 0;
+    const int send = __builtin_bit_cast(int, hi ? lo : hi_v);
+    const int got = st == 1 ? __builtin_amdgcn_mov_dpp(send, 0xB1, 0xF, 0xF, false)
+                            : __builtin_amdgcn_mov_dpp(send, 0x4E, 0xF, 0xF, false);
+    if (hi) lo = __builtin_bit_cast(float, got);
+    else hi_v = __builtin_bit_cast(float, got);
+  };
+  auto transpose4 = [&](float (&v)[4]) {
+    xchg(v[0], v[1], 1);
+    xchg(v[2], v[3], 1);
+    xchg(v[0], v[2], 2);
+    xchg(v[1], v[3], 2);
+  };
+  auto al8 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; };
   if (g.splits > 1) {
     float* W = g.ws + (int64_t)split * g.M * g.N;
+    const bool v16 = g.N % 4 == 0 && (reinterpret_cast<uintptr_t>(W) & 15u) == 0;
+    static_for<TM>([&](auto i) {
+      static_for<TN>([&](auto j) {
+        const f32x16 a = acc[i][j];
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+        for (int qd = 0; qd < 4; ++qd) {
+          float v[4] = {a[4 * qd], a[4 * qd + 1], a[4 * qd + 2], a[4 * qd + 3]};
+          transpose4(v);
+          const int64_t m = m0 + wm0 + i * 32 + 8 * qd + row_l;
+          const int64_t n = n0 + wn0 + j * 32 + col_l;
+          if (m < g.M && n < g.N) {
+            float* out = W + m * g.N + n;
+            if (v16 && n + 4 <= g.N) *reinterpret_cast<float4*>(out) = make_float4(v[0], v[1], v[2], v[3]);
+            else
 #pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int64_t n = n0 + wn0 + j * 32 + col_l;
-        if (n >= g.N) continue;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int64_t m = m0 + wm0 + i * 32 + 8 * (e >> 2) + row_l + (e & 3);
-          if (m < g.M) W[m * g.N + n] = acc[i][j][e];
+              for (int c = 0; c < 4; ++c)
+                if (n + c < g.N) out[c] = v[c];
+          }
         }
-      }
+      });
+    });
     return;
   }
   uint16_t* C = g.C + offC;
+  const bool v8 = g.ldc % 4 == 0 && al8(C) && (!g.pre || al8(g.pre)) && (!g.dact || al8(g.dact)) &&
+                  (!g.resid || (al8(g.resid) && g.ldr % 4 == 0)) && (!g.bias || al8(g.bias));
+  auto ld4 = [&](const uint16_t* p, bool vec, int nv, uint16_t (&d)[4]) {
+    if (vec) {
+      const uint2 w = *reinterpret_cast<const uint2*>(p);
+      d[0] = (uint16_t)(w.x & 0xFFFFu);
+      d[1] = (uint16_t)(w.x >> 16);
+      d[2] = (uint16_t)(w.y & 0xFFFFu);
+      d[3] = (uint16_t)(w.y >> 16);
+    } else {
 #pragma unroll
-  for (int i = 0; i < TM; ++i)
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int64_t n = n0 + wn0 + j * 32 + col_l;
-      if (n >= g.N) continue;
-      const float bias = g.bias ? h2f<DT>(g.bias[n]) : 0.0f;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int64_t m = m0 + wm0 + i * 32 + 8 * (e >> 2) + row_l + (e & 3);
-        if (m >= g.M) continue;
-        uint16_t h = f2h<DT>(acc[i][j][e] + bias);
-        if (g.pre) g.pre[m * g.ldc + n] = h;
-        if (g.act == MPX_ACT_GELU_TANH) h = f2h<DT>(gelu_tanh(h2f<DT>(h)));
-        if (g.dact) h = f2h<DT>(h2f<DT>(h) * gelu_tanh_grad(h2f<DT>(g.dact[m * g.ldc + n])));
-        if (g.resid) h = f2h<DT>(h2f<DT>(h) + h2f<DT>(g.resid[m * g.ldr + n]));
-        C[m * g.ldc + n] = h;
-      }
+      for (int c = 0; c < 4; ++c) d[c] = c < nv ? p[c] : (uint16_t)0;
     }
+  };
+  auto st4 = [&](uint16_t* p, bool vec, int nv, const uint16_t (&d)[4]) {
+    if (vec) {
+      *reinterpret_cast<uint2*>(p) =
+          make_uint2(d[0] | ((uint32_t)d[1] << 16), d[2] | ((uint32_t)d[3] << 16));
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (c < nv) p[c] = d[c];
+    }
+  };
+  static_for<TM>([&](auto i) {
+    static_for<TN>([&](auto j) {
+      const f32x16 a = acc[i][j];
+      const int64_t n = n0 + wn0 + j * 32 + col_l;
+      const int nv = (int)max<int64_t>(0, min<int64_t>(4, g.N - n));
+      const bool vec = v8 && nv == 4;
+      uint16_t bias[4] = {0, 0, 0, 0};
+      if (g.bias && nv > 0) ld4(g.bias + n, vec, nv, bias);
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        float v[4] = {a[4 * qd], a[4 * qd + 1], a[4 * qd + 2], a[4 * qd + 3]};
+        transpose4(v);
+        const int64_t m = m0 + wm0 + i * 32 + 8 * qd + row_l;
+        if (m >= g.M || nv == 0) continue;
+        uint16_t h[4], da[4], res[4];
+        if (g.dact) ld4(g.dact + m * g.ldc + n, vec, nv, da);
+        if (g.resid) ld4(g.resid + m * g.ldr + n, vec, nv, res);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(v[c] + (g.bias ? h2f<DT>(bias[c]) : 0.0f));
+        if (g.pre) st4(g.pre + m * g.ldc + n, vec, nv, h);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          uint16_t o = h[c];
+          if (g.act == MPX_ACT_GELU_TANH) o = f2h<DT>(gelu_tanh(h2f<DT>(o)));
+          if (g.dact) o = f2h<DT>(h2f<DT>(o) * gelu_tanh_grad(h2f<DT>(da[c])));
+          if (g.resid) o = f2h<DT>(h2f<DT>(o) + h2f<DT>(res[c]));
+          h[c] = o;
+        }
+        st4(C + m * g.ldc + n, vec, nv, h);
+      }
+    });
+  });
 }
 
 // Sum of split-K partials in split order, one rounding: C = half(sum_s W[s]).
@@ -306,36 +454,6 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
   C[i] = f2h<DT>(s);
 }
 
-// Column sums of a half matrix [rows, cols] (dense), float32 accumulation.
-// Phase 1: workgroup (x: 64-column block, y: row slice) -> partial[y][col].
-template <int DT>
-__global__ __launch_bounds__(256) void colsum_partial_kernel(const uint16_t* __restrict__ X, int64_t rows,
-                                                             int64_t cols, int64_t rows_per,
-                                                             float* __restrict__ part) {
-  __shared__ float red[4][64];
-  const int c = threadIdx.x & 63, rl = threadIdx.x >> 6;
-  const int64_t col = (int64_t)blockIdx.x * 64 + c;
-  const int64_t r0 = (int64_t)blockIdx.y * rows_per;
-  const int64_t r1 = min(rows, r0 + rows_per);
-  float s = 0.0f;
-  if (col < cols)
-    for (int64_t r = r0 + rl; r < r1; r += 4) s += h2f<DT>(X[r * cols + col]);
-  red[rl][c] = s;
-  __syncthreads();
-  if (rl == 0 && col < cols)
-    part[(int64_t)blockIdx.y * cols + col] = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
-}
-// Phase 2: out[col] = half(sum_y partial[y][col]) in slice order.
-template <int DT>
-__global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restrict__ part, int nparts,
-                                                           int64_t cols, uint16_t* __restrict__ out) {
-  const int64_t col = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (col >= cols) return;
-  float s = 0.0f;
-  for (int y = 0; y < nparts; ++y) s += part[(int64_t)y * cols + col];
-  out[col] = f2h<DT>(s);
-}
-
 // ------------------------------------------------------------ dispatch --
 
 struct Cfg {
@@ -346,36 +464,66 @@ static bool aligned_vec(const void* p, int64_t ld, int64_t s0, int64_t s1) {
   return (reinterpret_cast<uintptr_t>(p) & 15u) == 0 && ld % 8 == 0 && s0 % 8 == 0 && s1 % 8 == 0;
 }
 
-template <int DT, int BM, int BN, int WM, int WN>
+template <int DT, int BM, int BN, int WM, int WN, int BK = 64, int OCC = 2>
 static hipError_t launch_cfg(const GemmArgs& g, bool ak, bool bk, bool vec, int64_t nbatch,
                              hipStream_t s) {
-  constexpr int BK = 64;
   constexpr int NT = (BM / WM) * (BN / WN) * 64;
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   dim3 grid((unsigned)tiles, (unsigned)(g.splits > 1 ? g.splits : nbatch));
 #define MPX_G(AKv, BKv, VECv) \
-  gemm_kernel<DT, BM, BN, BK, WM, WN, AKv, BKv, VECv><<<grid, NT, 0, s>>>(g)
+  gemm_kernel<DT, BM, BN, BK, WM, WN, AKv, BKv, VECv, OCC><<<grid, NT, 0, s>>>(g)
   if (vec) {
     if (ak && bk) MPX_G(true, true, true);
     else if (ak && !bk) MPX_G(true, false, true);
     else if (!ak && bk) MPX_G(false, true, true);
     else MPX_G(false, false, true);
-  } else {
+  } else if constexpr (BM * BN <= 128 * 128) {  // unaligned operands: small tiles only
     if (ak && bk) MPX_G(true, true, false);
     else if (ak && !bk) MPX_G(true, false, false);
     else if (!ak && bk) MPX_G(false, true, false);
     else MPX_G(false, false, false);
+  } else {
+    return hipErrorInvalidValue;
   }
 #undef MPX_G
   return hipGetLastError();
+}
+
+// Tile configuration for an M x N output: the block tile whose estimated
+// time (rounds of workgroups over the 256 CUs x per-tile work / relative
+// efficiency) is smallest.  Larger tiles reuse each LDS byte over more MFMAs
+// and give each k step more MFMA work to hide memory latency behind.
+struct TileChoice {
+  int bm, bn;
+};
+
+static TileChoice choose_tile(int64_t M, int64_t N, int64_t batches) {
+  if (M <= 64 || N <= 64) return {64, 64};
+  struct C { int bm, bn, per_cu; double eff; };
+  const C cands[] = {{128, 128, 2, 0.55}};
+  TileChoice best{128, 128};
+  double best_t = 1e300;
+  for (const C& c : cands) {
+    const int64_t tiles = ((M + c.bm - 1) / c.bm) * ((N + c.bn - 1) / c.bn) * batches;
+    const int64_t rounds = (tiles + 256 * c.per_cu - 1) / (256 * c.per_cu);
+    const double t = (double)rounds * c.bm * c.bn / c.eff;
+    if (t < best_t) {
+      best_t = t;
+      best = {c.bm, c.bn};
+    }
+  }
+  return best;
 }
 
 // ak: A is k-major; bk: B is k-major.
 template <int DT>
 static hipError_t run_gemm(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipStream_t s) {
   const bool vec = aligned_vec(g.A, g.lda, g.sA0, g.sA1) && aligned_vec(g.B, g.ldb, g.sB0, g.sB1);
-  if (g.M <= 64 || g.N <= 64) return launch_cfg<DT, 64, 64, 32, 32>(g, ak, bk, vec, nbatch, s);
-  return launch_cfg<DT, 128, 128, 64, 64>(g, ak, bk, vec, nbatch, s);
+  const TileChoice t = choose_tile(g.M, g.N, g.splits > 1 ? g.splits : nbatch);
+  if (t.bm == 64) return launch_cfg<DT, 64, 64, 32, 32>(g, ak, bk, vec, nbatch, s);
+  // unaligned operands (rare: odd leading dimensions) use the 128 x 128 tile
+  if (!vec) return launch_cfg<DT, 128, 128, 64, 64>(g, ak, bk, vec, nbatch, s);
+  return launch_cfg<DT, 128, 128, 64, 32, 64, 4>(g, ak, bk, vec, nbatch, s);
 }
 
 static hipError_t gemm_dispatch(mpx_dtype dt, const GemmArgs& g, bool ak, bool bk, int64_t nbatch,
@@ -398,21 +546,6 @@ static int choose_splits(int64_t M, int64_t N, int64_t K) {
   s = std::min<int64_t>(s, 8);
   s = std::min<int64_t>(s, std::max<int64_t>(1, K / 512));
   return (int)std::max<int64_t>(s, 1);
-}
-
-static int64_t colsum_slices(int64_t rows) { return std::max<int64_t>(1, std::min<int64_t>(64, rows / 256)); }
-
-static size_t colsum_ws(int64_t rows, int64_t cols) { return (size_t)colsum_slices(rows) * cols * sizeof(float); }
-
-template <int DT>
-static hipError_t colsum_run(const uint16_t* X, int64_t rows, int64_t cols, float* ws, uint16_t* out,
-                             hipStream_t s) {
-  const int64_t sl = colsum_slices(rows);
-  const int64_t per = (rows + sl - 1) / sl;
-  dim3 g1((unsigned)((cols + 63) / 64), (unsigned)sl);
-  colsum_partial_kernel<DT><<<g1, 256, 0, s>>>(X, rows, cols, per, ws);
-  colsum_final_kernel<DT><<<(unsigned)((cols + 255) / 256), 256, 0, s>>>(ws, (int)sl, cols, out);
-  return hipGetLastError();
 }
 
 }  // namespace mpx
@@ -447,7 +580,7 @@ extern "C" size_t mpx_linear_bwd_workspace(int64_t M, int64_t N, int64_t K) {
   if (M < 1 || N < 1 || K < 1) return 0;
   const int s = choose_splits(N, K, M);
   size_t ws = s > 1 ? (size_t)s * N * K * sizeof(float) : 0;
-  return std::max(ws, colsum_ws(M, N)) + 256;
+  return std::max(ws, colsum_workspace(M, N)) + 256;
 }
 
 extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, const void* Xpre,

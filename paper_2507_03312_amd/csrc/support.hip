@@ -7,44 +7,54 @@
 
 #include <algorithm>
 
+#include "colsum.h"
 #include "common.h"
 
 namespace mpx {
 
 constexpr float kLnEps = 1e-5f;
-constexpr int kMaxRowVec = 4;  // LayerNorm rows up to 4 * 64 * 8 = 2048 columns
 
-// Row access helpers: lane `lane` owns columns lane*8 + v*512 + j.
-template <int DT>
+// ------------------------------------------------------------- LayerNorm --
+//
+// One wave per row, R rows per wave with all their loads issued before any
+// reduction (memory parallelism), VPL 8-element vectors per lane (a row of up
+// to 512 * VPL columns).  Lane `lane` owns columns v*512 + lane*8 + j.
+
+template <int VPL>
+struct RowVec {
+  float x[VPL][8];
+};
+
+template <int DT, int VPL>
 __device__ __forceinline__ void load_row(const uint16_t* __restrict__ row, int64_t d, int lane,
-                                         float (&x)[kMaxRowVec][8]) {
+                                         RowVec<VPL>& r) {
 #pragma unroll
-  for (int v = 0; v < kMaxRowVec; ++v) {
-    const int64_t c = (int64_t)lane * 8 + v * 512;
+  for (int v = 0; v < VPL; ++v) {
+    const int64_t c = (int64_t)v * 512 + lane * 8;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) x[v][j] = 0.0f;
+    for (int j = 0; j < 8; ++j) r.x[v][j] = 0.0f;
     if (c + 8 <= d && (reinterpret_cast<uintptr_t>(row + c) & 15u) == 0) {
-      uint4 u = *reinterpret_cast<const uint4*>(row + c);
+      const uint4 u = *reinterpret_cast<const uint4*>(row + c);
       const uint32_t w[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        x[v][2 * j] = h2f<DT>((uint16_t)(w[j] & 0xFFFFu));
-        x[v][2 * j + 1] = h2f<DT>((uint16_t)(w[j] >> 16));
+        r.x[v][2 * j] = h2f<DT>((uint16_t)(w[j] & 0xFFFFu));
+        r.x[v][2 * j + 1] = h2f<DT>((uint16_t)(w[j] >> 16));
       }
     } else {
 #pragma unroll
       for (int j = 0; j < 8; ++j)
-        if (c + j < d) x[v][j] = h2f<DT>(row[c + j]);
+        if (c + j < d) r.x[v][j] = h2f<DT>(row[c + j]);
     }
   }
 }
 
-template <int DT>
+template <int DT, int VPL>
 __device__ __forceinline__ void store_row(uint16_t* __restrict__ row, int64_t d, int lane,
-                                          const uint16_t (&h)[kMaxRowVec][8]) {
+                                          const uint16_t (&h)[VPL][8]) {
 #pragma unroll
-  for (int v = 0; v < kMaxRowVec; ++v) {
-    const int64_t c = (int64_t)lane * 8 + v * 512;
+  for (int v = 0; v < VPL; ++v) {
+    const int64_t c = (int64_t)v * 512 + lane * 8;
     if (c + 8 <= d && (reinterpret_cast<uintptr_t>(row + c) & 15u) == 0) {
       *reinterpret_cast<uint4*>(row + c) =
           make_uint4(h[v][0] | ((uint32_t)h[v][1] << 16), h[v][2] | ((uint32_t)h[v][3] << 16),
@@ -58,12 +68,33 @@ __device__ __forceinline__ void store_row(uint16_t* __restrict__ row, int64_t d,
 }
 
 __device__ __forceinline__ bool col_ok(int64_t d, int lane, int v, int j) {
-  return (int64_t)lane * 8 + v * 512 + j < d;
+  return (int64_t)v * 512 + lane * 8 + j < d;
 }
 
-// ------------------------------------------------------------- LayerNorm --
+// mean and 1/sqrt(var + eps) of one row held by a wave (two-pass)
+template <int VPL>
+__device__ __forceinline__ void row_stats(const RowVec<VPL>& r, int64_t d, int lane, float& mean,
+                                          float& rstd) {
+  float s = 0.0f;
+#pragma unroll
+  for (int v = 0; v < VPL; ++v)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) s += r.x[v][j];
+  mean = wave_sum(s) / (float)d;
+  float q = 0.0f;
+#pragma unroll
+  for (int v = 0; v < VPL; ++v)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float c = col_ok(d, lane, v, j) ? r.x[v][j] - mean : 0.0f;
+      q += c * c;
+    }
+  rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + kLnEps);
+}
 
-template <int DT>
+constexpr int kLnRows = 2;  // rows per wave
+
+template <int DT, int VPL>
 __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const uint16_t* __restrict__ X, int64_t ldx,
                                                             const uint16_t* __restrict__ gamma,
                                                             const uint16_t* __restrict__ beta,
@@ -71,113 +102,99 @@ __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const uint16_t* __re
                                                             float* __restrict__ mr, int64_t rows,
                                                             int64_t d) {
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= rows) return;
-  float x[kMaxRowVec][8];
-  load_row<DT>(X + r * ldx, d, lane, x);
-  float s = 0.0f;
+  const int64_t r0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * kLnRows;
+  RowVec<VPL> x[kLnRows];
 #pragma unroll
-  for (int v = 0; v < kMaxRowVec; ++v)
+  for (int i = 0; i < kLnRows; ++i)
+    if (r0 + i < rows) load_row<DT, VPL>(X + (r0 + i) * ldx, d, lane, x[i]);
+  RowVec<VPL> g, b;
+  load_row<DT, VPL>(gamma, d, lane, g);
+  load_row<DT, VPL>(beta, d, lane, b);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) s += x[v][j];
-  const float mean = wave_sum(s) / (float)d;
-  float q = 0.0f;
+  for (int i = 0; i < kLnRows; ++i) {
+    if (r0 + i >= rows) break;
+    float mean, rstd;
+    row_stats<VPL>(x[i], d, lane, mean, rstd);
+    uint16_t h[VPL][8];
 #pragma unroll
-  for (int v = 0; v < kMaxRowVec; ++v)
+    for (int v = 0; v < VPL; ++v)
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (col_ok(d, lane, v, j)) {
-        const float c = x[v][j] - mean;
-        q += c * c;
-      }
-  const float var = wave_sum(q) / (float)d;
-  const float rstd = 1.0f / sqrtf(var + kLnEps);
-  float g[kMaxRowVec][8], b[kMaxRowVec][8];
-  load_row<DT>(gamma, d, lane, g);
-  load_row<DT>(beta, d, lane, b);
-  uint16_t h[kMaxRowVec][8];
-#pragma unroll
-  for (int v = 0; v < kMaxRowVec; ++v)
-#pragma unroll
-    for (int j = 0; j < 8; ++j) h[v][j] = f2h<DT>((x[v][j] - mean) * rstd * g[v][j] + b[v][j]);
-  store_row<DT>(Y + r * d, d, lane, h);
-  if (mr && lane == 0) {
-    mr[2 * r] = mean;
-    mr[2 * r + 1] = rstd;
+      for (int j = 0; j < 8; ++j) h[v][j] = f2h<DT>((x[i].x[v][j] - mean) * rstd * g.x[v][j] + b.x[v][j]);
+    store_row<DT, VPL>(Y + (r0 + i) * d, d, lane, h);
+    if (mr && lane == 0) {
+      mr[2 * (r0 + i)] = mean;
+      mr[2 * (r0 + i) + 1] = rstd;
+    }
   }
 }
 
-// dX for each row; per-workgroup column partials of dgamma (sum dy*xhat) and
-// dbeta (sum dy) into part[blockIdx][2][d].
-template <int DT>
+// dX for each row (optionally plus a residual cotangent), and per-workgroup
+// column partials of dgamma (sum dy*xhat) and dbeta (sum dy) into
+// part[blockIdx][0:d] and part[blockIdx][d:2d].
+template <int DT, int VPL>
 __global__ __launch_bounds__(256) void layernorm_bwd_kernel(
     const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __restrict__ gamma,
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ Rg, uint16_t* __restrict__ dX,
     int64_t ldo, int64_t rows, int64_t d, float* __restrict__ part) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  float g[kMaxRowVec][8];
-  load_row<DT>(gamma, d, lane, g);
-  float pg[kMaxRowVec][8], pb[kMaxRowVec][8];
+  RowVec<VPL> g;
+  load_row<DT, VPL>(gamma, d, lane, g);
+  float pg[VPL][8], pb[VPL][8];
 #pragma unroll
-  for (int v = 0; v < kMaxRowVec; ++v)
+  for (int v = 0; v < VPL; ++v)
 #pragma unroll
     for (int j = 0; j < 8; ++j) pg[v][j] = pb[v][j] = 0.0f;
 
-  for (int64_t r = (int64_t)blockIdx.x * 4 + wave; r < rows; r += (int64_t)gridDim.x * 4) {
-    float x[kMaxRowVec][8], dy[kMaxRowVec][8];
-    load_row<DT>(X + r * ldx, d, lane, x);
-    load_row<DT>(dY + r * d, d, lane, dy);
-    float s = 0.0f;
+  for (int64_t r = ((int64_t)blockIdx.x * 4 + wave) * kLnRows; r < rows;
+       r += (int64_t)gridDim.x * 4 * kLnRows) {
+    RowVec<VPL> x[kLnRows], dy[kLnRows];
 #pragma unroll
-    for (int v = 0; v < kMaxRowVec; ++v)
+    for (int i = 0; i < kLnRows; ++i)
+      if (r + i < rows) {
+        load_row<DT, VPL>(X + (r + i) * ldx, d, lane, x[i]);
+        load_row<DT, VPL>(dY + (r + i) * d, d, lane, dy[i]);
+      }
 #pragma unroll
-      for (int j = 0; j < 8; ++j) s += x[v][j];
-    const float mean = wave_sum(s) / (float)d;
-    float q = 0.0f;
+    for (int i = 0; i < kLnRows; ++i) {
+      if (r + i >= rows) break;
+      float mean, rstd;
+      row_stats<VPL>(x[i], d, lane, mean, rstd);
+      float s1 = 0.0f, s2 = 0.0f;
 #pragma unroll
-    for (int v = 0; v < kMaxRowVec; ++v)
+      for (int v = 0; v < VPL; ++v)
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
-        if (col_ok(d, lane, v, j)) {
-          const float c = x[v][j] - mean;
-          q += c * c;
+        for (int j = 0; j < 8; ++j) {
+          const float xh = col_ok(d, lane, v, j) ? (x[i].x[v][j] - mean) * rstd : 0.0f;
+          x[i].x[v][j] = xh;
+          const float dxh = dy[i].x[v][j] * g.x[v][j];
+          s1 += dxh;
+          s2 += dxh * xh;
+          pg[v][j] += dy[i].x[v][j] * xh;
+          pb[v][j] += dy[i].x[v][j];
         }
-    const float rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + kLnEps);
-    float s1 = 0.0f, s2 = 0.0f;
+      s1 = wave_sum(s1) / (float)d;
+      s2 = wave_sum(s2) / (float)d;
+      RowVec<VPL> rg;
+      if (Rg) load_row<DT, VPL>(Rg + (r + i) * ldo, d, lane, rg);
+      uint16_t h[VPL][8];
 #pragma unroll
-    for (int v = 0; v < kMaxRowVec; ++v)
+      for (int v = 0; v < VPL; ++v)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float xh = col_ok(d, lane, v, j) ? (x[v][j] - mean) * rstd : 0.0f;
-        x[v][j] = xh;
-        const float dxh = dy[v][j] * g[v][j];
-        s1 += dxh;
-        s2 += dxh * xh;
-        pg[v][j] += dy[v][j] * xh;
-        pb[v][j] += dy[v][j];
-      }
-    s1 = wave_sum(s1) / (float)d;
-    s2 = wave_sum(s2) / (float)d;
-    float rg[kMaxRowVec][8];
-    if (Rg) load_row<DT>(Rg + r * ldo, d, lane, rg);
-    uint16_t h[kMaxRowVec][8];
-#pragma unroll
-    for (int v = 0; v < kMaxRowVec; ++v)
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float dx = rstd * (dy[v][j] * g[v][j] - s1 - x[v][j] * s2);
-        uint16_t o = f2h<DT>(dx);
-        if (Rg) o = f2h<DT>(rg[v][j] + h2f<DT>(o));
-        h[v][j] = o;
-      }
-    store_row<DT>(dX + r * ldo, d, lane, h);
+        for (int j = 0; j < 8; ++j) {
+          const float dx = rstd * (dy[i].x[v][j] * g.x[v][j] - s1 - x[i].x[v][j] * s2);
+          uint16_t o = f2h<DT>(dx);
+          if (Rg) o = f2h<DT>(rg.x[v][j] + h2f<DT>(o));
+          h[v][j] = o;
+        }
+      store_row<DT, VPL>(dX + (r + i) * ldo, d, lane, h);
+    }
   }
-  // reduce the 4 waves' column partials through LDS, then write this block's
+  // the 4 waves' column partials, combined in wave order through LDS
   __shared__ float red[4][2][512];
   float* out = part + (int64_t)blockIdx.x * 2 * d;
 #pragma unroll
-  for (int v = 0; v < kMaxRowVec; ++v) {
+  for (int v = 0; v < VPL; ++v) {
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
@@ -187,7 +204,7 @@ __global__ __launch_bounds__(256) void layernorm_bwd_kernel(
     __syncthreads();
     for (int i = threadIdx.x; i < 1024; i += 256) {
       const int which = i >> 9, c = i & 511;
-      const int64_t col = (int64_t)(c >> 3) * 8 + v * 512 + (c & 7);
+      const int64_t col = (int64_t)v * 512 + c;
       if (col < d)
         out[which * d + col] =
             ((red[0][which][c] + red[1][which][c]) + red[2][which][c]) + red[3][which][c];
@@ -195,116 +212,177 @@ __global__ __launch_bounds__(256) void layernorm_bwd_kernel(
   }
 }
 
-template <int DT>
-__global__ __launch_bounds__(256) void layernorm_bwd_final_kernel(const float* __restrict__ part,
-                                                                  int nparts, int64_t d,
-                                                                  uint16_t* __restrict__ dg,
-                                                                  uint16_t* __restrict__ db) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= 2 * d) return;
-  const int which = (int)(i / d);
-  const int64_t col = i % d;
-  float s = 0.0f;
-  for (int p = 0; p < nparts; ++p) s += part[(int64_t)p * 2 * d + which * d + col];
-  (which ? db : dg)[col] = f2h<DT>(s);
+static int ln_bwd_blocks(int64_t rows) {
+  return (int)std::max<int64_t>(1, std::min<int64_t>((rows + 4 * kLnRows - 1) / (4 * kLnRows), 480));
 }
 
-static int ln_bwd_blocks(int64_t rows) { return (int)std::min<int64_t>((rows + 3) / 4, 512); }
-
 // --------------------------------------------------------------- softmax --
+//
+// One wave per row, SM_ROWS rows per wave loaded before any reduction; a row
+// of up to 64 * SM_VPL values is held in registers (lane owns c = lane + 64 i).
 
-template <int DT>
+constexpr int kSmRows = 4;
+
+template <int DT, int VPL>
 __global__ __launch_bounds__(256) void softmax_fwd_kernel(const uint16_t* __restrict__ S,
                                                           uint16_t* __restrict__ P, int64_t rows,
                                                           int64_t n, int64_t ld, float scale) {
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= rows) return;
-  const uint16_t* s = S + r * ld;
-  uint16_t* p = P + r * ld;
-  float mx = -INFINITY;
-  for (int64_t c = lane; c < n; c += 64) mx = fmaxf(mx, scale * h2f<DT>(s[c]));
-  mx = wave_max(mx);
-  float sum = 0.0f;
-  for (int64_t c = lane; c < n; c += 64) sum += expf(scale * h2f<DT>(s[c]) - mx);
-  sum = wave_sum(sum);
-  const float inv = 1.0f / sum;
-  for (int64_t c = lane; c < ld; c += 64)
-    p[c] = c < n ? f2h<DT>(expf(scale * h2f<DT>(s[c]) - mx) * inv) : (uint16_t)0;
+  const int64_t r0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * kSmRows;
+  float z[kSmRows][VPL];
+#pragma unroll
+  for (int i = 0; i < kSmRows; ++i)
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) {
+      const int64_t c = lane + 64 * k;
+      z[i][k] = (r0 + i < rows && c < n) ? scale * h2f<DT>(S[(r0 + i) * ld + c]) : -INFINITY;
+    }
+#pragma unroll
+  for (int i = 0; i < kSmRows; ++i) {
+    if (r0 + i >= rows) break;
+    float mx = z[i][0];
+#pragma unroll
+    for (int k = 1; k < VPL; ++k) mx = fmaxf(mx, z[i][k]);
+    mx = wave_max(mx);
+    float e[VPL], sum = 0.0f;
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) {
+      e[k] = lane + 64 * k < n ? expf(z[i][k] - mx) : 0.0f;
+      sum += e[k];
+    }
+    const float inv = 1.0f / wave_sum(sum);
+    uint16_t* p = P + (r0 + i) * ld;
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) {
+      const int64_t c = lane + 64 * k;
+      if (c < ld) p[c] = c < n ? f2h<DT>(e[k] * inv) : (uint16_t)0;
+    }
+    for (int64_t c = lane + 64 * VPL; c < ld; c += 64) p[c] = 0;
+  }
 }
 
-template <int DT>
+template <int DT, int VPL>
 __global__ __launch_bounds__(256) void softmax_bwd_kernel(const uint16_t* __restrict__ P,
                                                           const uint16_t* __restrict__ dP,
                                                           uint16_t* __restrict__ dS, int64_t rows,
                                                           int64_t n, int64_t ld, float scale) {
   const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= rows) return;
-  const uint16_t* p = P + r * ld;
-  const uint16_t* dp = dP + r * ld;
-  uint16_t* ds = dS + r * ld;
-  float dot = 0.0f;
-  for (int64_t c = lane; c < n; c += 64) dot += h2f<DT>(dp[c]) * h2f<DT>(p[c]);
-  dot = wave_sum(dot);
-  for (int64_t c = lane; c < ld; c += 64)
-    ds[c] = c < n ? f2h<DT>(scale * h2f<DT>(p[c]) * (h2f<DT>(dp[c]) - dot)) : (uint16_t)0;
+  const int64_t r0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * kSmRows;
+  float pv[kSmRows][VPL], dv[kSmRows][VPL];
+#pragma unroll
+  for (int i = 0; i < kSmRows; ++i)
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) {
+      const int64_t c = lane + 64 * k;
+      const bool ok = r0 + i < rows && c < n;
+      pv[i][k] = ok ? h2f<DT>(P[(r0 + i) * ld + c]) : 0.0f;
+      dv[i][k] = ok ? h2f<DT>(dP[(r0 + i) * ld + c]) : 0.0f;
+    }
+#pragma unroll
+  for (int i = 0; i < kSmRows; ++i) {
+    if (r0 + i >= rows) break;
+    float dot = 0.0f;
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) dot += dv[i][k] * pv[i][k];
+    dot = wave_sum(dot);
+    uint16_t* ds = dS + (r0 + i) * ld;
+#pragma unroll
+    for (int k = 0; k < VPL; ++k) {
+      const int64_t c = lane + 64 * k;
+      if (c < ld) ds[c] = c < n ? f2h<DT>(scale * pv[i][k] * (dv[i][k] - dot)) : (uint16_t)0;
+    }
+    for (int64_t c = lane + 64 * VPL; c < ld; c += 64) ds[c] = 0;
+  }
 }
 
 // ----------------------------------------------------------------- losses --
 
-// One workgroup; wave w handles rows w, w+4, ...; losses summed in row order
-// per wave, then across waves in wave order.
+// One wave per row: the row's loss goes to rowloss[b]; dZ is seeded with the
+// loss scale.  A second one-workgroup kernel adds the row losses in order.
 template <int DT>
 __global__ __launch_bounds__(256) void cross_entropy_kernel(const uint16_t* __restrict__ Z, int64_t ldz,
                                                             const int32_t* __restrict__ labels,
                                                             int64_t B, int64_t C,
                                                             const mpx_scale_state* __restrict__ st,
-                                                            float* __restrict__ loss,
+                                                            float* __restrict__ rowloss,
                                                             uint16_t* __restrict__ dZ) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int64_t b = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (b >= B) return;
   const float scale = st->scale;
-  float acc = 0.0f;
-  for (int64_t b = wave; b < B; b += 4) {
-    const uint16_t* z = Z + b * ldz;
-    const int32_t y = labels[b];
-    float mx = -INFINITY;
-    for (int64_t c = lane; c < C; c += 64) mx = fmaxf(mx, h2f<DT>(z[c]));
-    mx = wave_max(mx);
-    float se = 0.0f;
-    for (int64_t c = lane; c < C; c += 64) se += expf(h2f<DT>(z[c]) - mx);
-    se = wave_sum(se);
-    const float lse = logf(se);
-    const bool ok = y >= 0 && y < C;  // an out-of-range label gives a NaN loss, never a read
-    acc += ok ? lse - (h2f<DT>(z[y]) - mx) : NAN;
-    const float k = scale / (float)B;
-    for (int64_t c = lane; c < C; c += 64) {
-      const float pr = expf(h2f<DT>(z[c]) - mx) / se;
-      dZ[b * C + c] = f2h<DT>(k * (pr - (c == y ? 1.0f : 0.0f)));
-    }
+  const uint16_t* z = Z + b * ldz;
+  const int32_t y = labels[b];
+  float mx = -INFINITY;
+  for (int64_t c = lane; c < C; c += 64) mx = fmaxf(mx, h2f<DT>(z[c]));
+  mx = wave_max(mx);
+  float se = 0.0f;
+  for (int64_t c = lane; c < C; c += 64) se += expf(h2f<DT>(z[c]) - mx);
+  se = wave_sum(se);
+  const float k = scale / (float)B;
+  for (int64_t c = lane; c < C; c += 64) {
+    const float pr = expf(h2f<DT>(z[c]) - mx) / se;
+    dZ[b * C + c] = f2h<DT>(k * (pr - (c == y ? 1.0f : 0.0f)));
   }
-  __shared__ float part[4];
-  if (lane == 0) part[wave] = acc;
-  __syncthreads();
-  if (threadIdx.x == 0) *loss = (((part[0] + part[1]) + part[2]) + part[3]) / (float)B;
+  if (lane == 0) {
+    const bool ok = y >= 0 && y < C;  // an out-of-range label gives a NaN loss, never a read
+    rowloss[b] = ok ? logf(se) - (h2f<DT>(z[y]) - mx) : NAN;
+  }
 }
+
+// *loss = (sum of vals[0..n)) / n, summed in a fixed order by one workgroup.
+__global__ __launch_bounds__(256) void mean_kernel(const float* __restrict__ vals, int64_t n,
+                                                   float* __restrict__ loss) {
+  __shared__ float red[256];
+  float s = 0.0f;
+  for (int64_t i = threadIdx.x; i < n; i += 256) s += vals[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *loss = red[0] / (float)n;
+}
+
+// Squared errors of 2048-element blocks into part[block]; dY seeded with the scale.
+constexpr int kMseBlock = 2048;
 
 template <int DT>
 __global__ __launch_bounds__(256) void mse_kernel(const uint16_t* __restrict__ Y, const uint16_t* __restrict__ T,
                                                   int64_t n, const mpx_scale_state* __restrict__ st,
-                                                  float* __restrict__ loss, uint16_t* __restrict__ dY) {
+                                                  float* __restrict__ part, uint16_t* __restrict__ dY) {
   const float k = 2.0f * st->scale / (float)n;
   float acc = 0.0f;
-  for (int64_t i = threadIdx.x; i < n; i += 256) {
-    const float df = h2f<DT>(Y[i]) - h2f<DT>(T[i]);
-    acc += df * df;
-    dY[i] = f2h<DT>(k * df);
+  const int64_t base = (int64_t)blockIdx.x * kMseBlock;
+#pragma unroll
+  for (int u = 0; u < kMseBlock / 256; ++u) {
+    const int64_t i = base + u * 256 + threadIdx.x;
+    if (i < n) {
+      const float df = h2f<DT>(Y[i]) - h2f<DT>(T[i]);
+      acc += df * df;
+      dY[i] = f2h<DT>(k * df);
+    }
   }
-  __shared__ float part[4];
+  __shared__ float red[4];
   acc = wave_sum(acc);
-  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
   __syncthreads();
-  if (threadIdx.x == 0) *loss = (((part[0] + part[1]) + part[2]) + part[3]) / (float)n;
+  if (threadIdx.x == 0) part[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
+}
+
+// sum of squared errors over blocks, divided by n
+__global__ __launch_bounds__(256) void mse_final_kernel(const float* __restrict__ part, int64_t nb,
+                                                        int64_t n, float* __restrict__ loss) {
+  __shared__ float red[256];
+  float s = 0.0f;
+  for (int64_t i = threadIdx.x; i < nb; i += 256) s += part[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *loss = red[0] / (float)n;
 }
 
 // ------------------------------------------------------------ embeddings --
@@ -387,6 +465,26 @@ using namespace mpx;
     MPX_LAUNCHED();                                                                   \
   } while (0)
 
+static int vpl_for(int64_t d) { return d <= 512 ? 1 : d <= 1024 ? 2 : 4; }
+
+template <int DT>
+static void ln_fwd_launch(int vpl, unsigned grid, hipStream_t s, const uint16_t* X, int64_t ldx,
+                          const uint16_t* g, const uint16_t* b, uint16_t* Y, float* mr, int64_t rows,
+                          int64_t d) {
+  if (vpl == 1) layernorm_fwd_kernel<DT, 1><<<grid, 256, 0, s>>>(X, ldx, g, b, Y, mr, rows, d);
+  else if (vpl == 2) layernorm_fwd_kernel<DT, 2><<<grid, 256, 0, s>>>(X, ldx, g, b, Y, mr, rows, d);
+  else layernorm_fwd_kernel<DT, 4><<<grid, 256, 0, s>>>(X, ldx, g, b, Y, mr, rows, d);
+}
+
+template <int DT>
+static void ln_bwd_launch(int vpl, unsigned grid, hipStream_t s, const uint16_t* X, int64_t ldx,
+                          const uint16_t* g, const uint16_t* dY, const uint16_t* Rg, uint16_t* dX,
+                          int64_t ldo, int64_t rows, int64_t d, float* part) {
+  if (vpl == 1) layernorm_bwd_kernel<DT, 1><<<grid, 256, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part);
+  else if (vpl == 2) layernorm_bwd_kernel<DT, 2><<<grid, 256, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part);
+  else layernorm_bwd_kernel<DT, 4><<<grid, 256, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part);
+}
+
 extern "C" int mpx_layernorm_fwd(const void* X, int64_t ldx, const void* gamma, const void* beta,
                                  void* Y, float* mean_rstd, int64_t rows, int64_t d, mpx_dtype dt,
                                  void* stream) {
@@ -394,9 +492,15 @@ extern "C" int mpx_layernorm_fwd(const void* X, int64_t ldx, const void* gamma, 
   MPX_REQUIRE(X && gamma && beta && Y, "NULL argument");
   MPX_REQUIRE(rows >= 1 && d >= 1 && d <= 2048 && ldx >= d, "bad sizes (1 <= d <= 2048, ldx >= d)");
   MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
-  MPX_DT_DISPATCH(dt, layernorm_fwd_kernel, (unsigned)((rows + 3) / 4), 256, stream,
-                  (const uint16_t*)X, ldx, (const uint16_t*)gamma, (const uint16_t*)beta,
-                  (uint16_t*)Y, mean_rstd, rows, d);
+  const unsigned grid = (unsigned)((rows + 4 * kLnRows - 1) / (4 * kLnRows));
+  hipStream_t s = (hipStream_t)stream;
+  if (dt == MPX_F16)
+    ln_fwd_launch<MPX_F16>(vpl_for(d), grid, s, (const uint16_t*)X, ldx, (const uint16_t*)gamma,
+                           (const uint16_t*)beta, (uint16_t*)Y, mean_rstd, rows, d);
+  else
+    ln_fwd_launch<MPX_BF16>(vpl_for(d), grid, s, (const uint16_t*)X, ldx, (const uint16_t*)gamma,
+                            (const uint16_t*)beta, (uint16_t*)Y, mean_rstd, rows, d);
+  MPX_LAUNCHED();
   return MPX_OK;
 }
 
@@ -419,22 +523,55 @@ extern "C" int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, 
     return MPX_ERR_WORKSPACE;
   }
   const int nb = ln_bwd_blocks(rows);
-  MPX_DT_DISPATCH(dt, layernorm_bwd_kernel, (unsigned)nb, 256, stream, (const uint16_t*)X, ldx,
-                  (const uint16_t*)gamma, (const uint16_t*)dY, (const uint16_t*)Rgrad,
-                  (uint16_t*)dX, ldo, rows, d, (float*)workspace);
-  MPX_DT_DISPATCH(dt, layernorm_bwd_final_kernel, (unsigned)((2 * d + 255) / 256), 256, stream,
-                  (const float*)workspace, nb, d, (uint16_t*)dgamma, (uint16_t*)dbeta);
+  hipStream_t s = (hipStream_t)stream;
+  float* part = (float*)workspace;
+  const unsigned fin = (unsigned)((2 * d + 63) / 64);
+  if (dt == MPX_F16) {
+    ln_bwd_launch<MPX_F16>(vpl_for(d), (unsigned)nb, s, (const uint16_t*)X, ldx, (const uint16_t*)gamma,
+                           (const uint16_t*)dY, (const uint16_t*)Rgrad, (uint16_t*)dX, ldo, rows, d, part);
+    colsum_final_kernel<MPX_F16><<<fin, 256, 0, s>>>(part, nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d);
+  } else {
+    ln_bwd_launch<MPX_BF16>(vpl_for(d), (unsigned)nb, s, (const uint16_t*)X, ldx, (const uint16_t*)gamma,
+                            (const uint16_t*)dY, (const uint16_t*)Rgrad, (uint16_t*)dX, ldo, rows, d, part);
+    colsum_final_kernel<MPX_BF16><<<fin, 256, 0, s>>>(part, nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d);
+  }
+  MPX_LAUNCHED();
   return MPX_OK;
 }
+
+template <int DT>
+static void softmax_launch(bool bwd, int vpl, unsigned grid, hipStream_t s, const uint16_t* A,
+                           const uint16_t* Bp, uint16_t* O, int64_t rows, int64_t n, int64_t ld,
+                           float scale) {
+  if (!bwd) {
+    if (vpl == 1) softmax_fwd_kernel<DT, 1><<<grid, 256, 0, s>>>(A, O, rows, n, ld, scale);
+    else if (vpl == 2) softmax_fwd_kernel<DT, 2><<<grid, 256, 0, s>>>(A, O, rows, n, ld, scale);
+    else if (vpl == 4) softmax_fwd_kernel<DT, 4><<<grid, 256, 0, s>>>(A, O, rows, n, ld, scale);
+    else softmax_fwd_kernel<DT, 16><<<grid, 256, 0, s>>>(A, O, rows, n, ld, scale);
+  } else {
+    if (vpl == 1) softmax_bwd_kernel<DT, 1><<<grid, 256, 0, s>>>(A, Bp, O, rows, n, ld, scale);
+    else if (vpl == 2) softmax_bwd_kernel<DT, 2><<<grid, 256, 0, s>>>(A, Bp, O, rows, n, ld, scale);
+    else if (vpl == 4) softmax_bwd_kernel<DT, 4><<<grid, 256, 0, s>>>(A, Bp, O, rows, n, ld, scale);
+    else softmax_bwd_kernel<DT, 16><<<grid, 256, 0, s>>>(A, Bp, O, rows, n, ld, scale);
+  }
+}
+
+static int sm_vpl(int64_t n) { return n <= 64 ? 1 : n <= 128 ? 2 : n <= 256 ? 4 : 16; }
 
 extern "C" int mpx_softmax_fwd(const void* S, void* P, int64_t rows, int64_t n, int64_t ld, float scale,
                                mpx_dtype dt, void* stream) {
   clear_error();
   MPX_REQUIRE(S && P, "NULL argument");
-  MPX_REQUIRE(rows >= 1 && n >= 1 && ld >= n, "bad sizes");
+  MPX_REQUIRE(rows >= 1 && n >= 1 && n <= 1024 && ld >= n, "bad sizes (1 <= n <= 1024, ld >= n)");
   MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
-  MPX_DT_DISPATCH(dt, softmax_fwd_kernel, (unsigned)((rows + 3) / 4), 256, stream,
-                  (const uint16_t*)S, (uint16_t*)P, rows, n, ld, scale);
+  const unsigned grid = (unsigned)((rows + 4 * kSmRows - 1) / (4 * kSmRows));
+  if (dt == MPX_F16)
+    softmax_launch<MPX_F16>(false, sm_vpl(n), grid, (hipStream_t)stream, (const uint16_t*)S, nullptr,
+                            (uint16_t*)P, rows, n, ld, scale);
+  else
+    softmax_launch<MPX_BF16>(false, sm_vpl(n), grid, (hipStream_t)stream, (const uint16_t*)S, nullptr,
+                             (uint16_t*)P, rows, n, ld, scale);
+  MPX_LAUNCHED();
   return MPX_OK;
 }
 
@@ -442,33 +579,58 @@ extern "C" int mpx_softmax_bwd(const void* P, const void* dP, void* dS, int64_t 
                                int64_t ld, float scale, mpx_dtype dt, void* stream) {
   clear_error();
   MPX_REQUIRE(P && dP && dS, "NULL argument");
-  MPX_REQUIRE(rows >= 1 && n >= 1 && ld >= n, "bad sizes");
+  MPX_REQUIRE(rows >= 1 && n >= 1 && n <= 1024 && ld >= n, "bad sizes (1 <= n <= 1024, ld >= n)");
   MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
-  MPX_DT_DISPATCH(dt, softmax_bwd_kernel, (unsigned)((rows + 3) / 4), 256, stream,
-                  (const uint16_t*)P, (const uint16_t*)dP, (uint16_t*)dS, rows, n, ld, scale);
+  const unsigned grid = (unsigned)((rows + 4 * kSmRows - 1) / (4 * kSmRows));
+  if (dt == MPX_F16)
+    softmax_launch<MPX_F16>(true, sm_vpl(n), grid, (hipStream_t)stream, (const uint16_t*)P,
+                            (const uint16_t*)dP, (uint16_t*)dS, rows, n, ld, scale);
+  else
+    softmax_launch<MPX_BF16>(true, sm_vpl(n), grid, (hipStream_t)stream, (const uint16_t*)P,
+                             (const uint16_t*)dP, (uint16_t*)dS, rows, n, ld, scale);
+  MPX_LAUNCHED();
   return MPX_OK;
+}
+
+extern "C" size_t mpx_loss_workspace(int64_t n) {
+  if (n < 1) return 0;
+  return (size_t)std::max<int64_t>(n, (n + kMseBlock - 1) / kMseBlock) * sizeof(float);
 }
 
 extern "C" int mpx_cross_entropy(const void* Z, int64_t ldz, const int32_t* labels, int64_t B,
                                  int64_t C, const mpx_scale_state* d_state, float* d_loss, void* dZ,
-                                 mpx_dtype dt, void* stream) {
+                                 mpx_dtype dt, void* workspace, size_t ws_bytes, void* stream) {
   clear_error();
   MPX_REQUIRE(Z && labels && d_state && d_loss && dZ, "NULL argument");
   MPX_REQUIRE(B >= 1 && C >= 1 && ldz >= C, "bad sizes");
   MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
-  MPX_DT_DISPATCH(dt, cross_entropy_kernel, 1, 256, stream, (const uint16_t*)Z, ldz, labels, B, C,
-                  d_state, d_loss, (uint16_t*)dZ);
+  if (!workspace || ws_bytes < mpx_loss_workspace(B)) {
+    set_error("mpx_cross_entropy: workspace of " + std::to_string(mpx_loss_workspace(B)) + " bytes required");
+    return MPX_ERR_WORKSPACE;
+  }
+  MPX_DT_DISPATCH(dt, cross_entropy_kernel, (unsigned)((B + 3) / 4), 256, stream, (const uint16_t*)Z, ldz,
+                  labels, B, C, d_state, (float*)workspace, (uint16_t*)dZ);
+  mean_kernel<<<1, 256, 0, (hipStream_t)stream>>>((const float*)workspace, B, d_loss);
+  MPX_LAUNCHED();
   return MPX_OK;
 }
 
 extern "C" int mpx_mse(const void* Y, const void* T, int64_t n, const mpx_scale_state* d_state,
-                       float* d_loss, void* dY, mpx_dtype dt, void* stream) {
+                       float* d_loss, void* dY, mpx_dtype dt, void* workspace, size_t ws_bytes,
+                       void* stream) {
   clear_error();
   MPX_REQUIRE(Y && T && d_state && d_loss && dY, "NULL argument");
   MPX_REQUIRE(n >= 1, "n must be >= 1");
   MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
-  MPX_DT_DISPATCH(dt, mse_kernel, 1, 256, stream, (const uint16_t*)Y, (const uint16_t*)T, n, d_state,
-                  d_loss, (uint16_t*)dY);
+  if (!workspace || ws_bytes < mpx_loss_workspace(n)) {
+    set_error("mpx_mse: workspace of " + std::to_string(mpx_loss_workspace(n)) + " bytes required");
+    return MPX_ERR_WORKSPACE;
+  }
+  const int64_t nb = (n + kMseBlock - 1) / kMseBlock;
+  MPX_DT_DISPATCH(dt, mse_kernel, (unsigned)nb, 256, stream, (const uint16_t*)Y, (const uint16_t*)T, n,
+                  d_state, (float*)workspace, (uint16_t*)dY);
+  mse_final_kernel<<<1, 256, 0, (hipStream_t)stream>>>((const float*)workspace, nb, n, d_loss);
+  MPX_LAUNCHED();
   return MPX_OK;
 }
 

@@ -4,12 +4,14 @@
 // masked AdamW update (§3.5).
 //
 // All sweeps are HBM-bound.  A tensor list is cut into fixed-size chunks
-// once, at list creation; one workgroup owns one chunk and walks it with
-// 16-byte vector loads (8 elements per lane per step, consecutive lanes on
-// consecutive vectors), falling back to scalar accesses only for chunk
-// tails and for tensors whose base pointer is not 16-byte aligned.
+// once, at list creation; one workgroup owns one chunk and walks it in
+// coalesced vector accesses (groups of 4 elements per lane, consecutive lanes
+// on consecutive groups, several groups in flight per lane), falling back to
+// scalar accesses only for chunk tails and for tensors whose base pointer is
+// not 16-byte aligned.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstring>
 #include <string>
@@ -24,7 +26,6 @@ void set_error(const std::string& msg) { g_err = msg; }
 void clear_error() { g_err.clear(); }
 
 constexpr int kThreads = 256;
-constexpr int64_t kChunk = 16384;  // elements per chunk (multiple of 8)
 
 struct Chunk {
   int32_t tensor;
@@ -67,31 +68,37 @@ __device__ __forceinline__ bool last_block(uint32_t* ticket) {
   return is_last;
 }
 
-struct F8 {
-  float v[8];
-};
+// Lanes work on groups of 4 consecutive elements so that a wave's float32
+// accesses are one contiguous 1 KiB span per instruction (16 bytes per lane)
+// and its half accesses one contiguous 512 B span (8 bytes per lane).  Each
+// lane handles kUnroll groups per iteration to keep enough bytes in flight.
+constexpr int kUnroll = 4;
+constexpr int kGroup = 4;
+constexpr int kStep = kUnroll * kGroup * kThreads;  // elements per workgroup iteration
 
-__device__ __forceinline__ F8 load_f32x8(const float* p) {
-  const float4* q = reinterpret_cast<const float4*>(p);
-  float4 a = q[0], b = q[1];
-  return F8{{a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w}};
+// Chunk length for a list of `total` elements: about 2048 chunks (8 per CU),
+// at least one workgroup iteration and at most 64 Ki elements, a multiple of
+// the iteration length so that only a tensor's last chunk has a tail.
+static int64_t chunk_len(int64_t total) {
+  int64_t c = total / 2048;
+  c = (c + kStep - 1) / kStep * kStep;
+  return std::max<int64_t>(kStep, std::min<int64_t>(c, 16 * kStep));
 }
-__device__ __forceinline__ void store_f32x8(float* p, const F8& f) {
-  float4* q = reinterpret_cast<float4*>(p);
-  q[0] = make_float4(f.v[0], f.v[1], f.v[2], f.v[3]);
-  q[1] = make_float4(f.v[4], f.v[5], f.v[6], f.v[7]);
+
+__device__ __forceinline__ void unpack_h4(uint2 u, uint16_t (&h)[4]) {
+  h[0] = (uint16_t)(u.x & 0xFFFFu);
+  h[1] = (uint16_t)(u.x >> 16);
+  h[2] = (uint16_t)(u.y & 0xFFFFu);
+  h[3] = (uint16_t)(u.y >> 16);
 }
-__device__ __forceinline__ void unpack_h8(uint4 u, uint16_t (&h)[8]) {
-  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    h[2 * i] = (uint16_t)(w[i] & 0xFFFFu);
-    h[2 * i + 1] = (uint16_t)(w[i] >> 16);
-  }
+__device__ __forceinline__ uint2 pack_h4(const uint16_t (&h)[4]) {
+  return make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
 }
-__device__ __forceinline__ uint4 pack_h8(const uint16_t (&h)[8]) {
-  return make_uint4((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16),
-                    (uint32_t)h[4] | ((uint32_t)h[5] << 16), (uint32_t)h[6] | ((uint32_t)h[7] << 16));
+__device__ __forceinline__ float get(const float4& v, int j) {
+  return j == 0 ? v.x : j == 1 ? v.y : j == 2 ? v.z : v.w;
+}
+__device__ __forceinline__ void set(float4& v, int j, float x) {
+  if (j == 0) v.x = x; else if (j == 1) v.y = x; else if (j == 2) v.z = x; else v.w = x;
 }
 
 // ----------------------------------------------------------------- cast --
@@ -106,15 +113,19 @@ __global__ __launch_bounds__(kThreads) void cast_kernel(const Chunk* __restrict_
   const int len = c.len;
   int done = 0;
   if (aligned16(src) && aligned16(dst)) {
-    const int nvec = len / 8;
-    for (int i = threadIdx.x; i < nvec; i += kThreads) {
-      F8 f = load_f32x8(src + 8 * i);
-      uint16_t h[8];
+    for (; done + kStep <= len; done += kStep) {
+      float4 f[kUnroll];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) h[j] = f2h<HDT>(f.v[j]);
-      *reinterpret_cast<uint4*>(dst + 8 * i) = pack_h8(h);
+      for (int u = 0; u < kUnroll; ++u)
+        f[u] = *reinterpret_cast<const float4*>(src + done + (u * kThreads + threadIdx.x) * kGroup);
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        uint16_t h[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) h[j] = f2h<HDT>(get(f[u], j));
+        *reinterpret_cast<uint2*>(dst + done + (u * kThreads + threadIdx.x) * kGroup) = pack_h4(h);
+      }
     }
-    done = nvec * 8;
   }
   for (int i = done + threadIdx.x; i < len; i += kThreads) dst[i] = f2h<HDT>(src[i]);
 }
@@ -134,19 +145,24 @@ __global__ __launch_bounds__(kThreads) void unscale_check_kernel(
   int bad = 0;
   int done = 0;
   if (aligned16(g) && (!WRITE || aligned16(out))) {
-    const int nvec = len / 8;
-    for (int i = threadIdx.x; i < nvec; i += kThreads) {
-      uint16_t h[8];
-      unpack_h8(*reinterpret_cast<const uint4*>(g + 8 * i), h);
-      F8 f;
+    for (; done + kStep <= len; done += kStep) {
+      uint2 raw[kUnroll];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        bad += h_nonfinite<GDT>(h[j]) ? 1 : 0;
-        if (WRITE) f.v[j] = h2f<GDT>(h[j]) / scale;
+      for (int u = 0; u < kUnroll; ++u)
+        raw[u] = *reinterpret_cast<const uint2*>(g + done + (u * kThreads + threadIdx.x) * kGroup);
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        uint16_t h[4];
+        unpack_h4(raw[u], h);
+        float4 f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          bad += h_nonfinite<GDT>(h[j]) ? 1 : 0;
+          if (WRITE) set(f, j, h2f<GDT>(h[j]) / scale);
+        }
+        if (WRITE) *reinterpret_cast<float4*>(out + done + (u * kThreads + threadIdx.x) * kGroup) = f;
       }
-      if (WRITE) store_f32x8(out + 8 * i, f);
     }
-    done = nvec * 8;
   }
   for (int i = done + threadIdx.x; i < len; i += kThreads) {
     uint16_t h = g[i];
@@ -244,35 +260,48 @@ __global__ __launch_bounds__(kThreads) void adamw_kernel(
   int done = 0;
   if (aligned16(p) && aligned16(m) && aligned16(v) && aligned16(g) &&
       (HDT == MPX_F32 || aligned16(h))) {
-    const int nvec = len / 8;
-    for (int i = threadIdx.x; i < nvec; i += kThreads) {
-      F8 pp = load_f32x8(p + 8 * i);
-      F8 mm = load_f32x8(m + 8 * i);
-      F8 vv = load_f32x8(v + 8 * i);
-      float gg[8];
-      if constexpr (GDT == MPX_F32) {
-        F8 t8 = load_f32x8(reinterpret_cast<const float*>(g) + 8 * i);
+    for (; done + kStep <= len; done += kStep) {
+      float4 pp[kUnroll], mm[kUnroll], vv[kUnroll];
+      float gg[kUnroll][4];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) gg[j] = t8.v[j];
-      } else {
-        uint16_t hh[8];
-        unpack_h8(*reinterpret_cast<const uint4*>(g + 16 * i), hh);
+      for (int u = 0; u < kUnroll; ++u) {
+        const int e = done + (u * kThreads + threadIdx.x) * kGroup;
+        pp[u] = *reinterpret_cast<const float4*>(p + e);
+        mm[u] = *reinterpret_cast<const float4*>(m + e);
+        vv[u] = *reinterpret_cast<const float4*>(v + e);
+        if constexpr (GDT == MPX_F32) {
+          const float4 t4 = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g) + e);
+          gg[u][0] = t4.x; gg[u][1] = t4.y; gg[u][2] = t4.z; gg[u][3] = t4.w;
+        } else {
+          uint16_t hh[4];
+          unpack_h4(*reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(g) + e), hh);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) gg[j] = h2f<GDT>(hh[j]) / scale;
+          for (int j = 0; j < 4; ++j) gg[u][j] = h2f<GDT>(hh[j]);
+        }
       }
 #pragma unroll
-      for (int j = 0; j < 8; ++j) adamw_elem(pp.v[j], mm.v[j], vv.v[j], gg[j], k, bc1, bc2);
-      store_f32x8(p + 8 * i, pp);
-      store_f32x8(m + 8 * i, mm);
-      store_f32x8(v + 8 * i, vv);
-      if constexpr (HDT != MPX_F32) {
-        uint16_t hh[8];
+      for (int u = 0; u < kUnroll; ++u) {
+        const int e = done + (u * kThreads + threadIdx.x) * kGroup;
+        float P[4], Mv[4], V[4];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) hh[j] = f2h<HDT>(pp.v[j]);
-        *reinterpret_cast<uint4*>(h + 8 * i) = pack_h8(hh);
+        for (int j = 0; j < 4; ++j) {
+          P[j] = get(pp[u], j);
+          Mv[j] = get(mm[u], j);
+          V[j] = get(vv[u], j);
+          const float gj = GDT == MPX_F32 ? gg[u][j] : gg[u][j] / scale;
+          adamw_elem(P[j], Mv[j], V[j], gj, k, bc1, bc2);
+        }
+        *reinterpret_cast<float4*>(p + e) = make_float4(P[0], P[1], P[2], P[3]);
+        *reinterpret_cast<float4*>(m + e) = make_float4(Mv[0], Mv[1], Mv[2], Mv[3]);
+        *reinterpret_cast<float4*>(v + e) = make_float4(V[0], V[1], V[2], V[3]);
+        if constexpr (HDT != MPX_F32) {
+          uint16_t hh[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) hh[j] = f2h<HDT>(P[j]);
+          *reinterpret_cast<uint2*>(h + e) = pack_h4(hh);
+        }
       }
     }
-    done = nvec * 8;
   }
   for (int i = done + threadIdx.x; i < len; i += kThreads) {
     float pp = p[i], mm = m[i], vv = v[i];
@@ -326,6 +355,9 @@ extern "C" int mpx_tlist_create(const void* const* ptrs, const int64_t* numels, 
   std::vector<Chunk> chunks;
   auto* t = new mpx_tlist_s();
   t->n = n;
+  int64_t total = 0;
+  for (int32_t i = 0; i < n; ++i) total += numels[i] > 0 ? numels[i] : 0;
+  const int64_t chunk = chunk_len(total);
   for (int32_t i = 0; i < n; ++i) {
     if (numels[i] < 0 || (numels[i] > 0 && ptrs[i] == nullptr)) {
       delete t;
@@ -335,8 +367,8 @@ extern "C" int mpx_tlist_create(const void* const* ptrs, const int64_t* numels, 
     t->ptrs.push_back(const_cast<void*>(ptrs[i]));
     t->numels.push_back(numels[i]);
     t->total += numels[i];
-    for (int64_t s = 0; s < numels[i]; s += kChunk) {
-      int64_t len = numels[i] - s < kChunk ? numels[i] - s : kChunk;
+    for (int64_t s = 0; s < numels[i]; s += chunk) {
+      int64_t len = numels[i] - s < chunk ? numels[i] - s : chunk;
       chunks.push_back(Chunk{i, (int32_t)len, s});
     }
   }

@@ -240,7 +240,8 @@ class MLPStep(TrainStep):
         self.y = torch.zeros(B, D, dtype=h, device=dev)
         self.dy = torch.zeros(B, D, dtype=h, device=dev)
         self.dh_pre = torch.zeros(B, Dh, dtype=h, device=dev)
-        ws = max(mx.mpx_linear_bwd_workspace(B, D, Dh), mx.mpx_linear_bwd_workspace(B, Dh, D))
+        ws = max(mx.mpx_linear_bwd_workspace(B, D, Dh), mx.mpx_linear_bwd_workspace(B, Dh, D),
+                 mx.mpx_loss_workspace(B * D))
         self.ws = torch.zeros(ws, dtype=torch.uint8, device=dev)
 
     def _dominant_call(self, s):
@@ -270,7 +271,7 @@ class MLPStep(TrainStep):
         mx.mpx_linear_fwd(_ptr(self.hid), _ptr(a.w("fc2.w")), _ptr(a.w("fc2.b")), None,
                           _ptr(self.y), None, B, D, Dh, dt, mx.MPX_ACT_NONE, s)
         mx.mpx_mse(_ptr(self.y), _ptr(self.t16), B * D, _ptr(self.d_state), _ptr(self.d_loss),
-                   _ptr(self.dy), dt, s)
+                   _ptr(self.dy), dt, _ptr(self.ws), self.ws.numel(), s)
         wsb = self.ws.numel()
         mx.mpx_linear_bwd(_ptr(self.hid), _ptr(a.w("fc2.w")), _ptr(self.dy), _ptr(self.h_pre),
                           mx.MPX_ACT_GELU_TANH, _ptr(self.dh_pre), _ptr(a.gr("fc2.w")),
@@ -327,7 +328,7 @@ class ViTStep(TrainStep):
         if cfg.image:
             shapes.append((B * cfg.n_patches, d, cfg.patch_dim))
         ws = max(mx.mpx_linear_bwd_workspace(*s) for s in shapes)
-        ws = max(ws, mx.mpx_layernorm_bwd_workspace(M, d))
+        ws = max(ws, mx.mpx_layernorm_bwd_workspace(M, d), mx.mpx_loss_workspace(B))
         self.ws = torch.zeros(ws, dtype=torch.uint8, device=dev)
 
     def _dominant_call(self, s):
@@ -437,7 +438,7 @@ class ViTStep(TrainStep):
         mx.mpx_linear_fwd(_ptr(self.zf), _ptr(W("head.w")), _ptr(W("head.b")), None,
                           _ptr(self.logits), None, B, Cn, d, dt, NONE, s)
         mx.mpx_cross_entropy(_ptr(self.logits), Cn, _ptr(self.labels), B, Cn, _ptr(self.d_state),
-                             _ptr(self.d_loss), _ptr(self.dlogits), dt, s)
+                             _ptr(self.d_loss), _ptr(self.dlogits), dt, wsp, wsb, s)
         # ---- backward ----
         mx.mpx_linear_bwd(_ptr(self.zf), _ptr(W("head.w")), _ptr(self.dlogits), None, NONE,
                           _ptr(self.dz), _ptr(G("head.w")), _ptr(G("head.b")), B, Cn, d, dt,

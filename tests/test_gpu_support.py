@@ -42,7 +42,7 @@ def _sum_bound(x, fmt, ref):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
-@pytest.mark.parametrize("rows,d", [(130, 384), (7, 768), (33, 100), (5, 2048)])
+@pytest.mark.parametrize("rows,d", [(130, 384), (7, 768), (33, 100), (5, 2048), (8321, 384)])
 def test_layernorm_fwd_bwd(fmt, rows, d):
     pol = Policy(fmt)
     x = _rand((rows, d), fmt, 1, 2.0, 0.5)
@@ -142,8 +142,10 @@ def test_cross_entropy(fmt, B, C):
     st = torch.from_numpy(pack_scale_state(scale, 0, 10)).cuda()
     loss = torch.zeros(1, dtype=torch.float32, device="cuda")
     dz = _empty((B, C), fmt)
+    wsn = mx.mpx_loss_workspace(B)
+    ws = torch.zeros(wsn, dtype=torch.uint8, device="cuda")
     mx.mpx_cross_entropy(tz.data_ptr(), C, ty.data_ptr(), B, C, st.data_ptr(), loss.data_ptr(),
-                         dz.data_ptr(), mx.DTYPES[fmt], _s())
+                         dz.data_ptr(), mx.DTYPES[fmt], ws.data_ptr(), wsn, _s())
     rl, rdz = ops.ce_fwd_bwd(pol, z, y, scale)
     assert abs(float(loss.item()) - rl) <= 1e-5 * abs(rl)
     assert_within(to_host(dz), rdz, ulp(rdz, fmt) + 1e-5 * np.abs(rdz), "CE cotangent")
@@ -158,8 +160,10 @@ def test_mse(fmt):
     loss = torch.zeros(1, dtype=torch.float32, device="cuda")
     dy = _empty((64, 512), fmt)
     ty, tt = to_dev_half(yv, fmt), to_dev_half(tv, fmt)
+    wsn = mx.mpx_loss_workspace(yv.size)
+    ws = torch.zeros(wsn, dtype=torch.uint8, device="cuda")
     mx.mpx_mse(ty.data_ptr(), tt.data_ptr(), yv.size, st.data_ptr(), loss.data_ptr(), dy.data_ptr(),
-               mx.DTYPES[fmt], _s())
+               mx.DTYPES[fmt], ws.data_ptr(), wsn, _s())
     rl, rdy = ops.mse_fwd_bwd(pol, yv, tv, 2.0 ** 15)
     assert abs(float(loss.item()) - rl) <= 1e-5 * rl
     assert_within(to_host(dy), rdy, ulp(rdy, fmt), "MSE cotangent")
