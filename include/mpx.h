@@ -81,9 +81,7 @@ typedef struct {
  * the element type is given per call.  The library copies the descriptors to
  * device memory (a synchronous upload: create lists at set-up, not inside a
  * captured region) and owns that copy; the caller keeps owning the tensors and
- * must keep them alive while the list is used.  A list also owns a few bytes of
- * device scratch used by the reductions of the calls below, so calls that use
- * the same list must not run concurrently on different streams. */
+ * must keep them alive while the list is used. */
 typedef struct mpx_tlist_s* mpx_tlist;
 
 int mpx_tlist_create(const void* const* ptrs, const int64_t* numels, int32_t n,
@@ -104,7 +102,9 @@ int mpx_cast_to_half(mpx_tlist src_f32, mpx_tlist dst_half, mpx_dtype half, void
  *                  (+-inf or NaN); 0 means the gradients are finite;
  *   if out_f32 != NULL: out_f32[i][j] = float32(g) / d_state->scale
  *                  (widen first, then divide; exact for a power-of-two scale).
- * The count is exact (integer); *d_nonfinite is overwritten, not added to. */
+ * The count is exact (integer); *d_nonfinite is overwritten, not added to
+ * (it is zeroed first, then workgroups that find non-finite values add their
+ * counts, so two calls sharing d_nonfinite must not overlap). */
 int mpx_unscale_check(mpx_tlist grads, mpx_dtype gdt, const mpx_scale_state* d_state,
                       int32_t* d_nonfinite, mpx_tlist out_f32, void* stream);
 

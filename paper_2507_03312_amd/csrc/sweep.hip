@@ -43,7 +43,6 @@ struct mpx_tlist_s {
   void** d_ptrs = nullptr;
   mpx::Chunk* d_chunks = nullptr;
   int32_t nchunks = 0;
-  uint32_t* d_scratch = nullptr;  // [0] ticket, [1] accumulator
 };
 
 namespace mpx {
@@ -54,20 +53,6 @@ __device__ __forceinline__ bool aligned16(const void* p) {
   return (reinterpret_cast<uintptr_t>(p) & 15u) == 0;
 }
 
-// True in exactly one workgroup: the last one to arrive.  Every workgroup
-// must call it (after finishing its own work).
-__device__ __forceinline__ bool last_block(uint32_t* ticket) {
-  __shared__ bool is_last;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    __threadfence();
-    uint32_t t = atomicAdd(ticket, 1u);
-    is_last = (t == gridDim.x - 1);
-  }
-  __syncthreads();
-  return is_last;
-}
-
 // Lanes work on groups of 4 consecutive elements so that a wave's float32
 // accesses are one contiguous 1 KiB span per instruction (16 bytes per lane)
 // and its half accesses one contiguous 512 B span (8 bytes per lane).  Each
@@ -76,13 +61,28 @@ constexpr int kUnroll = 4;
 constexpr int kGroup = 4;
 constexpr int kStep = kUnroll * kGroup * kThreads;  // elements per workgroup iteration
 
-// Chunk length for a list of `total` elements: about 2048 chunks (8 per CU),
-// at least one workgroup iteration and at most 64 Ki elements, a multiple of
-// the iteration length so that only a tensor's last chunk has a tail.
-static int64_t chunk_len(int64_t total) {
-  int64_t c = total / 2048;
-  c = (c + kStep - 1) / kStep * kStep;
-  return std::max<int64_t>(kStep, std::min<int64_t>(c, 16 * kStep));
+// Chunk length: one workgroup iteration, so that every lane issues all of its
+// loads at once and the grid holds as many workgroups as there are chunks
+// (measured: the highest sustained bandwidth for these streaming updates).
+static int64_t chunk_len(int64_t) { return kStep; }
+
+// Streaming accesses: every byte is touched once per sweep, so loads and
+// stores are marked non-temporal.
+typedef float nt_f4 __attribute__((ext_vector_type(4)));
+typedef uint32_t nt_u2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ float4 ld_nt(const float* p) {
+  const nt_f4 v = __builtin_nontemporal_load(reinterpret_cast<const nt_f4*>(p));
+  return make_float4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ void st_nt(float* p, float4 v) {
+  __builtin_nontemporal_store((nt_f4){v.x, v.y, v.z, v.w}, reinterpret_cast<nt_f4*>(p));
+}
+__device__ __forceinline__ uint2 ld_nt(const uint16_t* p) {
+  const nt_u2 v = __builtin_nontemporal_load(reinterpret_cast<const nt_u2*>(p));
+  return make_uint2(v.x, v.y);
+}
+__device__ __forceinline__ void st_nt(uint16_t* p, uint2 v) {
+  __builtin_nontemporal_store((nt_u2){v.x, v.y}, reinterpret_cast<nt_u2*>(p));
 }
 
 __device__ __forceinline__ void unpack_h4(uint2 u, uint16_t (&h)[4]) {
@@ -117,13 +117,13 @@ __global__ __launch_bounds__(kThreads) void cast_kernel(const Chunk* __restrict_
       float4 f[kUnroll];
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u)
-        f[u] = *reinterpret_cast<const float4*>(src + done + (u * kThreads + threadIdx.x) * kGroup);
+        f[u] = ld_nt(src + done + (u * kThreads + threadIdx.x) * kGroup);
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         uint16_t h[4];
 #pragma unroll
         for (int j = 0; j < 4; ++j) h[j] = f2h<HDT>(get(f[u], j));
-        *reinterpret_cast<uint2*>(dst + done + (u * kThreads + threadIdx.x) * kGroup) = pack_h4(h);
+        st_nt(dst + done + (u * kThreads + threadIdx.x) * kGroup, pack_h4(h));
       }
     }
   }
@@ -136,7 +136,7 @@ template <int GDT, bool WRITE>
 __global__ __launch_bounds__(kThreads) void unscale_check_kernel(
     const Chunk* __restrict__ chunks, void* const* __restrict__ g_ptrs,
     void* const* __restrict__ o_ptrs, const mpx_scale_state* __restrict__ state,
-    int32_t* __restrict__ nonfinite, uint32_t* __restrict__ scratch) {
+    int32_t* __restrict__ nonfinite) {
   const Chunk c = chunks[blockIdx.x];
   const uint16_t* g = reinterpret_cast<const uint16_t*>(g_ptrs[c.tensor]) + c.start;
   float* out = WRITE ? reinterpret_cast<float*>(o_ptrs[c.tensor]) + c.start : nullptr;
@@ -149,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void unscale_check_kernel(
       uint2 raw[kUnroll];
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u)
-        raw[u] = *reinterpret_cast<const uint2*>(g + done + (u * kThreads + threadIdx.x) * kGroup);
+        raw[u] = ld_nt(g + done + (u * kThreads + threadIdx.x) * kGroup);
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         uint16_t h[4];
@@ -160,7 +160,7 @@ __global__ __launch_bounds__(kThreads) void unscale_check_kernel(
           bad += h_nonfinite<GDT>(h[j]) ? 1 : 0;
           if (WRITE) set(f, j, h2f<GDT>(h[j]) / scale);
         }
-        if (WRITE) *reinterpret_cast<float4*>(out + done + (u * kThreads + threadIdx.x) * kGroup) = f;
+        if (WRITE) st_nt(out + done + (u * kThreads + threadIdx.x) * kGroup, f);
       }
     }
   }
@@ -178,13 +178,8 @@ __global__ __launch_bounds__(kThreads) void unscale_check_kernel(
     int s = 0;
 #pragma unroll
     for (int w = 0; w < kThreads / 64; ++w) s += part[w];
-    if (s) atomicAdd(&scratch[1], (uint32_t)s);
-  }
-  if (last_block(&scratch[0]) && threadIdx.x == 0) {
-    __threadfence();
-    uint32_t total = atomicExch(&scratch[1], 0u);
-    *nonfinite = (int32_t)total;
-    atomicExch(&scratch[0], 0u);
+    // only workgroups that found a non-finite value touch the (pre-zeroed) count
+    if (s) atomicAdd(nonfinite, s);
   }
 }
 
@@ -241,8 +236,8 @@ __global__ __launch_bounds__(kThreads) void adamw_kernel(
     const Chunk* __restrict__ chunks, void* const* __restrict__ p_ptrs,
     void* const* __restrict__ m_ptrs, void* const* __restrict__ v_ptrs,
     void* const* __restrict__ g_ptrs, void* const* __restrict__ h_ptrs, AdamConsts k,
-    int32_t* __restrict__ step, const mpx_scale_state* __restrict__ state,
-    const int32_t* __restrict__ nonfinite, uint32_t* __restrict__ scratch) {
+    const int32_t* __restrict__ step, const mpx_scale_state* __restrict__ state,
+    const int32_t* __restrict__ nonfinite) {
   if (*nonfinite != 0) return;  // skipped step: nothing is written (uniform)
   const int t = *step + 1;
   const float bc1 = (float)(1.0 - pow(k.beta1, (double)t));
@@ -266,15 +261,15 @@ __global__ __launch_bounds__(kThreads) void adamw_kernel(
 #pragma unroll
       for (int u = 0; u < kUnroll; ++u) {
         const int e = done + (u * kThreads + threadIdx.x) * kGroup;
-        pp[u] = *reinterpret_cast<const float4*>(p + e);
-        mm[u] = *reinterpret_cast<const float4*>(m + e);
-        vv[u] = *reinterpret_cast<const float4*>(v + e);
+        pp[u] = ld_nt(p + e);
+        mm[u] = ld_nt(m + e);
+        vv[u] = ld_nt(v + e);
         if constexpr (GDT == MPX_F32) {
-          const float4 t4 = *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(g) + e);
+          const float4 t4 = ld_nt(reinterpret_cast<const float*>(g) + e);
           gg[u][0] = t4.x; gg[u][1] = t4.y; gg[u][2] = t4.z; gg[u][3] = t4.w;
         } else {
           uint16_t hh[4];
-          unpack_h4(*reinterpret_cast<const uint2*>(reinterpret_cast<const uint16_t*>(g) + e), hh);
+          unpack_h4(ld_nt(reinterpret_cast<const uint16_t*>(g) + e), hh);
 #pragma unroll
           for (int j = 0; j < 4; ++j) gg[u][j] = h2f<GDT>(hh[j]);
         }
@@ -291,14 +286,14 @@ __global__ __launch_bounds__(kThreads) void adamw_kernel(
           const float gj = GDT == MPX_F32 ? gg[u][j] : gg[u][j] / scale;
           adamw_elem(P[j], Mv[j], V[j], gj, k, bc1, bc2);
         }
-        *reinterpret_cast<float4*>(p + e) = make_float4(P[0], P[1], P[2], P[3]);
-        *reinterpret_cast<float4*>(m + e) = make_float4(Mv[0], Mv[1], Mv[2], Mv[3]);
-        *reinterpret_cast<float4*>(v + e) = make_float4(V[0], V[1], V[2], V[3]);
+        st_nt(p + e, make_float4(P[0], P[1], P[2], P[3]));
+        st_nt(m + e, make_float4(Mv[0], Mv[1], Mv[2], Mv[3]));
+        st_nt(v + e, make_float4(V[0], V[1], V[2], V[3]));
         if constexpr (HDT != MPX_F32) {
           uint16_t hh[4];
 #pragma unroll
           for (int j = 0; j < 4; ++j) hh[j] = f2h<HDT>(P[j]);
-          *reinterpret_cast<uint2*>(h + e) = pack_h4(hh);
+          st_nt(h + e, pack_h4(hh));
         }
       }
     }
@@ -312,13 +307,15 @@ __global__ __launch_bounds__(kThreads) void adamw_kernel(
     v[i] = vv;
     if constexpr (HDT != MPX_F32) h[i] = f2h<HDT>(pp);
   }
-  // the last workgroup to finish advances the applied-step count
-  if (last_block(&scratch[0]) && threadIdx.x == 0) {
-    __threadfence();
-    *step = t;
-    atomicExch(&scratch[0], 0u);
-  }
 }
+
+// Advances the applied-step count after the update (one thread; on a skipped
+// step nothing changes).
+__global__ void step_count_kernel(int32_t* step, const int32_t* nonfinite) {
+  if (*nonfinite == 0) *step += 1;
+}
+
+__global__ void zero_i32_kernel(int32_t* p) { *p = 0; }
 
 // ------------------------------------------------------------------ zero --
 
@@ -380,8 +377,6 @@ extern "C" int mpx_tlist_create(const void* const* ptrs, const int64_t* numels, 
   if (e == hipSuccess && !chunks.empty()) e = hipMalloc(&t->d_chunks, sizeof(Chunk) * chunks.size());
   if (e == hipSuccess && !chunks.empty())
     e = hipMemcpy(t->d_chunks, chunks.data(), sizeof(Chunk) * chunks.size(), hipMemcpyHostToDevice);
-  if (e == hipSuccess) e = hipMalloc(&t->d_scratch, 64);
-  if (e == hipSuccess) e = hipMemset(t->d_scratch, 0, 64);
   if (e != hipSuccess) {
     set_error(std::string("mpx_tlist_create: ") + hipGetErrorString(e));
     mpx_tlist_destroy(t);
@@ -395,7 +390,6 @@ extern "C" int mpx_tlist_destroy(mpx_tlist t) {
   if (!t) return MPX_OK;
   if (t->d_ptrs) (void)hipFree(t->d_ptrs);
   if (t->d_chunks) (void)hipFree(t->d_chunks);
-  if (t->d_scratch) (void)hipFree(t->d_scratch);
   delete t;
   return MPX_OK;
 }
@@ -425,23 +419,21 @@ extern "C" int mpx_unscale_check(mpx_tlist grads, mpx_dtype gdt, const mpx_scale
   MPX_REQUIRE(!out_f32 || d_state, "d_state is required when out_f32 is given");
   MPX_REQUIRE(!out_f32 || same_shape(grads, out_f32), "out_f32 differs in shape from grads");
   hipStream_t s = (hipStream_t)stream;
-  if (grads->nchunks == 0) {
-    zero_kernel<<<1, 64, 0, s>>>(reinterpret_cast<uint8_t*>(d_nonfinite), sizeof(int32_t));
-    MPX_LAUNCHED();
-    return MPX_OK;
-  }
+  zero_i32_kernel<<<1, 1, 0, s>>>(d_nonfinite);
+  MPX_LAUNCHED();
+  if (grads->nchunks == 0) return MPX_OK;
   void* const* o = out_f32 ? out_f32->d_ptrs : nullptr;
   dim3 g(grads->nchunks), b(kThreads);
   if (gdt == MPX_F16) {
     if (out_f32)
-      unscale_check_kernel<MPX_F16, true><<<g, b, 0, s>>>(grads->d_chunks, grads->d_ptrs, o, d_state, d_nonfinite, grads->d_scratch);
+      unscale_check_kernel<MPX_F16, true><<<g, b, 0, s>>>(grads->d_chunks, grads->d_ptrs, o, d_state, d_nonfinite);
     else
-      unscale_check_kernel<MPX_F16, false><<<g, b, 0, s>>>(grads->d_chunks, grads->d_ptrs, o, d_state, d_nonfinite, grads->d_scratch);
+      unscale_check_kernel<MPX_F16, false><<<g, b, 0, s>>>(grads->d_chunks, grads->d_ptrs, o, d_state, d_nonfinite);
   } else {
     if (out_f32)
-      unscale_check_kernel<MPX_BF16, true><<<g, b, 0, s>>>(grads->d_chunks, grads->d_ptrs, o, d_state, d_nonfinite, grads->d_scratch);
+      unscale_check_kernel<MPX_BF16, true><<<g, b, 0, s>>>(grads->d_chunks, grads->d_ptrs, o, d_state, d_nonfinite);
     else
-      unscale_check_kernel<MPX_BF16, false><<<g, b, 0, s>>>(grads->d_chunks, grads->d_ptrs, o, d_state, d_nonfinite, grads->d_scratch);
+      unscale_check_kernel<MPX_BF16, false><<<g, b, 0, s>>>(grads->d_chunks, grads->d_ptrs, o, d_state, d_nonfinite);
   }
   MPX_LAUNCHED();
   return MPX_OK;
@@ -461,7 +453,8 @@ static void launch_adamw(mpx_tlist p, mpx_tlist m, mpx_tlist v, mpx_tlist g, mpx
                          const int32_t* nf, hipStream_t s) {
   adamw_kernel<GDT, HDT><<<p->nchunks, kThreads, 0, s>>>(
       p->d_chunks, p->d_ptrs, m->d_ptrs, v->d_ptrs, g->d_ptrs, h ? h->d_ptrs : nullptr, k, step,
-      st, nf, p->d_scratch);
+      st, nf);
+  step_count_kernel<<<1, 1, 0, s>>>(step, nf);
 }
 
 extern "C" int mpx_adamw_masked(mpx_tlist p32, mpx_tlist m32, mpx_tlist v32, mpx_tlist grads,
