@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--config", default=DEFAULT_CONFIG, choices=workloads.CONFIG_ORDER)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="after the timed region, run one plain device copy of this many MiB "
+                         "(reference dispatch for hardware byte counters)")
     return ap.parse_args()
 
 
@@ -175,6 +178,12 @@ def main():
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps
     k_ms = st.time_dominant()
+    if args.copy_calibration_mib:
+        n = args.copy_calibration_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
     achieved = site["flops"] / (k_ms * 1e-3) / 1e12
     peak = PEAK_MFMA_TFLOPS[cfg.half]
     line = {"metric": "train steps/s", "value": round(1000.0 / ms, 3), "unit": "steps/s",

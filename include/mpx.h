@@ -173,6 +173,16 @@ int mpx_gemm_batched(int32_t trans_a, int32_t trans_b, int64_t M, int64_t N, int
                      void* C, int64_t ldc, int64_t sC0, int64_t sC1, mpx_dtype dt,
                      void* stream);
 
+/* Tile configuration of the GEMMs above, for tuning and tests: 0 (default)
+ * picks per call from the problem shape; 1..7 force one configuration
+ * (1: 64x64 register-staged; 2: 128x128 register-staged; 3: 256x256,
+ * 4: 256x128, 5: 128x256, 6: 128x128 four-stage, 7: 128x128 two-stage
+ * direct-to-LDS).  A forced configuration that a call's operands do not
+ * allow (alignment, k not a multiple of 64) falls back to the automatic
+ * choice.  Process-wide setting; not synchronised with concurrent calls.
+ * Errors: MPX_ERR_INVALID for a value outside [0, 7]. */
+int mpx_gemm_set_config(int32_t config);
+
 /* ---- Support ops of the half forward/backward (full-precision islands,
  * MPX §3.2 force_full_precision: sums, means, softmax) ---- */
 

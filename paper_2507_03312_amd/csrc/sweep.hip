@@ -68,21 +68,24 @@ static int64_t chunk_len(int64_t) { return kStep; }
 
 // Streaming accesses: every byte is touched once per sweep, so loads and
 // stores are marked non-temporal.
+// The tensor pointers come from a device table, so the compiler cannot tell
+// they are global memory; the casts let it use global (not flat) accesses.
 typedef float nt_f4 __attribute__((ext_vector_type(4)));
 typedef uint32_t nt_u2 __attribute__((ext_vector_type(2)));
+#define MPX_GLOBAL __attribute__((address_space(1)))
 __device__ __forceinline__ float4 ld_nt(const float* p) {
-  const nt_f4 v = __builtin_nontemporal_load(reinterpret_cast<const nt_f4*>(p));
+  const nt_f4 v = __builtin_nontemporal_load((const MPX_GLOBAL nt_f4*)p);
   return make_float4(v.x, v.y, v.z, v.w);
 }
 __device__ __forceinline__ void st_nt(float* p, float4 v) {
-  __builtin_nontemporal_store((nt_f4){v.x, v.y, v.z, v.w}, reinterpret_cast<nt_f4*>(p));
+  __builtin_nontemporal_store((nt_f4){v.x, v.y, v.z, v.w}, (MPX_GLOBAL nt_f4*)p);
 }
 __device__ __forceinline__ uint2 ld_nt(const uint16_t* p) {
-  const nt_u2 v = __builtin_nontemporal_load(reinterpret_cast<const nt_u2*>(p));
+  const nt_u2 v = __builtin_nontemporal_load((const MPX_GLOBAL nt_u2*)p);
   return make_uint2(v.x, v.y);
 }
 __device__ __forceinline__ void st_nt(uint16_t* p, uint2 v) {
-  __builtin_nontemporal_store((nt_u2){v.x, v.y}, reinterpret_cast<nt_u2*>(p));
+  __builtin_nontemporal_store((nt_u2){v.x, v.y}, (MPX_GLOBAL nt_u2*)p);
 }
 
 __device__ __forceinline__ void unpack_h4(uint2 u, uint16_t (&h)[4]) {

@@ -217,3 +217,74 @@ def test_full_size_linear_sampled(fmt, mnk):
     assert_within(to_host(gdx)[np.ix_(rows, kc)], ref, gemm_bound(dy[rows], w[:, kc], ref, fmt, N), "dX")
     ref = pol.gemm(dy[:, cols].T, x[:, kc])
     assert_within(to_host(gdw)[np.ix_(cols, kc)], ref, gemm_bound(dy[:, cols].T, x[:, kc], ref, fmt, M), "dW")
+
+
+CONFIGS = [1, 2, 3, 4, 5, 6, 7]
+
+
+@pytest.fixture
+def gemm_config(request):
+    mx.mpx_gemm_set_config(request.param)
+    yield request.param
+    mx.mpx_gemm_set_config(0)
+
+
+@pytest.mark.parametrize("gemm_config", CONFIGS, indirect=True)
+@pytest.mark.parametrize("fmt", FMTS)
+def test_every_tile_config(gemm_config, fmt):
+    """Each tile configuration forced in turn (the direct-to-LDS ones need k a
+    multiple of 64): forward with bias + GELU on a ragged output, backward
+    with dX through GELU' and split-K dW, all three operand layouts."""
+    pol = Policy(fmt)
+    dt = mx.DTYPES[fmt]
+    # forward, ragged M and N
+    M, N, K = 300, 200, 320
+    x, w, b = _rand((M, K), fmt, 41), _rand((N, K), fmt, 42, 0.05), _rand((N,), fmt, 43, 0.5)
+    tx, tw, tb = (to_dev_half(a, fmt) for a in (x, w, b))
+    y, pre = _empty((M, N), fmt), _empty((M, N), fmt)
+    mx.mpx_linear_fwd(tx.data_ptr(), tw.data_ptr(), tb.data_ptr(), None, y.data_ptr(),
+                      pre.data_ptr(), M, N, K, dt, mx.MPX_ACT_GELU_TANH, _s())
+    ref = ops.linear_fwd(pol, x, w, b)
+    gpre = to_host(pre)
+    assert_within(gpre, ref, gemm_bound(x, w.T, ref, fmt, K), "pre-activation")
+    g_ref = ops.gelu_fwd(pol, gpre)
+    assert_within(to_host(y), g_ref, ulp(g_ref, fmt), "gelu epilogue")
+    # backward: every reduction a multiple of 64, outputs ragged w.r.t. the tiles
+    M, N, K = 2112, 448, 320
+    x, w = _rand((M, K), fmt, 44), _rand((N, K), fmt, 45, 0.05)
+    dy, xpre = _rand((M, N), fmt, 46), _rand((M, K), fmt, 47)
+    tx, tw, tdy, txp = (to_dev_half(a, fmt) for a in (x, w, dy, xpre))
+    gdx, gdw = _empty((M, K), fmt), _empty((N, K), fmt)
+    ws_n = mx.mpx_linear_bwd_workspace(M, N, K)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), txp.data_ptr(),
+                      mx.MPX_ACT_GELU_TANH, gdx.data_ptr(), gdw.data_ptr(), None, M, N, K, dt,
+                      ws.data_ptr(), ws_n, _s())
+    rdx, rdw, _ = ops.linear_bwd(pol, x, w, dy)
+    assert_within(to_host(gdw), rdw, gemm_bound(dy.T, x, rdw, fmt, M), "dW")
+    ref = ops.gelu_bwd(pol, xpre, rdx)
+    assert_within(to_host(gdx), ref, 1.13 * gemm_bound(dy, w, rdx, fmt, N) + ulp(ref, fmt),
+                  "dX through gelu'")
+    # batched, both transposed layouts, head dim 64 and 128 tokens
+    B, H, T, hd = 2, 2, 128, 64
+    d = H * hd
+    qkv = _rand((B * T, 3 * d), fmt, 48)
+    tq = to_dev_half(qkv, fmt)
+    e = tq.element_size()
+    q, k, v = ops.split_heads(qkv, B, T, H, hd)
+    out_s, out_o = _empty((B * H * T, T), fmt), _empty((B * T, d), fmt)
+    mx.mpx_gemm_batched(0, 1, T, T, hd, B, H, tq.data_ptr(), 3 * d, T * 3 * d, hd,
+                        tq.data_ptr() + d * e, 3 * d, T * 3 * d, hd,
+                        out_s.data_ptr(), T, H * T * T, T * T, dt, _s())
+    k_t = np.swapaxes(k, -1, -2)
+    ref = pol.R(pol.mm(q, k_t))
+    bnd = ulp(ref, fmt) + 2 * hd * 2.0 ** -24 * (np.abs(q.astype(np.float64)) @ np.abs(k_t.astype(np.float64)))
+    assert_within(to_host(out_s).reshape(B, H, T, T), ref, bnd, "QK^T")
+    # K^T V-like product: both operands mn-major (trans_a = 1, trans_b = 0)
+    mx.mpx_gemm_batched(1, 0, hd, hd, T, B, H, tq.data_ptr() + d * e, 3 * d, T * 3 * d, hd,
+                        tq.data_ptr() + 2 * d * e, 3 * d, T * 3 * d, hd,
+                        out_o.data_ptr(), d, T * d, hd, dt, _s())
+    kt_v = pol.R(pol.mm(k_t, v))
+    bnd = ulp(kt_v, fmt) + 2 * T * 2.0 ** -24 * (np.abs(k_t.astype(np.float64)) @ np.abs(v.astype(np.float64)))
+    got = to_host(out_o).reshape(B, T, H, hd)[:, :hd].transpose(0, 2, 1, 3)
+    assert_within(got, kt_v, bnd, "K^T V")
