@@ -1,0 +1,965 @@
+// Half-precision GEMMs with float32 accumulation on gfx950 MFMA, for the
+// forward and backward passes of MPX's mixed-precision step (§2: forward and
+// backward in half precision; the products accumulate in float32).
+//
+// One kernel template computes  C[m,n] = sum_k A(m,k) B(n,k)  where each
+// operand is stored either with the reduction index contiguous ("k-major") or
+// with the output index contiguous ("mn-major"):
+//   forward  Y  = X W^T   : A = X  k-major,  B = W  k-major
+//   backward dX = dY W    : A = dY k-major,  B = W  mn-major
+//   backward dW = dY^T X  : A = dY mn-major, B = X  mn-major
+// Tiles are staged through LDS in one layout, [row][k] with k contiguous, so
+// the MFMA operand reads are always 16-byte ds_read_b128.  An mn-major operand
+// is transposed on the way in: each lane loads 4 rows of 8 contiguous values
+// and writes them as 8 rows of 4 k-values (a register transpose of 16-bit
+// pairs).  The MFMA is v_mfma_f32_32x32x16_{f16,bf16}: lane l holds 8 k-values
+// of row l%32 for A and of column l%32 for B; the 16 accumulators of lane l are
+// column l%32, rows 8*(i/4) + 4*(l/32) + i%4.
+//
+// Epilogue (all optional, in this order, each rounding once to half):
+//   h = half(acc + bias[n]);  pre_out = h;  h = half(gelu(h));
+//   h = half(h * gelu'(dact[m,n]));  h = half(h + resid[m,n]);  C = h
+// or, for split-K, the float32 partial sums go to a workspace and a second
+// kernel adds the partials in a fixed order and rounds once.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <utility>
+
+#include "colsum.h"
+#include "common.h"
+
+namespace mpx {
+
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+// Clang vector types for 8- and 16-byte global accesses (a store through the
+// HIP uint2 / float4 structs is split into 4-byte stores)
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+
+struct GemmArgs {
+  const uint16_t* A;
+  const uint16_t* B;
+  uint16_t* C;
+  float* ws;  // split-K partials [splits][M][N] (when splits > 1)
+  int64_t M, N, K, lda, ldb, ldc;
+  int64_t sA0, sA1, sB0, sB1, sC0, sC1, nb1;
+  int32_t splits;
+  int64_t k_split;  // reduction length per split (multiple of the k tile)
+  const uint16_t* bias;
+  const uint16_t* resid;
+  int64_t ldr;
+  uint16_t* pre;
+  const uint16_t* dact;
+  int32_t act;
+  int32_t full_epi;  // set by the dispatcher: whole tiles may use gemm_epilogue_full
+};
+
+// Compile-time loop: f(std::integral_constant<int, I>) for I in [0, N).  The
+// accumulator tiles are indexed only with such constants, so they stay in
+// registers (a runtime index would force them into scratch memory).
+template <typename F, int... I>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
+  (f(std::integral_constant<int, I>{}), ...);
+}
+template <int N, typename F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+template <int DT>
+__device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
+  if constexpr (DT == MPX_F16) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
+                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
+  } else {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  }
+}
+
+// Loader of one operand tile (ROWS output rows x BK reduction values) into
+// registers, then into LDS as [row][k].  KMAJ: element (r,k) at base[r*ld + k];
+// otherwise at base[k*ld + r].
+template <int ROWS, int BK, int NT, bool KMAJ, bool VEC>
+struct TileLoader {
+  // k rows per lane for an mn-major operand: 4 when the tile is large enough,
+  // else 2, so that every lane owns whole units
+  static constexpr int KR = (ROWS * BK / 8) / NT >= 4 ? 4 : 2;
+  static constexpr int UNITS = KMAJ ? ROWS * BK / 8 : ROWS * BK / (8 * KR);
+  static constexpr int PER = UNITS / NT;                         // units per lane
+  static_assert(UNITS % NT == 0, "tile does not split evenly over the workgroup");
+  uint4 reg[KMAJ ? PER : PER * KR];
+
+  // rows_valid: rows r < rows_valid exist; k_valid: reduction values k < k_valid exist.
+  //
+  // VEC (16-byte aligned base, leading dimension a multiple of 8): every load
+  // is a plain 16-byte load with no branch, so the compiler keeps the next
+  // stage's loads in flight.  A vector that starts inside the matrix lies
+  // wholly inside its row's leading dimension (ld is a multiple of 8 and at
+  // least the row length), so it is loaded whole and its elements past the
+  // end are zeroed; a vector that starts outside is redirected to the tile's
+  // first vector (always inside) and zeroed entirely.
+  __device__ __forceinline__ static uint4 mask_vec(uint4 v, int nvalid) {
+    // keep elements [0, nvalid) of 8, zero the rest
+    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+    uint32_t o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t lo = 2 * q < nvalid ? 0x0000FFFFu : 0u;
+      const uint32_t hi = 2 * q + 1 < nvalid ? 0xFFFF0000u : 0u;
+      o[q] = w[q] & (lo | hi);
+    }
+    return make_uint4(o[0], o[1], o[2], o[3]);
+  }
+
+  // extent of the tile last loaded (the masking happens in store(), next to
+  // the LDS writes, so that nothing waits on the loads before then)
+  int rv_ = ROWS, kv_ = BK;
+
+  __device__ __forceinline__ void load(const uint16_t* __restrict__ base, int64_t ld, int rows_valid,
+                                       int k_valid, int tid) {
+    rv_ = rows_valid;
+    kv_ = k_valid;
+    // a whole tile (the common case) needs no clamping or masking; the test
+    // is uniform over the workgroup, so it costs one scalar branch
+    const bool full = rows_valid >= ROWS && k_valid >= BK;
+    if constexpr (!VEC) {
+      load_guarded(base, ld, rows_valid, k_valid, tid);
+    } else {
+#pragma unroll
+      for (int u = 0; u < PER; ++u) {
+        const int unit = tid + u * NT;
+        if constexpr (KMAJ) {
+          const int r = unit / (BK / 8);
+          const int k = (unit % (BK / 8)) * 8;
+          const bool inside = full || (r < rows_valid && k < k_valid);
+          const int64_t off = inside ? (int64_t)r * ld + k : 0;
+          reg[u] = *reinterpret_cast<const uint4*>(base + off);
+        } else {
+          const int r = (unit / (BK / KR)) * 8;
+          const int k = (unit % (BK / KR)) * KR;
+#pragma unroll
+          for (int q = 0; q < KR; ++q) {
+            const bool inside = full || (k + q < k_valid && r < rows_valid);
+            const int64_t off = inside ? (int64_t)(k + q) * ld + r : 0;
+            reg[u * KR + q] = *reinterpret_cast<const uint4*>(base + off);
+          }
+        }
+      }
+    }
+  }
+
+  __device__ __forceinline__ void load_guarded(const uint16_t* __restrict__ base, int64_t ld,
+                                               int rows_valid, int k_valid, int tid) {
+    auto pack8 = [](const uint16_t (&h)[8]) {
+      return make_uint4(h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16),
+                        h[4] | ((uint32_t)h[5] << 16), h[6] | ((uint32_t)h[7] << 16));
+    };
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int unit = tid + u * NT;
+      if constexpr (KMAJ) {
+        const int r = unit / (BK / 8);
+        const int k = (unit % (BK / 8)) * 8;
+        const uint16_t* p = base + (int64_t)r * ld + k;
+        uint16_t h[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) h[j] = (r < rows_valid && k + j < k_valid) ? p[j] : (uint16_t)0;
+        reg[u] = pack8(h);
+      } else {
+        const int r = (unit / (BK / KR)) * 8;
+        const int k = (unit % (BK / KR)) * KR;
+#pragma unroll
+        for (int q = 0; q < KR; ++q) {
+          const uint16_t* p = base + (int64_t)(k + q) * ld + r;
+          uint16_t h[8];
+#pragma unroll
+          for (int j = 0; j < 8; ++j) h[j] = (k + q < k_valid && r + j < rows_valid) ? p[j] : (uint16_t)0;
+          reg[u * KR + q] = pack8(h);
+        }
+      }
+    }
+  }
+
+  // LDS tile: ROWS rows of pitch LDSP halves.
+  template <int LDSP>
+  __device__ __forceinline__ void store(uint16_t* __restrict__ lds, int tid) const {
+    const int rv_ = this->rv_, kv_ = this->kv_;
+    const bool full = rv_ >= ROWS && kv_ >= BK;
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int unit = tid + u * NT;
+      if constexpr (KMAJ) {
+        const int r = unit / (BK / 8);
+        const int k = (unit % (BK / 8)) * 8;
+        uint4 v = reg[u];
+        if (VEC && !full) v = mask_vec(v, r < rv_ && k < kv_ ? min(8, kv_ - k) : 0);
+        *reinterpret_cast<uint4*>(lds + r * LDSP + k) = v;
+      } else {
+        const int r = (unit / (BK / KR)) * 8;
+        const int k = (unit % (BK / KR)) * KR;
+        // register transpose: lane holds rows k..k+KR-1 of 8 consecutive
+        // output indices; write output index r+j as KR consecutive k values
+        uint32_t w[KR][4];
+#pragma unroll
+        for (int q = 0; q < KR; ++q) {
+          uint4 v = reg[u * KR + q];
+          if (VEC && !full) v = mask_vec(v, k + q < kv_ && r < rv_ ? min(8, rv_ - r) : 0);
+          w[q][0] = v.x;
+          w[q][1] = v.y;
+          w[q][2] = v.z;
+          w[q][3] = v.w;
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const int i = j >> 1;
+          uint32_t d[KR / 2];
+#pragma unroll
+          for (int q = 0; q < KR / 2; ++q) {
+            const uint32_t a = w[2 * q][i], b = w[2 * q + 1][i];
+            d[q] = (j & 1) ? ((a >> 16) | (b & 0xFFFF0000u)) : ((a & 0xFFFFu) | (b << 16));
+          }
+          if constexpr (KR == 4)
+            *reinterpret_cast<uint2*>(lds + (r + j) * LDSP + k) = make_uint2(d[0], d[1]);
+          else
+            *reinterpret_cast<uint32_t*>(lds + (r + j) * LDSP + k) = d[0];
+        }
+      }
+    }
+  }
+};
+
+// Output tile of this workgroup.  Workgroups are dealt to the 8 XCDs
+// round-robin (workgroup w runs on XCD w % 8); they are renumbered so that
+// each XCD works through one contiguous range of tiles, and that range is
+// walked in groups of 8 tile rows, column by column, so the tiles an XCD
+// runs at the same time form a compact block: their A row panels and B
+// column panels are shared through that XCD's L2 instead of each B panel
+// being fetched again for every tile row.
+template <int BM, int BN>
+__device__ __forceinline__ void tile_origin(int64_t M, int64_t N, int64_t& m0, int64_t& n0) {
+  constexpr int64_t GM = 8;
+  const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
+  const int64_t ntiles = gridDim.x;
+  const int64_t xcd = blockIdx.x % 8, local = blockIdx.x / 8;
+  const int64_t t = xcd * (ntiles / 8) + min(xcd, ntiles % 8) + local;
+  const int64_t first = (t / (GM * tiles_n)) * GM;
+  const int64_t gm = min(tiles_m - first, GM);
+  const int64_t r = t - first * tiles_n;
+  m0 = (first + r % gm) * BM;
+  n0 = (r / gm) * BN;
+}
+
+// Epilogue variants chosen at compile time (a mask of these bits), used for
+// tiles that lie wholly inside the output when every epilogue operand is
+// 8-byte aligned: no per-element masks, no runtime flag tests, one 64-bit
+// base per wave and 32-bit lane offsets.  The arithmetic is the generic
+// epilogue's, step for step, so both give identical bits.
+enum : int { EPI_BIAS = 1, EPI_GELU = 2, EPI_DACT = 4, EPI_RESID = 8, EPI_GENERIC = -1 };
+
+// 4x4 transpose across each group of 4 lanes (two butterfly exchanges
+// through DPP quad permutations: lane ^ 1 is quad_perm [1,0,3,2], lane ^ 2 is
+// [2,3,0,1]): lane q of the group then holds row q of the 4 x 4 block.
+__device__ __forceinline__ void quad_transpose(float (&v)[4], int q4) {
+  auto xchg = [&](float& lo, float& hi_v, int st) {
+    const bool hi = (q4 & st) != 0;
+    const int send = __builtin_bit_cast(int, hi ? lo : hi_v);
+    const int got = st == 1 ? __builtin_amdgcn_mov_dpp(send, 0xB1, 0xF, 0xF, false)
+                            : __builtin_amdgcn_mov_dpp(send, 0x4E, 0xF, 0xF, false);
+    if (hi) lo = __builtin_bit_cast(float, got);
+    else hi_v = __builtin_bit_cast(float, got);
+  };
+  xchg(v[0], v[1], 1);
+  xchg(v[2], v[3], 1);
+  xchg(v[0], v[2], 2);
+  xchg(v[1], v[3], 2);
+}
+
+template <int DT, int TM, int TN, int E>
+__device__ __forceinline__ void gemm_epilogue_full(const GemmArgs& g, const f32x16 (&acc)[TM][TN],
+                                                   int64_t mw, int64_t nw, int lane, int64_t offC) {
+  const int q4 = lane & 3;
+  const int row_l = 4 * (lane >> 5) + q4;
+  const int col_l = 4 * ((lane & 31) >> 2);
+  const int64_t ldc = g.ldc;
+  const int64_t base = offC + mw * ldc + nw;           // wave-uniform
+  const uint32_t lane_off = (uint32_t)(row_l * ldc + col_l);
+  uint16_t* C = g.C + base;
+  uint16_t* pre = (E & EPI_GELU) ? g.pre + (mw * ldc + nw) : nullptr;
+  const uint16_t* dact = (E & EPI_DACT) ? g.dact + (mw * ldc + nw) : nullptr;
+  const uint16_t* res = (E & EPI_RESID) ? g.resid + (mw * g.ldr + nw) : nullptr;
+  const uint32_t res_off = (E & EPI_RESID) ? (uint32_t)(row_l * g.ldr + col_l) : 0u;
+  auto unpack = [](u32x2 w, float (&f)[4]) {
+    f[0] = h2f<DT>((uint16_t)(w.x & 0xFFFFu));
+    f[1] = h2f<DT>((uint16_t)(w.x >> 16));
+    f[2] = h2f<DT>((uint16_t)(w.y & 0xFFFFu));
+    f[3] = h2f<DT>((uint16_t)(w.y >> 16));
+  };
+  auto pack = [](const uint16_t (&h)[4]) {
+    return u32x2{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16)};
+  };
+  static_for<TN>([&](auto j) {
+    float bias[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if constexpr ((E & EPI_BIAS) != 0)
+      unpack(*reinterpret_cast<const u32x2*>(g.bias + nw + j * 32 + col_l), bias);
+    static_for<TM>([&](auto i) {
+      const f32x16 a = acc[i][j];
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        float v[4] = {a[4 * qd], a[4 * qd + 1], a[4 * qd + 2], a[4 * qd + 3]};
+        quad_transpose(v, q4);
+        const uint32_t rofs = (uint32_t)((i * 32 + 8 * qd) * ldc + j * 32);
+        const uint32_t off = lane_off + rofs;
+        uint16_t h[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(v[c] + bias[c]);
+        if constexpr ((E & EPI_GELU) != 0) {
+          *reinterpret_cast<u32x2*>(pre + off) = pack(h);
+#pragma unroll
+          for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(gelu_tanh(h2f<DT>(h[c])));
+        }
+        if constexpr ((E & EPI_DACT) != 0) {
+          float da[4];
+          unpack(*reinterpret_cast<const u32x2*>(dact + off), da);
+#pragma unroll
+          for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) * gelu_tanh_grad(da[c]));
+        }
+        if constexpr ((E & EPI_RESID) != 0) {
+          float r[4];
+          unpack(*reinterpret_cast<const u32x2*>(
+                     res + res_off + (uint32_t)((i * 32 + 8 * qd) * g.ldr + j * 32)), r);
+#pragma unroll
+          for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) + r[c]);
+        }
+        *reinterpret_cast<u32x2*>(C + off) = pack(h);
+      }
+    });
+  });
+}
+
+// Epilogue shared by the GEMM kernels: the wave's TM x TN accumulator
+// blocks of 32 x 32 start at output row mw and column nw.
+template <int DT, int TM, int TN>
+__device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const f32x16 (&acc)[TM][TN],
+                                              int64_t mw, int64_t nw, int lane, int split,
+                                              int64_t offC) {
+  // The accumulators of a 32x32 block hold, per lane, one column and 4 runs
+  // of 4 consecutive rows.  A 4x4 transpose across each group of 4 lanes
+  // (two butterfly exchanges) turns every run into 4 consecutive columns of
+  // one row, so bias / residual / activation inputs are read and outputs
+  // written 4 elements (8 bytes; 16 for float partials) at a time.
+  const int q4 = lane & 3;
+  const int row_l = 4 * (lane >> 5) + q4;        // row within an 8-row group
+  const int col_l = 4 * ((lane & 31) >> 2);      // first of the lane's 4 columns
+  // exchange (p, p + st) pairs with the lane st apart (st = 1 or 2) through a
+  // DPP quad permutation (lane ^ 1: quad_perm [1,0,3,2]; lane ^ 2: [2,3,0,1])
+  auto xchg = [&](float& lo, float& hi_v, int st) {
+    const bool hi = (q4 & st) != 0;
+    const int send = __builtin_bit_cast(int, hi ? lo : hi_v);
+    const int got = st == 1 ? __builtin_amdgcn_mov_dpp(send, 0xB1, 0xF, 0xF, false)
+                            : __builtin_amdgcn_mov_dpp(send, 0x4E, 0xF, 0xF, false);
+    if (hi) lo = __builtin_bit_cast(float, got);
+    else hi_v = __builtin_bit_cast(float, got);
+  };
+  auto transpose4 = [&](float (&v)[4]) {
+    xchg(v[0], v[1], 1);
+    xchg(v[2], v[3], 1);
+    xchg(v[0], v[2], 2);
+    xchg(v[1], v[3], 2);
+  };
+  auto al8 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; };
+  if (g.splits > 1) {
+    float* W = g.ws + (int64_t)split * g.M * g.N;
+    const bool v16 = g.N % 4 == 0 && (reinterpret_cast<uintptr_t>(W) & 15u) == 0;
+    static_for<TM>([&](auto i) {
+      static_for<TN>([&](auto j) {
+        const f32x16 a = acc[i][j];
+#pragma unroll
+        for (int qd = 0; qd < 4; ++qd) {
+          float v[4] = {a[4 * qd], a[4 * qd + 1], a[4 * qd + 2], a[4 * qd + 3]};
+          transpose4(v);
+          const int64_t m = mw + i * 32 + 8 * qd + row_l;
+          const int64_t n = nw + j * 32 + col_l;
+          if (m < g.M && n < g.N) {
+            float* out = W + m * g.N + n;
+            if (v16 && n + 4 <= g.N) *reinterpret_cast<f32x4*>(out) = f32x4{v[0], v[1], v[2], v[3]};
+            else
+#pragma unroll
+              for (int c = 0; c < 4; ++c)
+                if (n + c < g.N) out[c] = v[c];
+          }
+        }
+      });
+    });
+    return;
+  }
+  uint16_t* C = g.C + offC;
+  const bool v8 = g.ldc % 4 == 0 && al8(C) && (!g.pre || al8(g.pre)) && (!g.dact || al8(g.dact)) &&
+                  (!g.resid || (al8(g.resid) && g.ldr % 4 == 0)) && (!g.bias || al8(g.bias));
+  auto ld4 = [&](const uint16_t* p, bool vec, int nv, uint16_t (&d)[4]) {
+    if (vec) {
+      const u32x2 w = *reinterpret_cast<const u32x2*>(p);
+      d[0] = (uint16_t)(w.x & 0xFFFFu);
+      d[1] = (uint16_t)(w.x >> 16);
+      d[2] = (uint16_t)(w.y & 0xFFFFu);
+      d[3] = (uint16_t)(w.y >> 16);
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c) d[c] = c < nv ? p[c] : (uint16_t)0;
+    }
+  };
+  auto st4 = [&](uint16_t* p, bool vec, int nv, const uint16_t (&d)[4]) {
+    if (vec) {
+      *reinterpret_cast<u32x2*>(p) = u32x2{d[0] | ((uint32_t)d[1] << 16), d[2] | ((uint32_t)d[3] << 16)};
+    } else {
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (c < nv) p[c] = d[c];
+    }
+  };
+  static_for<TM>([&](auto i) {
+    static_for<TN>([&](auto j) {
+      const f32x16 a = acc[i][j];
+      const int64_t n = nw + j * 32 + col_l;
+      const int nv = (int)max<int64_t>(0, min<int64_t>(4, g.N - n));
+      const bool vec = v8 && nv == 4;
+      uint16_t bias[4] = {0, 0, 0, 0};
+      if (g.bias && nv > 0) ld4(g.bias + n, vec, nv, bias);
+#pragma unroll
+      for (int qd = 0; qd < 4; ++qd) {
+        float v[4] = {a[4 * qd], a[4 * qd + 1], a[4 * qd + 2], a[4 * qd + 3]};
+        transpose4(v);
+        const int64_t m = mw + i * 32 + 8 * qd + row_l;
+        if (m >= g.M || nv == 0) continue;
+        uint16_t h[4], da[4], res[4];
+        if (g.dact) ld4(g.dact + m * g.ldc + n, vec, nv, da);
+        if (g.resid) ld4(g.resid + m * g.ldr + n, vec, nv, res);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(v[c] + (g.bias ? h2f<DT>(bias[c]) : 0.0f));
+        if (g.pre) st4(g.pre + m * g.ldc + n, vec, nv, h);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          uint16_t o = h[c];
+          if (g.act == MPX_ACT_GELU_TANH) o = f2h<DT>(gelu_tanh(h2f<DT>(o)));
+          if (g.dact) o = f2h<DT>(h2f<DT>(o) * gelu_tanh_grad(h2f<DT>(da[c])));
+          if (g.resid) o = f2h<DT>(h2f<DT>(o) + h2f<DT>(res[c]));
+          h[c] = o;
+        }
+        st4(C + m * g.ldc + n, vec, nv, h);
+      }
+    });
+  });
+}
+
+// OCC: waves per SIMD the register budget is sized for.
+template <int DT, int BM, int BN, int BK, int WM, int WN, bool AK, bool BKM, bool VEC, int OCC>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(OCC, OCC)))
+void gemm_kernel(GemmArgs g) {
+  constexpr int NW = (BM / WM) * (BN / WN);
+  constexpr int NT = NW * 64;
+  constexpr int PAD = 8;
+  constexpr int LDSP = BK + PAD;
+  constexpr int TM = WM / 32, TN = WN / 32;
+  // one LDS block: the double-buffered A and B tiles during the main loop,
+  // then the float32 staging area of the epilogue
+  __shared__ __attribute__((aligned(16))) uint16_t smem[2 * (BM + BN) * LDSP];
+  uint16_t (*sA)[BM * LDSP] = reinterpret_cast<uint16_t (*)[BM * LDSP]>(smem);
+  uint16_t (*sB)[BN * LDSP] = reinterpret_cast<uint16_t (*)[BN * LDSP]>(smem + 2 * BM * LDSP);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm0 = (wave / (BN / WN)) * WM;
+  const int wn0 = (wave % (BN / WN)) * WN;
+
+  int64_t m0, n0;
+  tile_origin<BM, BN>(g.M, g.N, m0, n0);
+  // batch / split
+  int64_t z = blockIdx.y;
+  int split = 0;
+  int64_t offA = 0, offB = 0, offC = 0;
+  if (g.splits > 1) {
+    split = (int)z;
+  } else {
+    const int64_t i0 = z / g.nb1, i1 = z % g.nb1;
+    offA = i0 * g.sA0 + i1 * g.sA1;
+    offB = i0 * g.sB0 + i1 * g.sB1;
+    offC = i0 * g.sC0 + i1 * g.sC1;
+  }
+  const int64_t kbeg = (int64_t)split * g.k_split;
+  const int64_t kend = min(g.K, kbeg + g.k_split);
+  const int nk = (int)((kend - kbeg + BK - 1) / BK);
+
+  const uint16_t* A = g.A + offA;
+  const uint16_t* B = g.B + offB;
+  // operand tile base pointers at k = kbeg
+  const uint16_t* Ab = AK ? A + m0 * g.lda + kbeg : A + kbeg * g.lda + m0;
+  const uint16_t* Bb = BKM ? B + n0 * g.ldb + kbeg : B + kbeg * g.ldb + n0;
+  const int64_t Astep = AK ? BK : BK * g.lda;
+  const int64_t Bstep = BKM ? BK : BK * g.ldb;
+  const int rowsA = (int)min<int64_t>(BM, g.M - m0);
+  const int rowsB = (int)min<int64_t>(BN, g.N - n0);
+
+  // One register stage: the loads of k tile kt+1 are issued before the MFMAs
+  // of tile kt and land in LDS (the other buffer) after them.
+  TileLoader<BM, BK, NT, AK, VEC> la;
+  TileLoader<BN, BK, NT, BKM, VEC> lb;
+
+  f32x16 acc[TM][TN];
+  static_for<TM>([&](auto i) {
+    static_for<TN>([&](auto j) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+    });
+  });
+
+  auto kvalid = [&](int kt) { return (int)min<int64_t>(BK, kend - (kbeg + (int64_t)kt * BK)); };
+  if (nk > 0) {
+    la.load(Ab, g.lda, rowsA, kvalid(0), tid);
+    lb.load(Bb, g.ldb, rowsB, kvalid(0), tid);
+    la.template store<LDSP>(sA[0], tid);
+    lb.template store<LDSP>(sB[0], tid);
+  }
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int c = kt & 1;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      la.load(Ab + (kt + 1) * Astep, g.lda, rowsA, kvalid(kt + 1), tid);
+      lb.load(Bb + (kt + 1) * Bstep, g.ldb, rowsB, kvalid(kt + 1), tid);
+    }
+    const uint16_t* a_s = sA[c];
+    const uint16_t* b_s = sB[c];
+#pragma unroll
+    for (int kk = 0; kk < BK / 16; ++kk) {
+      const int kofs = kk * 16 + 8 * (lane >> 5);
+      uint4 af[TM], bf[TN];
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+        af[i] = *reinterpret_cast<const uint4*>(a_s + (wm0 + i * 32 + (lane & 31)) * LDSP + kofs);
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        bf[j] = *reinterpret_cast<const uint4*>(b_s + (wn0 + j * 32 + (lane & 31)) * LDSP + kofs);
+      static_for<TM>([&](auto i) {
+        static_for<TN>([&](auto j) { acc[i][j] = mfma32<DT>(af[i], bf[j], acc[i][j]); });
+      });
+    }
+    if (more) {
+      la.template store<LDSP>(sA[c ^ 1], tid);
+      lb.template store<LDSP>(sB[c ^ 1], tid);
+    }
+    __syncthreads();
+  }
+
+  gemm_epilogue<DT, TM, TN>(g, acc, m0 + wm0, n0 + wn0, lane, split, offC);
+}
+
+// ------------------------------------------------- direct-to-LDS kernel --
+//
+// The main loop of the kernel below moves operand tiles from global memory
+// straight into LDS (global_load_lds_dwordx4: each lane's 16 bytes land at
+// M0 + 16 * lane, so one wave instruction fills 1 KiB of LDS) and keeps
+// S - 1 k tiles of 64 in flight while the MFMAs consume the oldest one.  No
+// registers stage the tiles, so deep pipelines cost LDS only.  The compiler
+// does not track these copies: each k step waits for its own tile with an
+// explicit vmcnt and one barrier makes the tile visible to every wave.
+//
+// LDS layouts (no padding: a copy fills 1 KiB contiguously, so bank
+// conflicts are avoided by permuting 16-byte chunks instead):
+//   k-major operand   [row][64 k], 128 B per row; chunk c of row r sits at
+//                     position c ^ ((r >> 1) & 7).  The 16 lanes reading one
+//                     ds_read_b128 phase (16 rows, one chunk) hit all 64 banks.
+//   mn-major operand  [k][ROWS] (ROWS = 128 or 256 outputs, 16 or 32 chunks
+//                     per k row); chunk c of k row kr sits at c ^ (4*(kr & 3)).
+//                     MFMA fragments are read with ds_read_b64_tr_b16, which
+//                     transposes 16-bit elements across groups of 16 lanes, so
+//                     the operand needs no transposition on the way in.
+// Requirements (checked by the dispatcher): 16-byte aligned operands with
+// leading dimensions and batch strides that are multiples of 8, and every
+// split's k range a multiple of 64.  Rows past M or N read clamped (valid)
+// addresses; their results are never stored.
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// 16 bytes per lane from base + off (bytes) into LDS at lds + 16 * lane
+__device__ __forceinline__ void dma16(const void* base, uint32_t off, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+               :
+               : "v"(off), "s"(base), "s"(lds)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+__device__ __forceinline__ uint32_t lds_u32(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint2 lds_tr_b64(uint32_t addr) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s16x4*)(uintptr_t)addr);
+  return __builtin_bit_cast(uint2, v);
+}
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint4 lds_b128(uint32_t addr) {
+  const u32x4 v = *(const __attribute__((address_space(3))) u32x4*)(uintptr_t)addr;
+  return __builtin_bit_cast(uint4, v);
+}
+
+// One operand of the direct-to-LDS kernel: ROWS output rows (of M or N) by
+// 64 k per stage, copied by NWAVES waves, Q copies per wave.
+template <int ROWS, bool KMAJ, int NWAVES>
+struct DmaOperand {
+  static constexpr int BLOCKS = ROWS / 8;  // 1 KiB copies per stage
+  static constexpr int Q = BLOCKS / NWAVES;
+  static_assert(BLOCKS % NWAVES == 0, "copies do not split evenly over the waves");
+  static_assert(KMAJ || ROWS == 128 || ROWS == 256, "mn-major tiles are 128 or 256 wide");
+  uint32_t off[Q];  // per-lane byte offsets of the copies, relative to the tile base
+  int64_t step;     // bytes from one k tile to the next
+
+  // rv: valid rows (>= 1) of the tile; ld: leading dimension in elements
+  __device__ __forceinline__ void init(int64_t ld, int rv, int wave, int lane) {
+    if constexpr (KMAJ) {
+      step = 128;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int r = 8 * (wave + NWAVES * q) + (lane >> 3);
+        const int c = (lane & 7) ^ ((r >> 1) & 7);
+        off[q] = (uint32_t)(min(r, rv - 1) * ld * 2 + c * 16);
+      }
+    } else {
+      constexpr int CH = ROWS / 8;   // 16-byte chunks per k row
+      constexpr int RPB = 64 / CH;   // k rows per 1 KiB copy
+      step = 64 * ld * 2;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int kr = RPB * (wave + NWAVES * q) + lane / CH;
+        const int c = (lane % CH) ^ (4 * (kr & 3));
+        off[q] = (uint32_t)(kr * ld * 2 + (8 * c < rv ? 16 * c : 0));
+      }
+    }
+  }
+  // copy the tile whose first element is at base into LDS at lds
+  __device__ __forceinline__ void issue(const uint16_t* base, uint32_t lds, int wave) const {
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+      dma16(base, off[q], lds + 1024u * (uint32_t)(wave + NWAVES * q));
+  }
+};
+
+// Per-lane LDS byte offsets of the MFMA fragments of one operand, for a
+// wave whose rows start at w0 within the tile (relative to the tile base).
+template <int ROWS, bool KMAJ, int T>
+struct FragReader {
+  uint32_t base[KMAJ ? 4 : T];
+  __device__ __forceinline__ void init(int w0, int lane) {
+    if constexpr (KMAJ) {
+      const int r = w0 + (lane & 31);
+      const int sw = (r >> 1) & 7;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) base[kk] = (uint32_t)(r * 128 + (((2 * kk + (lane >> 5)) ^ sw) << 4));
+    } else {
+      const int g = lane >> 4, e = (lane >> 2) & 3, t = lane & 3;
+      const int kr = 8 * (g >> 1) + e;  // + 16 kk + 4 h
+#pragma unroll
+      for (int i = 0; i < T; ++i) {
+        const int m = w0 + 32 * i + 16 * (g & 1) + 4 * t;
+        base[i] = (uint32_t)(kr * ROWS * 2 + (((m >> 3) ^ (4 * e)) << 4) + (m & 7) * 2);
+      }
+    }
+  }
+  // fragment i (rows w0 + 32 i ..) at k step kk of the tile at lds
+  template <int I, int KK>
+  __device__ __forceinline__ uint4 read(uint32_t lds) const {
+    if constexpr (KMAJ) {
+      return lds_b128(lds + base[KK] + I * 32 * 128);
+    } else {
+      const uint2 lo = lds_tr_b64(lds + base[I] + KK * 16 * ROWS * 2);
+      const uint2 hi = lds_tr_b64(lds + base[I] + KK * 16 * ROWS * 2 + 4 * ROWS * 2);
+      return make_uint4(lo.x, lo.y, hi.x, hi.y);
+    }
+  }
+};
+
+// OCC: waves per SIMD the register budget is sized for.  E: the epilogue
+// variant of whole tiles (EPI_GENERIC: always the generic epilogue).
+template <int DT, int BM, int BN, int WM, int WN, int S, int OCC, bool AK, bool BKM, int E>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(OCC, OCC)))
+void gemm_dma_kernel(GemmArgs g) {
+  constexpr int NWAVES = (BM / WM) * (BN / WN);
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int A_BYTES = BM * 64 * 2, B_BYTES = BN * 64 * 2;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int L = (BM + BN) / 8 / NWAVES;  // copies per lane per stage
+  static_assert((S - 2) * L <= 63, "vmcnt range");
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[S * STAGE];
+  const uint32_t lds0 = lds_u32(smem);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm0 = (wave / (BN / WN)) * WM;
+  const int wn0 = (wave % (BN / WN)) * WN;
+
+  int64_t m0, n0;
+  tile_origin<BM, BN>(g.M, g.N, m0, n0);
+  int64_t z = blockIdx.y;
+  int split = 0;
+  int64_t offA = 0, offB = 0, offC = 0;
+  if (g.splits > 1) {
+    split = (int)z;
+  } else {
+    const int64_t i0 = z / g.nb1, i1 = z % g.nb1;
+    offA = i0 * g.sA0 + i1 * g.sA1;
+    offB = i0 * g.sB0 + i1 * g.sB1;
+    offC = i0 * g.sC0 + i1 * g.sC1;
+  }
+  const int64_t kbeg = (int64_t)split * g.k_split;
+  const int64_t kend = min(g.K, kbeg + g.k_split);
+  const int nk = (int)((kend - kbeg) / 64);
+
+  const uint16_t* Ab = g.A + offA + (AK ? m0 * g.lda + kbeg : kbeg * g.lda + m0);
+  const uint16_t* Bb = g.B + offB + (BKM ? n0 * g.ldb + kbeg : kbeg * g.ldb + n0);
+  DmaOperand<BM, AK, NWAVES> da;
+  DmaOperand<BN, BKM, NWAVES> db;
+  da.init(g.lda, (int)min<int64_t>(BM, g.M - m0), wave, lane);
+  db.init(g.ldb, (int)min<int64_t>(BN, g.N - n0), wave, lane);
+  FragReader<BM, AK, TM> fa;
+  FragReader<BN, BKM, TN> fb;
+  fa.init(wm0, lane);
+  fb.init(wn0, lane);
+
+  f32x16 acc[TM][TN];
+  static_for<TM>([&](auto i) {
+    static_for<TN>([&](auto j) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+    });
+  });
+
+  auto issue = [&](int kt) {
+    const uint32_t st = lds0 + (uint32_t)((kt % S) * STAGE);
+    da.issue(reinterpret_cast<const uint16_t*>(reinterpret_cast<const uint8_t*>(Ab) + kt * da.step), st, wave);
+    db.issue(reinterpret_cast<const uint16_t*>(reinterpret_cast<const uint8_t*>(Bb) + kt * db.step),
+             st + A_BYTES, wave);
+  };
+#pragma unroll
+  for (int s = 0; s < S - 1; ++s)
+    if (s < nk) issue(s);
+
+  for (int kt = 0; kt < nk; ++kt) {
+    // tile kt has landed once at most min(S - 2, nk - 1 - kt) later tiles are in flight
+    const int later = min(S - 2, nk - 1 - kt);
+    static_for<S - 1>([&](auto p) {
+      if (later == p) wait_vmcnt<p * L>();
+    });
+    __syncthreads();
+    if (kt + S - 1 < nk) issue(kt + S - 1);
+    const uint32_t sa = lds0 + (uint32_t)((kt % S) * STAGE), sb = sa + A_BYTES;
+    // fragments double-buffered over the four k steps of 16: the LDS reads
+    // of step kk + 1 are issued ahead of the MFMAs of step kk (the scheduling
+    // barriers keep the compiler from sinking them next to their uses)
+    uint4 af[2][TM], bf[2][TN];
+    static_for<TM>([&](auto i) { af[0][i] = fa.template read<i, 0>(sa); });
+    static_for<TN>([&](auto j) { bf[0][j] = fb.template read<j, 0>(sb); });
+    static_for<4>([&](auto kk) {
+      constexpr int cur = kk & 1, nxt = cur ^ 1;
+      if constexpr (kk + 1 < 4) {
+        static_for<TM>([&](auto i) { af[nxt][i] = fa.template read<i, kk + 1>(sa); });
+        static_for<TN>([&](auto j) { bf[nxt][j] = fb.template read<j, kk + 1>(sb); });
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      static_for<TM>([&](auto i) {
+        static_for<TN>([&](auto j) { acc[i][j] = mfma32<DT>(af[cur][i], bf[cur][j], acc[i][j]); });
+      });
+      __builtin_amdgcn_sched_barrier(0);
+    });
+  }
+  if constexpr (E != EPI_GENERIC) {
+    if (g.full_epi && m0 + BM <= g.M && n0 + BN <= g.N) {
+      gemm_epilogue_full<DT, TM, TN, E>(g, acc, m0 + wm0, n0 + wn0, lane, offC);
+      return;
+    }
+  }
+  gemm_epilogue<DT, TM, TN>(g, acc, m0 + wm0, n0 + wn0, lane, split, offC);
+}
+
+// Sum of split-K partials in split order, one rounding: C = half(sum_s W[s]).
+template <int DT>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ ws, int splits,
+                                                            int64_t MN, uint16_t* __restrict__ C) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= MN) return;
+  float s = ws[i];
+  for (int k = 1; k < splits; ++k) s += ws[(int64_t)k * MN + i];
+  C[i] = f2h<DT>(s);
+}
+
+// ------------------------------------------------------------ dispatch --
+
+struct Cfg {
+  int bm, bn;
+};
+
+static bool aligned_vec(const void* p, int64_t ld, int64_t s0, int64_t s1) {
+  return (reinterpret_cast<uintptr_t>(p) & 15u) == 0 && ld % 8 == 0 && s0 % 8 == 0 && s1 % 8 == 0;
+}
+
+template <int DT, int BM, int BN, int WM, int WN, int BK = 64, int OCC = 2>
+static hipError_t launch_cfg(const GemmArgs& g, bool ak, bool bk, bool vec, int64_t nbatch,
+                             hipStream_t s) {
+  constexpr int NT = (BM / WM) * (BN / WN) * 64;
+  const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  dim3 grid((unsigned)tiles, (unsigned)(g.splits > 1 ? g.splits : nbatch));
+#define MPX_G(AKv, BKv, VECv) \
+  gemm_kernel<DT, BM, BN, BK, WM, WN, AKv, BKv, VECv, OCC><<<grid, NT, 0, s>>>(g)
+  if (vec) {
+    if (ak && bk) MPX_G(true, true, true);
+    else if (ak && !bk) MPX_G(true, false, true);
+    else if (!ak && bk) MPX_G(false, true, true);
+    else MPX_G(false, false, true);
+  } else if constexpr (BM * BN <= 128 * 128) {  // unaligned operands: small tiles only
+    if (ak && bk) MPX_G(true, true, false);
+    else if (ak && !bk) MPX_G(true, false, false);
+    else if (!ak && bk) MPX_G(false, true, false);
+    else MPX_G(false, false, false);
+  } else {
+    return hipErrorInvalidValue;
+  }
+#undef MPX_G
+  return hipGetLastError();
+}
+
+// Epilogue mask of a call, or EPI_GENERIC when it has no compiled variant
+static int epilogue_mask(const GemmArgs& g) {
+  if (g.splits > 1) return EPI_GENERIC;
+  return (g.bias ? EPI_BIAS : 0) | (g.act == MPX_ACT_GELU_TANH ? EPI_GELU : 0) |
+         (g.dact ? EPI_DACT : 0) | (g.resid ? EPI_RESID : 0);
+}
+
+// Whole-tile epilogue preconditions that do not depend on the tile: every
+// epilogue operand 8-byte aligned with row strides a multiple of 4, and the
+// per-lane 32-bit offsets in range.
+static bool full_epilogue_ok(const GemmArgs& g, int bm) {
+  auto al8 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; };
+  const bool strides = g.sC0 % 4 == 0 && g.sC1 % 4 == 0;
+  return g.splits == 1 && strides && g.ldc % 4 == 0 && al8(g.C) && (!g.bias || al8(g.bias)) &&
+         (!g.pre || al8(g.pre)) && (!g.dact || al8(g.dact)) &&
+         (!g.resid || (al8(g.resid) && g.ldr % 4 == 0)) && g.ldc * bm < ((int64_t)1 << 30) &&
+         g.ldr * bm < ((int64_t)1 << 30);
+}
+
+template <int DT, int BM, int BN, int WM, int WN, int S, int OCC>
+static hipError_t launch_dma(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipStream_t s) {
+  constexpr int NT = (BM / WM) * (BN / WN) * 64;
+  const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  dim3 grid((unsigned)tiles, (unsigned)(g.splits > 1 ? g.splits : nbatch));
+  g.full_epi = full_epilogue_ok(g, BM) ? 1 : 0;
+  const int e = g.full_epi ? epilogue_mask(g) : EPI_GENERIC;
+#define MPX_D(AKv, BKv, Ev) gemm_dma_kernel<DT, BM, BN, WM, WN, S, OCC, AKv, BKv, Ev><<<grid, NT, 0, s>>>(g)
+  if constexpr (BM == 128 && BN == 128 && S == 2) {
+    // the configuration the dispatcher picks: whole tiles get the
+    // specialised epilogue of each call pattern of the training step
+    if (ak && bk) {
+      switch (e) {
+        case 0: MPX_D(true, true, 0); break;
+        case EPI_BIAS: MPX_D(true, true, EPI_BIAS); break;
+        case EPI_BIAS | EPI_GELU: MPX_D(true, true, EPI_BIAS | EPI_GELU); break;
+        case EPI_BIAS | EPI_RESID: MPX_D(true, true, EPI_BIAS | EPI_RESID); break;
+        default: MPX_D(true, true, EPI_GENERIC);
+      }
+    } else if (ak && !bk) {
+      switch (e) {
+        case 0: MPX_D(true, false, 0); break;
+        case EPI_DACT: MPX_D(true, false, EPI_DACT); break;
+        default: MPX_D(true, false, EPI_GENERIC);
+      }
+    } else if (!ak && bk) {
+      if (e == 0) MPX_D(false, true, 0);
+      else MPX_D(false, true, EPI_GENERIC);
+    } else {
+      if (e == 0) MPX_D(false, false, 0);
+      else MPX_D(false, false, EPI_GENERIC);
+    }
+  } else {
+    if (ak && bk) MPX_D(true, true, EPI_GENERIC);
+    else if (ak && !bk) MPX_D(true, false, EPI_GENERIC);
+    else if (!ak && bk) MPX_D(false, true, EPI_GENERIC);
+    else MPX_D(false, false, EPI_GENERIC);
+  }
+#undef MPX_D
+  return hipGetLastError();
+}
+
+// Tile configurations (the value of mpx_gemm_set_config):
+//   1  register-staged 64 x 64, 4 waves          (any operands)
+//   2  register-staged 128 x 128, 8 waves        (16-byte aligned operands)
+//   3  direct-to-LDS 256 x 256, 4 waves, 2 stages
+//   4  direct-to-LDS 256 x 128, 4 waves, 3 stages
+//   5  direct-to-LDS 128 x 256, 4 waves, 3 stages
+//   6  direct-to-LDS 128 x 128, 4 waves, 4 stages
+//   7  direct-to-LDS 128 x 128, 4 waves, 2 stages, two workgroups per CU
+extern int g_forced_config;  // defined in gemm.hip
+
+// The direct-to-LDS kernel needs 16-byte aligned operands and whole k tiles
+// of 64 in every split, and 32-bit per-lane copy offsets.
+static bool dma_ok(const GemmArgs& g, bool vec, bool ak, bool bk) {
+  if (!vec || g.K % 64 != 0) return false;
+  if (g.splits > 1 && g.k_split % 64 != 0) return false;
+  const int64_t lim = (int64_t)1 << 31;
+  const int64_t spanA = (ak ? 256 : 64) * g.lda * 2, spanB = (bk ? 256 : 64) * g.ldb * 2;
+  return spanA < lim && spanB < lim;
+}
+
+// Measured on MI355X over the transformer layer shapes (M 8320..25216, N and K
+// 384..3072) and 8192^3: configuration 7 (two co-resident workgroups hide
+// each other's epilogue and pipeline bubbles) is the fastest direct-to-LDS
+// variant for every shape, forward and backward; the register-staged
+// kernels serve operands the copies cannot take.
+static int choose_config(const GemmArgs& g, bool vec, bool ak, bool bk) {
+  const bool dma = dma_ok(g, vec, ak, bk);
+  const int f = g_forced_config;
+  if (f >= 3 && dma) return f;
+  if (f == 1 || (f == 2 && vec)) return f;
+  if (g.M <= 64 || g.N <= 64) return 1;
+  if (dma) return 7;
+  return vec ? 2 : 0;
+}
+
+// ak: A is k-major; bk: B is k-major.
+template <int DT>
+static hipError_t run_gemm(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipStream_t s) {
+  const bool vec = aligned_vec(g.A, g.lda, g.sA0, g.sA1) && aligned_vec(g.B, g.ldb, g.sB0, g.sB1);
+  switch (choose_config(g, vec, ak, bk)) {
+    case 1: return launch_cfg<DT, 64, 64, 32, 32>(g, ak, bk, vec, nbatch, s);
+    case 2: return launch_cfg<DT, 128, 128, 64, 32, 64, 4>(g, ak, bk, vec, nbatch, s);
+    case 3: return launch_dma<DT, 256, 256, 128, 128, 2, 1>(g, ak, bk, nbatch, s);
+    case 4: return launch_dma<DT, 256, 128, 128, 64, 3, 1>(g, ak, bk, nbatch, s);
+    case 5: return launch_dma<DT, 128, 256, 64, 128, 3, 1>(g, ak, bk, nbatch, s);
+    case 6: return launch_dma<DT, 128, 128, 64, 64, 4, 1>(g, ak, bk, nbatch, s);
+    case 7: return launch_dma<DT, 128, 128, 64, 64, 2, 2>(g, ak, bk, nbatch, s);
+    default:  // unaligned operands (rare: odd leading dimensions)
+      return launch_cfg<DT, 128, 128, 64, 64>(g, ak, bk, vec, nbatch, s);
+  }
+}
+
+hipError_t run_gemm_f16(const GemmArgs& g, bool ak, bool bk, int64_t nbatch, hipStream_t s);
+hipError_t run_gemm_bf16(const GemmArgs& g, bool ak, bool bk, int64_t nbatch, hipStream_t s);
+
+}  // namespace mpx
