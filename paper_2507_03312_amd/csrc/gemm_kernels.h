@@ -283,17 +283,24 @@ __device__ __forceinline__ void quad_transpose(float (&v)[4], int q4) {
 template <int DT, int TM, int TN, int E>
 __device__ __forceinline__ void gemm_epilogue_full(const GemmArgs& g, const f32x16 (&acc)[TM][TN],
                                                    int64_t mw, int64_t nw, int lane, int64_t offC) {
+  static_assert(TN % 2 == 0, "column blocks are paired");
   const int q4 = lane & 3;
-  const int row_l = 4 * (lane >> 5) + q4;
+  const int hi = lane >> 5;
+  const int row_l = 4 * hi + q4;
   const int col_l = 4 * ((lane & 31) >> 2);
   const int64_t ldc = g.ldc;
-  const int64_t base = offC + mw * ldc + nw;           // wave-uniform
-  const uint32_t lane_off = (uint32_t)(row_l * ldc + col_l);
-  uint16_t* C = g.C + base;
+  uint16_t* C = g.C + (offC + mw * ldc + nw);         // wave-uniform bases
   uint16_t* pre = (E & EPI_GELU) ? g.pre + (mw * ldc + nw) : nullptr;
   const uint16_t* dact = (E & EPI_DACT) ? g.dact + (mw * ldc + nw) : nullptr;
   const uint16_t* res = (E & EPI_RESID) ? g.resid + (mw * g.ldr + nw) : nullptr;
+  // inputs are read where the accumulators sit: row row_l, columns col_l..+3
+  const uint32_t in_off = (uint32_t)(row_l * ldc + col_l);
   const uint32_t res_off = (E & EPI_RESID) ? (uint32_t)(row_l * g.ldr + col_l) : 0u;
+  // outputs are written after pairing the column blocks (2p, 2p + 1): a lane
+  // then holds row q4 (first block of the pair) or 4 + q4 (second) of the
+  // 8-row group, columns 32 * hi + col_l, so one store covers 4 rows x 64
+  // columns = whole 128-byte row segments
+  const uint32_t out_off = (uint32_t)(q4 * ldc + 32 * hi + col_l);
   auto unpack = [](u32x2 w, float (&f)[4]) {
     f[0] = h2f<DT>((uint16_t)(w.x & 0xFFFFu));
     f[1] = h2f<DT>((uint16_t)(w.x >> 16));
@@ -303,40 +310,66 @@ __device__ __forceinline__ void gemm_epilogue_full(const GemmArgs& g, const f32x
   auto pack = [](const uint16_t (&h)[4]) {
     return u32x2{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16)};
   };
-  static_for<TN>([&](auto j) {
-    float bias[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    if constexpr ((E & EPI_BIAS) != 0)
-      unpack(*reinterpret_cast<const u32x2*>(g.bias + nw + j * 32 + col_l), bias);
+  // exchange the upper lane half of x with the lower lane half of y
+  auto pair_swap = [](u32x2& x, u32x2& y) {
+    const auto r0 = __builtin_amdgcn_permlane32_swap(x.x, y.x, false, false);
+    const auto r1 = __builtin_amdgcn_permlane32_swap(x.y, y.y, false, false);
+    x = u32x2{r0[0], r1[0]};
+    y = u32x2{r0[1], r1[1]};
+  };
+  // the epilogue of one 4-value run of block (i, j): returns the packed
+  // output and (with GELU) the packed pre-activation
+  auto run = [&](const f32x16& a, int i, int j, int qd, const float (&bias)[4], u32x2& out,
+                 u32x2& pre_out) {
+    float v[4] = {a[4 * qd], a[4 * qd + 1], a[4 * qd + 2], a[4 * qd + 3]};
+    quad_transpose(v, q4);
+    const uint32_t rofs = (uint32_t)((i * 32 + 8 * qd) * ldc + j * 32);
+    uint16_t h[4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(v[c] + bias[c]);
+    if constexpr ((E & EPI_GELU) != 0) {
+      pre_out = pack(h);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(gelu_tanh(h2f<DT>(h[c])));
+    }
+    if constexpr ((E & EPI_DACT) != 0) {
+      float da[4];
+      unpack(*reinterpret_cast<const u32x2*>(dact + in_off + rofs), da);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) * gelu_tanh_grad(da[c]));
+    }
+    if constexpr ((E & EPI_RESID) != 0) {
+      float r[4];
+      unpack(*reinterpret_cast<const u32x2*>(
+                 res + res_off + (uint32_t)((i * 32 + 8 * qd) * g.ldr + j * 32)), r);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) + r[c]);
+    }
+    out = pack(h);
+  };
+  static_for<TN / 2>([&](auto p) {
+    constexpr int j0 = 2 * p, j1 = 2 * p + 1;
+    float b0[4] = {0.0f, 0.0f, 0.0f, 0.0f}, b1[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+    if constexpr ((E & EPI_BIAS) != 0) {
+      unpack(*reinterpret_cast<const u32x2*>(g.bias + nw + j0 * 32 + col_l), b0);
+      unpack(*reinterpret_cast<const u32x2*>(g.bias + nw + j1 * 32 + col_l), b1);
+    }
     static_for<TM>([&](auto i) {
-      const f32x16 a = acc[i][j];
 #pragma unroll
       for (int qd = 0; qd < 4; ++qd) {
-        float v[4] = {a[4 * qd], a[4 * qd + 1], a[4 * qd + 2], a[4 * qd + 3]};
-        quad_transpose(v, q4);
-        const uint32_t rofs = (uint32_t)((i * 32 + 8 * qd) * ldc + j * 32);
-        const uint32_t off = lane_off + rofs;
-        uint16_t h[4];
-#pragma unroll
-        for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(v[c] + bias[c]);
+        u32x2 x, y, px{0u, 0u}, py{0u, 0u};
+        run(acc[i][j0], i, j0, qd, b0, x, px);
+        run(acc[i][j1], i, j1, qd, b1, y, py);
+        pair_swap(x, y);
+        const uint32_t o = out_off + (uint32_t)((i * 32 + 8 * qd) * ldc + j0 * 32);
+        const uint32_t o4 = o + (uint32_t)(4 * ldc);
         if constexpr ((E & EPI_GELU) != 0) {
-          *reinterpret_cast<u32x2*>(pre + off) = pack(h);
-#pragma unroll
-          for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(gelu_tanh(h2f<DT>(h[c])));
+          pair_swap(px, py);
+          *reinterpret_cast<u32x2*>(pre + o) = px;
+          *reinterpret_cast<u32x2*>(pre + o4) = py;
         }
-        if constexpr ((E & EPI_DACT) != 0) {
-          float da[4];
-          unpack(*reinterpret_cast<const u32x2*>(dact + off), da);
-#pragma unroll
-          for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) * gelu_tanh_grad(da[c]));
-        }
-        if constexpr ((E & EPI_RESID) != 0) {
-          float r[4];
-          unpack(*reinterpret_cast<const u32x2*>(
-                     res + res_off + (uint32_t)((i * 32 + 8 * qd) * g.ldr + j * 32)), r);
-#pragma unroll
-          for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) + r[c]);
-        }
-        *reinterpret_cast<u32x2*>(C + off) = pack(h);
+        *reinterpret_cast<u32x2*>(C + o) = x;
+        *reinterpret_cast<u32x2*>(C + o4) = y;
       }
     });
   });

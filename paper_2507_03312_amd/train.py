@@ -222,6 +222,12 @@ class TrainStep:
         flat[element % flat.numel()] = value
 
 
+def _linear_gelu_bytes(M: int, N: int, K: int) -> int:
+    """Algorithmic HBM bytes of one linear_fwd + GELU launch in half precision:
+    read X [M,K], W [N,K], b [N]; write the output and the pre-activation [M,N]."""
+    return 2 * (M * K + N * K + N + 2 * M * N)
+
+
 class MLPStep(TrainStep):
     """2-layer MLP with GELU and an MSE loss."""
 
@@ -252,8 +258,9 @@ class MLPStep(TrainStep):
 
     def dominant_site(self):
         c = self.cfg
-        return {"name": "fc1.fwd", "flops": 2.0 * c.batch * c.d_hidden * c.d_in,
-                "desc": f"linear_fwd+GELU M={c.batch} N={c.d_hidden} K={c.d_in} ({c.half})"}
+        M, N, K = c.batch, c.d_hidden, c.d_in
+        return {"name": "fc1.fwd", "flops": 2.0 * M * N * K, "bytes": _linear_gelu_bytes(M, N, K),
+                "desc": f"linear_fwd+GELU M={M} N={N} K={K} ({c.half})"}
 
     def describe(self):
         c = self.cfg
@@ -341,6 +348,7 @@ class ViTStep(TrainStep):
         c = self.cfg
         M = c.batch * c.tokens
         return {"name": "blk0.up.fwd", "flops": 2.0 * M * c.d_mlp * c.d_model,
+                "bytes": _linear_gelu_bytes(M, c.d_mlp, c.d_model),
                 "desc": f"linear_fwd+GELU (MLP up-projection) M={M} N={c.d_mlp} K={c.d_model} ({c.half})"}
 
     def describe(self):
