@@ -183,6 +183,29 @@ int mpx_gemm_batched(int32_t trans_a, int32_t trans_b, int64_t M, int64_t N, int
  * Errors: MPX_ERR_INVALID for a value outside [0, 7]. */
 int mpx_gemm_set_config(int32_t config);
 
+/* Fused multi-head self-attention core (MPX §2.1 half products with float32
+ * accumulation; §3.2 softmax and its backward in full precision), one pass
+ * each way:
+ *   S = half(Q K^T);  P = half(softmax(S / sqrt(hd))) (float32 math);
+ *   O = half(P V).
+ * qkv [B*T, 3*H*hd] half, row-major: Q | K | V, head h at columns h*hd of
+ * each third.  O [B*T, H*hd].  P [B*H, T, ldP] with ldP = T rounded up to a
+ * multiple of 8: the probabilities, kept for the backward pass (columns
+ * T..ldP-1 are written as 0).  Buffers are caller-owned device memory.
+ * Implemented for hd == 64 and 1 <= T <= 128 (else MPX_ERR_UNSUPPORTED);
+ * qkv and O 16-byte aligned, P 8-byte aligned (else MPX_ERR_INVALID). */
+int mpx_attention_fwd(const void* qkv, void* O, void* P, int64_t B, int64_t T, int64_t H,
+                      int64_t hd, mpx_dtype dt, void* stream);
+
+/* Backward of mpx_attention_fwd, given the P it wrote and dO [B*T, H*hd]:
+ *   dP = half(dO V^T);  dV = half(P^T dO);
+ *   dS = half(scale P (dP - rowsum(dP P))) (float32 math, scale = 1/sqrt(hd));
+ *   dQ = half(dS K);  dK = half(dS^T Q),
+ * written into dqkv [B*T, 3*H*hd] in the layout of qkv.  Same limits and
+ * alignment as the forward (dO and dqkv 16-byte aligned). */
+int mpx_attention_bwd(const void* qkv, const void* P, const void* dO, void* dqkv, int64_t B,
+                      int64_t T, int64_t H, int64_t hd, mpx_dtype dt, void* stream);
+
 /* ---- Support ops of the half forward/backward (full-precision islands,
  * MPX §3.2 force_full_precision: sums, means, softmax) ---- */
 

@@ -63,6 +63,8 @@ _SIGS = {
     "mpx_gemm_batched": (C.c_int, [I32, I32, I64, I64, I64, I64, I64, P, I64, I64, I64, P, I64,
                                    I64, I64, P, I64, I64, I64, I32, P]),
     "mpx_gemm_set_config": (C.c_int, [I32]),
+    "mpx_attention_fwd": (C.c_int, [P, P, P, I64, I64, I64, I64, I32, P]),
+    "mpx_attention_bwd": (C.c_int, [P, P, P, P, I64, I64, I64, I64, I32, P]),
     "mpx_layernorm_fwd": (C.c_int, [P, I64, P, P, P, P, I64, I64, I32, P]),
     "mpx_layernorm_bwd": (C.c_int, [P, I64, P, P, P, P, I64, P, P, I64, I64, I32, P, SZ, P]),
     "mpx_layernorm_bwd_workspace": (SZ, [I64, I64]),
@@ -160,6 +162,8 @@ mpx_linear_fwd = _call("mpx_linear_fwd")
 mpx_linear_bwd = _call("mpx_linear_bwd")
 mpx_gemm_batched = _call("mpx_gemm_batched")
 mpx_gemm_set_config = _call("mpx_gemm_set_config")
+mpx_attention_fwd = _call("mpx_attention_fwd")
+mpx_attention_bwd = _call("mpx_attention_bwd")
 mpx_layernorm_fwd = _call("mpx_layernorm_fwd")
 mpx_layernorm_bwd = _call("mpx_layernorm_bwd")
 mpx_softmax_fwd = _call("mpx_softmax_fwd")

@@ -1,0 +1,408 @@
+// Fused multi-head self-attention core for short sequences (T <= 128, head
+// dimension 64), forward and backward, with the half-precision policy of
+// MPX (§2.1: products in half with float32 accumulation; §3.2: the softmax
+// and its backward run in full precision as a force_full_precision island):
+//
+//   forward   S = half(Q K^T),  P = half(softmax(scale S)) in float32,
+//             O = half(P V)                                (scale = 1/sqrt(hd))
+//   backward  dP = half(dO V^T),  dV = half(P^T dO),
+//             dS = half(scale P (dP - sum_k dP P)) in float32,
+//             dQ = half(dS K),  dK = half(dS^T Q)
+//
+// One workgroup per (batch, head) with one wave per 32-row block of the
+// sequence.  Each wave computes the transposed score block S^T = K Q^T for
+// its 32 queries, so that a lane holds one query (column) and half of every
+// key block (rows): the softmax reductions over keys are lane-local plus one
+// exchange with the lane 32 apart.  The probabilities then feed the P V
+// product straight from registers: a v_permlane32_swap turns the
+// accumulator layout into the MFMA B-operand layout (8 consecutive keys per
+// lane).  V, and in the backward K, Q, dO, P and dS, are staged in LDS and
+// read as transposed MFMA operands with ds_read_b64_tr_b16.
+//
+// Layouts: qkv [B*T, 3*H*64] (Q | K | V, head h at columns h*64 of each
+// third), O and dO [B*T, H*64], dqkv like qkv, P [B*H, T, ldP] with
+// ldP = T rounded up to 8 (columns T..ldP-1 hold 0).
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+
+#include "common.h"
+#include "mfma.h"
+
+namespace mpx {
+namespace {
+
+constexpr int HD = 64;               // head dimension
+constexpr int PD = HD + 16;          // LDS row pitch (halves) of [row][d] arrays:
+                                     // 160 B, so 4 consecutive rows of a
+                                     // transposed read fall in distinct banks
+
+// MFMA operand fragment (32 rows of m or n, 16 k) from an LDS array stored
+// [k][mn] with mn contiguous and a pitch of `pitch` halves: two
+// ds_read_b64_tr_b16, each giving 4 consecutive k of one mn per lane.
+__device__ __forceinline__ uint4 frag_tr(uint32_t base, int pitch, int k0, int mn0, int lane) {
+  const int g = lane >> 4, e = (lane >> 2) & 3, t = lane & 3;
+  const int kr = k0 + 8 * (g >> 1) + e;
+  const int mn = mn0 + 16 * (g & 1) + 4 * t;
+  const uint2 lo = lds_tr_b64(base + (uint32_t)((kr * pitch + mn) * 2));
+  const uint2 hi = lds_tr_b64(base + (uint32_t)(((kr + 4) * pitch + mn) * 2));
+  return make_uint4(lo.x, lo.y, hi.x, hi.y);
+}
+
+// Rows [0, rows) of a [T, 64] head slice (row stride ld) into LDS [rows][PD];
+// rows >= T are zero.
+__device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* src, int64_t ld, int T,
+                                           int rows, int tid, int nthreads) {
+  for (int c = tid; c < rows * 8; c += nthreads) {
+    const int r = c >> 3, col = (c & 7) * 8;
+    u32x4 v = {0u, 0u, 0u, 0u};
+    if (r < T) v = *reinterpret_cast<const u32x4*>(src + r * ld + col);
+    *reinterpret_cast<u32x4*>(lds + r * PD + col) = v;
+  }
+}
+
+// Packs 4 halves.
+__device__ __forceinline__ u32x2 pack4(uint16_t a, uint16_t b, uint16_t c, uint16_t d) {
+  return u32x2{a | ((uint32_t)b << 16), c | ((uint32_t)d << 16)};
+}
+
+// B operand (n = query, 16 keys starting at 16 ks) from the packed
+// probabilities of the lane's query: R[j][gq] holds keys 32 j + 8 gq + 4 hi +
+// (0..3).  Half 0 needs keys 8 g' + 0..7 with g' = 2s, half 1 with g' = 2s+1;
+// swapping the upper half of group 2s with the lower half of group 2s+1
+// leaves the first 4 keys in x and the next 4 in y on every lane.
+template <int NB>
+__device__ __forceinline__ uint4 keys_operand(const u32x2 (&R)[NB][4], int ks) {
+  u32x2 x = R[ks / 2][2 * (ks % 2)], y = R[ks / 2][2 * (ks % 2) + 1];
+  half_swap(x, y);
+  return make_uint4(x.x, x.y, y.x, y.y);
+}
+
+// ----------------------------------------------------------------- forward --
+
+template <int DT, int NB>
+__global__ __launch_bounds__(NB * 64) void attn_fwd_kernel(const uint16_t* __restrict__ qkv,
+                                                           uint16_t* __restrict__ O,
+                                                           uint16_t* __restrict__ P, int T, int H,
+                                                           int ldP, float scale) {
+  constexpr int TK = 32 * NB;
+  __shared__ __attribute__((aligned(16))) uint16_t sV[TK * PD];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hi = lane >> 5;
+  const int bh = blockIdx.x, b = bh / H, h = bh % H;
+  const int dm = H * HD;
+  const int64_t ld = 3 * (int64_t)dm;
+  const uint16_t* Q = qkv + (int64_t)b * T * ld + h * HD;
+  const uint16_t* K = Q + dm;
+  const uint16_t* V = Q + 2 * dm;
+
+  stage_rows(sV, V, ld, T, TK, tid, NB * 64);
+
+  // S^T blocks: rows = keys of block j, columns = the wave's 32 queries
+  const int q = 32 * w + (lane & 31);
+  const int qc = min(q, T - 1);
+  uint4 qf[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) qf[kk] = ld_u4(Q + qc * ld + 16 * kk + 8 * hi);
+  f32x16 s[NB];
+  static_for<NB>([&](auto j) {
+    const int key = min(32 * j + (lane & 31), T - 1);
+    f32x16 acc;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) acc = mfma32<DT>(ld_u4(K + key * ld + 16 * kk + 8 * hi), qf[kk], acc);
+    s[j] = acc;
+  });
+
+  // softmax over the keys of query q (float32; S rounded to half first)
+  float mx = -INFINITY;
+  static_for<NB>([&](auto j) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int key = 32 * j + 8 * (e >> 2) + 4 * hi + (e & 3);
+      const float z = h2f<DT>(f2h<DT>(s[j][e])) * scale;
+      s[j][e] = key < T ? z : -INFINITY;
+      mx = fmaxf(mx, s[j][e]);
+    }
+  });
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  float sum = 0.0f;
+  static_for<NB>([&](auto j) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int key = 32 * j + 8 * (e >> 2) + 4 * hi + (e & 3);
+      const float ex = key < T ? __expf(s[j][e] - mx) : 0.0f;
+      s[j][e] = ex;
+      sum += ex;
+    }
+  });
+  sum += __shfl_xor(sum, 32);
+  const float inv = 1.0f / sum;
+  u32x2 R[NB][4];
+  static_for<NB>([&](auto j) {
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      uint16_t p[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) p[c] = f2h<DT>(s[j][4 * gq + c] * inv);
+      R[j][gq] = pack4(p[0], p[1], p[2], p[3]);
+      const int key0 = 32 * j + 8 * gq + 4 * hi;
+      if (q < T && key0 < ldP) st_u2(P + ((int64_t)bh * T + q) * ldP + key0, R[j][gq]);
+    }
+  });
+
+  // O^T = V^T P^T: rows = d (two blocks of 32), columns = the wave's queries
+  __syncthreads();
+  const uint32_t vbase = lds_u32(sV);
+  f32x16 o[2];
+#pragma unroll
+  for (int db = 0; db < 2; ++db)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[db][e] = 0.0f;
+  static_for<2 * NB>([&](auto ks) {
+    const uint4 bf = keys_operand<NB>(R, ks);
+#pragma unroll
+    for (int db = 0; db < 2; ++db) o[db] = mfma32<DT>(frag_tr(vbase, PD, 16 * ks, 32 * db, lane), bf, o[db]);
+  });
+  if (q < T) {
+    uint16_t* out = O + ((int64_t)b * T + q) * dm + h * HD;
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq)
+        st_u2(out + 32 * db + 8 * gq + 4 * hi,
+              pack4(f2h<DT>(o[db][4 * gq]), f2h<DT>(o[db][4 * gq + 1]), f2h<DT>(o[db][4 * gq + 2]),
+                    f2h<DT>(o[db][4 * gq + 3])));
+  }
+}
+
+// ---------------------------------------------------------------- backward --
+
+template <int DT, int NB>
+__global__ __launch_bounds__(NB * 64) void attn_bwd_kernel(const uint16_t* __restrict__ qkv,
+                                                           const uint16_t* __restrict__ P,
+                                                           const uint16_t* __restrict__ dO,
+                                                           uint16_t* __restrict__ dqkv, int T, int H,
+                                                           int ldP, float scale) {
+  constexpr int TK = 32 * NB;
+  constexpr int PK = TK + 16;  // pitch (halves) of the [query][key] arrays
+  __shared__ __attribute__((aligned(16))) uint16_t sK[TK * PD];
+  __shared__ __attribute__((aligned(16))) uint16_t sQ[TK * PD];
+  __shared__ __attribute__((aligned(16))) uint16_t sdO[TK * PD];
+  __shared__ __attribute__((aligned(16))) uint16_t sP[TK * PK];
+  __shared__ __attribute__((aligned(16))) uint16_t sdS[TK * PK];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hi = lane >> 5;
+  const int bh = blockIdx.x, b = bh / H, h = bh % H;
+  const int dm = H * HD;
+  const int64_t ld = 3 * (int64_t)dm;
+  const uint16_t* Q = qkv + (int64_t)b * T * ld + h * HD;
+  const uint16_t* K = Q + dm;
+  const uint16_t* V = Q + 2 * dm;
+  const uint16_t* G = dO + (int64_t)b * T * dm + h * HD;
+  uint16_t* dQ = dqkv + (int64_t)b * T * ld + h * HD;
+  uint16_t* dK = dQ + dm;
+  uint16_t* dV = dQ + 2 * dm;
+
+  stage_rows(sK, K, ld, T, TK, tid, NB * 64);
+  stage_rows(sQ, Q, ld, T, TK, tid, NB * 64);
+  stage_rows(sdO, G, dm, T, TK, tid, NB * 64);
+
+  // ---- per query block (wave w): dP^T, dS, dQ
+  const int q = 32 * w + (lane & 31);
+  const int qc = min(q, T - 1);
+  uint4 gf[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) gf[kk] = ld_u4(G + qc * dm + 16 * kk + 8 * hi);
+  f32x16 dp[NB];
+  static_for<NB>([&](auto j) {
+    const int key = min(32 * j + (lane & 31), T - 1);
+    f32x16 acc;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) acc = mfma32<DT>(ld_u4(V + key * ld + 16 * kk + 8 * hi), gf[kk], acc);
+    dp[j] = acc;
+  });
+  // P of query q (keys >= T hold 0; queries >= T read as 0)
+  u32x2 Pr[NB][4];
+  float rs = 0.0f;
+  static_for<NB>([&](auto j) {
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const int key0 = 32 * j + 8 * gq + 4 * hi;
+      Pr[j][gq] = (q < T && key0 < T) ? ld_u2(P + ((int64_t)bh * T + q) * ldP + key0) : u32x2{0u, 0u};
+      const uint16_t ph[4] = {(uint16_t)(Pr[j][gq].x & 0xFFFFu), (uint16_t)(Pr[j][gq].x >> 16),
+                              (uint16_t)(Pr[j][gq].y & 0xFFFFu), (uint16_t)(Pr[j][gq].y >> 16)};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const float d = h2f<DT>(f2h<DT>(dp[j][4 * gq + c]));
+        dp[j][4 * gq + c] = d;
+        if (key0 + c < T) rs += d * h2f<DT>(ph[c]);
+      }
+    }
+  });
+  rs += __shfl_xor(rs, 32);
+  u32x2 Sr[NB][4];
+  static_for<NB>([&](auto j) {
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const int key0 = 32 * j + 8 * gq + 4 * hi;
+      const uint16_t ph[4] = {(uint16_t)(Pr[j][gq].x & 0xFFFFu), (uint16_t)(Pr[j][gq].x >> 16),
+                              (uint16_t)(Pr[j][gq].y & 0xFFFFu), (uint16_t)(Pr[j][gq].y >> 16)};
+      uint16_t ds[4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const bool ok = q < T && key0 + c < T;
+        ds[c] = ok ? f2h<DT>((scale * h2f<DT>(ph[c])) * (dp[j][4 * gq + c] - rs)) : (uint16_t)0;
+      }
+      Sr[j][gq] = pack4(ds[0], ds[1], ds[2], ds[3]);
+      // the [query][key] copies for the dK / dV products (rows >= T are 0)
+      *reinterpret_cast<u32x2*>(sP + q * PK + key0) = Pr[j][gq];
+      *reinterpret_cast<u32x2*>(sdS + q * PK + key0) = Sr[j][gq];
+    }
+  });
+  __syncthreads();  // sK / sQ / sdO staged, sP / sdS complete
+
+  // dQ^T = K^T dS^T: rows = d, columns = the wave's queries
+  const uint32_t kbase = lds_u32(sK), qbase = lds_u32(sQ), gbase = lds_u32(sdO);
+  const uint32_t pbase = lds_u32(sP), sbase = lds_u32(sdS);
+  {
+    f32x16 o[2];
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) o[db][e] = 0.0f;
+    static_for<2 * NB>([&](auto ks) {
+      const uint4 bf = keys_operand<NB>(Sr, ks);
+#pragma unroll
+      for (int db = 0; db < 2; ++db) o[db] = mfma32<DT>(frag_tr(kbase, PD, 16 * ks, 32 * db, lane), bf, o[db]);
+    });
+    if (q < T) {
+#pragma unroll
+      for (int db = 0; db < 2; ++db)
+#pragma unroll
+        for (int gq = 0; gq < 4; ++gq)
+          st_u2(dQ + q * ld + 32 * db + 8 * gq + 4 * hi,
+                pack4(f2h<DT>(o[db][4 * gq]), f2h<DT>(o[db][4 * gq + 1]), f2h<DT>(o[db][4 * gq + 2]),
+                      f2h<DT>(o[db][4 * gq + 3])));
+    }
+  }
+
+  // ---- per key block (wave w): dK = dS^T Q and dV = P^T dO, rows = keys of
+  // block w, columns = d, reduced over all queries
+  f32x16 dk[2], dv[2];
+#pragma unroll
+  for (int db = 0; db < 2; ++db)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) dk[db][e] = dv[db][e] = 0.0f;
+  static_for<2 * NB>([&](auto ks) {
+    const uint4 sa = frag_tr(sbase, PK, 16 * ks, 32 * w, lane);
+    const uint4 pa = frag_tr(pbase, PK, 16 * ks, 32 * w, lane);
+#pragma unroll
+    for (int db = 0; db < 2; ++db) {
+      dk[db] = mfma32<DT>(sa, frag_tr(qbase, PD, 16 * ks, 32 * db, lane), dk[db]);
+      dv[db] = mfma32<DT>(pa, frag_tr(gbase, PD, 16 * ks, 32 * db, lane), dv[db]);
+    }
+  });
+  // accumulator runs (4 consecutive keys of one d) -> 4 consecutive d of one key
+  const int q4 = lane & 3;
+  const int col = 4 * ((lane & 31) >> 2);
+#pragma unroll
+  for (int db = 0; db < 2; ++db)
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      float a[4] = {dk[db][4 * gq], dk[db][4 * gq + 1], dk[db][4 * gq + 2], dk[db][4 * gq + 3]};
+      float c[4] = {dv[db][4 * gq], dv[db][4 * gq + 1], dv[db][4 * gq + 2], dv[db][4 * gq + 3]};
+      quad_transpose(a, q4);
+      quad_transpose(c, q4);
+      const int key = 32 * w + 8 * gq + 4 * hi + q4;
+      if (key < T) {
+        st_u2(dK + key * ld + 32 * db + col, pack4(f2h<DT>(a[0]), f2h<DT>(a[1]), f2h<DT>(a[2]), f2h<DT>(a[3])));
+        st_u2(dV + key * ld + 32 * db + col, pack4(f2h<DT>(c[0]), f2h<DT>(c[1]), f2h<DT>(c[2]), f2h<DT>(c[3])));
+      }
+    }
+}
+
+template <int DT>
+hipError_t launch_fwd(const uint16_t* qkv, uint16_t* O, uint16_t* P, int B, int T, int H, int ldP,
+                      float scale, hipStream_t s) {
+  const dim3 grid((unsigned)(B * H));
+  switch ((T + 31) / 32) {
+    case 1: attn_fwd_kernel<DT, 1><<<grid, 64, 0, s>>>(qkv, O, P, T, H, ldP, scale); break;
+    case 2: attn_fwd_kernel<DT, 2><<<grid, 128, 0, s>>>(qkv, O, P, T, H, ldP, scale); break;
+    case 3: attn_fwd_kernel<DT, 3><<<grid, 192, 0, s>>>(qkv, O, P, T, H, ldP, scale); break;
+    default: attn_fwd_kernel<DT, 4><<<grid, 256, 0, s>>>(qkv, O, P, T, H, ldP, scale); break;
+  }
+  return hipGetLastError();
+}
+
+template <int DT>
+hipError_t launch_bwd(const uint16_t* qkv, const uint16_t* P, const uint16_t* dO, uint16_t* dqkv,
+                      int B, int T, int H, int ldP, float scale, hipStream_t s) {
+  const dim3 grid((unsigned)(B * H));
+  switch ((T + 31) / 32) {
+    case 1: attn_bwd_kernel<DT, 1><<<grid, 64, 0, s>>>(qkv, P, dO, dqkv, T, H, ldP, scale); break;
+    case 2: attn_bwd_kernel<DT, 2><<<grid, 128, 0, s>>>(qkv, P, dO, dqkv, T, H, ldP, scale); break;
+    case 3: attn_bwd_kernel<DT, 3><<<grid, 192, 0, s>>>(qkv, P, dO, dqkv, T, H, ldP, scale); break;
+    default: attn_bwd_kernel<DT, 4><<<grid, 256, 0, s>>>(qkv, P, dO, dqkv, T, H, ldP, scale); break;
+  }
+  return hipGetLastError();
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+}  // namespace mpx
+
+using namespace mpx;
+
+extern "C" int mpx_attention_fwd(const void* qkv, void* O, void* P, int64_t B, int64_t T, int64_t H,
+                                 int64_t hd, mpx_dtype dt, void* stream) {
+  clear_error();
+  MPX_REQUIRE(qkv && O && P, "NULL operand");
+  MPX_REQUIRE(B >= 1 && T >= 1 && H >= 1, "B, T, H must be >= 1");
+  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(B * H <= INT32_MAX && B * T * H * 3 * 64 < ((int64_t)1 << 31), "problem too large");
+  if (hd != 64 || T > 128) {
+    set_error("mpx_attention_fwd: implemented for head dimension 64 and T <= 128");
+    return MPX_ERR_UNSUPPORTED;
+  }
+  MPX_REQUIRE(aligned16(qkv) && aligned16(O) && (reinterpret_cast<uintptr_t>(P) & 7u) == 0,
+              "qkv and O must be 16-byte aligned, P 8-byte aligned");
+  const int ldP = (int)((T + 7) / 8 * 8);
+  const float scale = (float)(1.0 / std::sqrt((double)hd));
+  hipStream_t s = (hipStream_t)stream;
+  if (dt == MPX_F16)
+    MPX_HIP(launch_fwd<MPX_F16>((const uint16_t*)qkv, (uint16_t*)O, (uint16_t*)P, (int)B, (int)T, (int)H,
+                                ldP, scale, s));
+  else
+    MPX_HIP(launch_fwd<MPX_BF16>((const uint16_t*)qkv, (uint16_t*)O, (uint16_t*)P, (int)B, (int)T,
+                                 (int)H, ldP, scale, s));
+  return MPX_OK;
+}
+
+extern "C" int mpx_attention_bwd(const void* qkv, const void* P, const void* dO, void* dqkv, int64_t B,
+                                 int64_t T, int64_t H, int64_t hd, mpx_dtype dt, void* stream) {
+  clear_error();
+  MPX_REQUIRE(qkv && P && dO && dqkv, "NULL operand");
+  MPX_REQUIRE(B >= 1 && T >= 1 && H >= 1, "B, T, H must be >= 1");
+  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(B * H <= INT32_MAX && B * T * H * 3 * 64 < ((int64_t)1 << 31), "problem too large");
+  if (hd != 64 || T > 128) {
+    set_error("mpx_attention_bwd: implemented for head dimension 64 and T <= 128");
+    return MPX_ERR_UNSUPPORTED;
+  }
+  MPX_REQUIRE(aligned16(qkv) && aligned16(dO) && aligned16(dqkv) &&
+                  (reinterpret_cast<uintptr_t>(P) & 7u) == 0,
+              "qkv, dO and dqkv must be 16-byte aligned, P 8-byte aligned");
+  const int ldP = (int)((T + 7) / 8 * 8);
+  const float scale = (float)(1.0 / std::sqrt((double)hd));
+  hipStream_t s = (hipStream_t)stream;
+  if (dt == MPX_F16)
+    MPX_HIP(launch_bwd<MPX_F16>((const uint16_t*)qkv, (const uint16_t*)P, (const uint16_t*)dO,
+                                (uint16_t*)dqkv, (int)B, (int)T, (int)H, ldP, scale, s));
+  else
+    MPX_HIP(launch_bwd<MPX_BF16>((const uint16_t*)qkv, (const uint16_t*)P, (const uint16_t*)dO,
+                                 (uint16_t*)dqkv, (int)B, (int)T, (int)H, ldP, scale, s));
+  return MPX_OK;
+}

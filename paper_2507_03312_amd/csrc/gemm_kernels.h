@@ -30,16 +30,9 @@
 
 #include "colsum.h"
 #include "common.h"
+#include "mfma.h"
 
 namespace mpx {
-
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
-// Clang vector types for 8- and 16-byte global accesses (a store through the
-// HIP uint2 / float4 structs is split into 4-byte stores)
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
 
 struct GemmArgs {
   const uint16_t* A;
@@ -58,29 +51,6 @@ struct GemmArgs {
   int32_t act;
   int32_t full_epi;  // set by the dispatcher: whole tiles may use gemm_epilogue_full
 };
-
-// Compile-time loop: f(std::integral_constant<int, I>) for I in [0, N).  The
-// accumulator tiles are indexed only with such constants, so they stay in
-// registers (a runtime index would force them into scratch memory).
-template <typename F, int... I>
-__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, I...>) {
-  (f(std::integral_constant<int, I>{}), ...);
-}
-template <int N, typename F>
-__device__ __forceinline__ void static_for(F&& f) {
-  static_for_impl(f, std::make_integer_sequence<int, N>{});
-}
-
-template <int DT>
-__device__ __forceinline__ f32x16 mfma32(uint4 a, uint4 b, f32x16 c) {
-  if constexpr (DT == MPX_F16) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a),
-                                                  __builtin_bit_cast(f16x8, b), c, 0, 0, 0);
-  } else {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
-                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-  }
-}
 
 // Loader of one operand tile (ROWS output rows x BK reduction values) into
 // registers, then into LDS as [row][k].  KMAJ: element (r,k) at base[r*ld + k];
@@ -262,24 +232,6 @@ __device__ __forceinline__ void tile_origin(int64_t M, int64_t N, int64_t& m0, i
 // epilogue's, step for step, so both give identical bits.
 enum : int { EPI_BIAS = 1, EPI_GELU = 2, EPI_DACT = 4, EPI_RESID = 8, EPI_GENERIC = -1 };
 
-// 4x4 transpose across each group of 4 lanes (two butterfly exchanges
-// through DPP quad permutations: lane ^ 1 is quad_perm [1,0,3,2], lane ^ 2 is
-// [2,3,0,1]): lane q of the group then holds row q of the 4 x 4 block.
-__device__ __forceinline__ void quad_transpose(float (&v)[4], int q4) {
-  auto xchg = [&](float& lo, float& hi_v, int st) {
-    const bool hi = (q4 & st) != 0;
-    const int send = __builtin_bit_cast(int, hi ? lo : hi_v);
-    const int got = st == 1 ? __builtin_amdgcn_mov_dpp(send, 0xB1, 0xF, 0xF, false)
-                            : __builtin_amdgcn_mov_dpp(send, 0x4E, 0xF, 0xF, false);
-    if (hi) lo = __builtin_bit_cast(float, got);
-    else hi_v = __builtin_bit_cast(float, got);
-  };
-  xchg(v[0], v[1], 1);
-  xchg(v[2], v[3], 1);
-  xchg(v[0], v[2], 2);
-  xchg(v[1], v[3], 2);
-}
-
 template <int DT, int TM, int TN, int E>
 __device__ __forceinline__ void gemm_epilogue_full(const GemmArgs& g, const f32x16 (&acc)[TM][TN],
                                                    int64_t mw, int64_t nw, int lane, int64_t offC) {
@@ -309,13 +261,6 @@ __device__ __forceinline__ void gemm_epilogue_full(const GemmArgs& g, const f32x
   };
   auto pack = [](const uint16_t (&h)[4]) {
     return u32x2{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16)};
-  };
-  // exchange the upper lane half of x with the lower lane half of y
-  auto pair_swap = [](u32x2& x, u32x2& y) {
-    const auto r0 = __builtin_amdgcn_permlane32_swap(x.x, y.x, false, false);
-    const auto r1 = __builtin_amdgcn_permlane32_swap(x.y, y.y, false, false);
-    x = u32x2{r0[0], r1[0]};
-    y = u32x2{r0[1], r1[1]};
   };
   // the epilogue of one 4-value run of block (i, j): returns the packed
   // output and (with GELU) the packed pre-activation
@@ -360,11 +305,11 @@ __device__ __forceinline__ void gemm_epilogue_full(const GemmArgs& g, const f32x
         u32x2 x, y, px{0u, 0u}, py{0u, 0u};
         run(acc[i][j0], i, j0, qd, b0, x, px);
         run(acc[i][j1], i, j1, qd, b1, y, py);
-        pair_swap(x, y);
+        half_swap(x, y);
         const uint32_t o = out_off + (uint32_t)((i * 32 + 8 * qd) * ldc + j0 * 32);
         const uint32_t o4 = o + (uint32_t)(4 * ldc);
         if constexpr ((E & EPI_GELU) != 0) {
-          pair_swap(px, py);
+          half_swap(px, py);
           *reinterpret_cast<u32x2*>(pre + o) = px;
           *reinterpret_cast<u32x2*>(pre + o4) = py;
         }
@@ -633,25 +578,6 @@ __device__ __forceinline__ void dma16(const void* base, uint32_t off, uint32_t l
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
-}
-
-__device__ __forceinline__ uint32_t lds_u32(const void* p) {
-  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
-}
-
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ uint2 lds_tr_b64(uint32_t addr) {
-  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) s16x4*)(uintptr_t)addr);
-  return __builtin_bit_cast(uint2, v);
-}
-
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-
-__device__ __forceinline__ uint4 lds_b128(uint32_t addr) {
-  const u32x4 v = *(const __attribute__((address_space(3))) u32x4*)(uintptr_t)addr;
-  return __builtin_bit_cast(uint4, v);
 }
 
 // One operand of the direct-to-LDS kernel: ROWS output rows (of M or N) by

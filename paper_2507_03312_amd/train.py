@@ -315,9 +315,10 @@ class ViTStep(TrainStep):
             self.blocks.append({
                 "a": z(M, d), "qkv": z(M, 3 * d), "P": z(B * H * T, self.ldT), "O": z(M, d),
                 "x1": z(M, d), "c": z(M, d), "u_pre": z(M, F), "u": z(M, F), "x2": z(M, d)})
-        self.S = z(B * H * T, self.ldT)
-        self.dP = z(B * H * T, self.ldT)
-        self.dS = z(B * H * T, self.ldT)
+        if not self._fused_attention():   # score buffers of the unfused path
+            self.S = z(B * H * T, self.ldT)
+            self.dP = z(B * H * T, self.ldT)
+            self.dS = z(B * H * T, self.ldT)
         self.zf = z(B, d)
         self.logits = z(B, Cn)
         self.dlogits = z(B, Cn)
@@ -367,11 +368,20 @@ class ViTStep(TrainStep):
             self.tok32.copy_(torch.from_numpy(batch["x"].reshape(c.batch * c.tokens, c.d_model)))
         self.labels.copy_(torch.from_numpy(batch["labels"].astype(np.int32)))
 
-    # attention core of one block: S = Q K^T, P = softmax, O = P V
+    # attention core of one block: S = Q K^T, P = softmax, O = P V.  Short
+    # sequences (T <= 128, head dim 64) run the fused kernels; longer ones
+    # the batched GEMMs around the row softmax.
+    def _fused_attention(self):
+        c = self.cfg
+        return c.tokens <= 128 and c.head_dim == 64
+
     def _attn_fwd(self, blk, s):
         c, dt = self.cfg, self.dt
         B, T, d, H, hd, ldT = c.batch, c.tokens, c.d_model, c.heads, c.head_dim, self.ldT
         qkv, P, O = blk["qkv"], blk["P"], blk["O"]
+        if self._fused_attention():
+            mx.mpx_attention_fwd(_ptr(qkv), _ptr(O), _ptr(P), B, T, H, hd, dt, s)
+            return
         mx.mpx_gemm_batched(0, 1, T, T, hd, B, H,
                             _ptr(qkv), 3 * d, T * 3 * d, hd,
                             _off(qkv, d), 3 * d, T * 3 * d, hd,
@@ -386,6 +396,9 @@ class ViTStep(TrainStep):
         c, dt = self.cfg, self.dt
         B, T, d, H, hd, ldT = c.batch, c.tokens, c.d_model, c.heads, c.head_dim, self.ldT
         qkv, P, dO, dqkv = blk["qkv"], blk["P"], self.dO, self.dqkv
+        if self._fused_attention():
+            mx.mpx_attention_bwd(_ptr(qkv), _ptr(P), _ptr(dO), _ptr(dqkv), B, T, H, hd, dt, s)
+            return
         # dP = dO V^T
         mx.mpx_gemm_batched(0, 1, T, T, hd, B, H, _ptr(dO), d, T * d, hd,
                             _off(qkv, 2 * d), 3 * d, T * 3 * d, hd,

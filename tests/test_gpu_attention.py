@@ -1,0 +1,139 @@
+"""GPU parity of the fused attention core (mpx_attention_fwd / _bwd) against
+the oracle's attention_fwd / attention_bwd, through the C ABI.
+
+Bars (per element), from the rounding steps both sides share:
+  S    |dS| <= ulp(S) + 2 hd 2^-24 (|Q||K|^T)          (float32 vs float64 sums)
+  P    |dP| <= P scale (dS + sum_j P_j dS_j) 1.1 + 2^-18 P + ulp(P)
+       (first-order softmax sensitivity, float32 softmax error, final rounding)
+  O    ulp(O) + 2 T 2^-24 (|P||V|) + |P_gpu - P_oracle| |V|
+The backward takes the GPU's P on both sides; dP, dV, dQ, dK follow the GEMM
+bar, dS adds the propagated dP difference and its float32 evaluation error,
+and dQ / dK add the propagated dS bound.
+"""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import ops
+from oracle.numfmt import round_to
+from oracle.policy import Policy
+from tests.gpu_util import HAVE_GPU, assert_within, to_dev_half, to_host, ulp
+
+pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not HAVE_GPU, reason="no GPU")]
+
+if HAVE_GPU:
+    import torch
+    from paper_2507_03312_amd import binding as mx
+
+HD = 64
+SHAPES = [(2, 2, 1), (2, 3, 5), (1, 2, 32), (2, 2, 33), (2, 3, 65), (1, 2, 97), (1, 2, 128)]
+
+
+def _s():
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _empty(shape, fmt):
+    return torch.zeros(*shape, dtype=torch.float16 if fmt == "f16" else torch.bfloat16, device="cuda")
+
+
+def _inputs(B, T, H, fmt, seed):
+    rng = np.random.default_rng(seed)
+    d = H * HD
+    qkv = round_to(rng.normal(0.0, 1.0, size=(B * T, 3 * d)), fmt)
+    dout = round_to(rng.normal(0.0, 1.0, size=(B * T, d)), fmt)
+    return qkv, dout
+
+
+def _abs(a):
+    return np.abs(np.asarray(a, np.float64))
+
+
+def _run(B, T, H, fmt, seed=0):
+    pol = Policy(fmt)
+    dt = mx.DTYPES[fmt]
+    qkv, dout = _inputs(B, T, H, fmt, seed)
+    d = H * HD
+    ldP = -(-T // 8) * 8
+    tq, tdo = to_dev_half(qkv, fmt), to_dev_half(dout, fmt)
+    tO, tP, tdq = _empty((B * T, d), fmt), _empty((B * H * T, ldP), fmt), _empty((B * T, 3 * d), fmt)
+    tP.fill_(7.0)  # padding must be overwritten with 0
+    mx.mpx_attention_fwd(tq.data_ptr(), tO.data_ptr(), tP.data_ptr(), B, T, H, HD, dt, _s())
+    mx.mpx_attention_bwd(tq.data_ptr(), tP.data_ptr(), tdo.data_ptr(), tdq.data_ptr(), B, T, H, HD,
+                         dt, _s())
+    torch.cuda.synchronize()
+    return pol, qkv, dout, to_host(tO), to_host(tP).reshape(B, H, T, ldP), to_host(tdq)
+
+
+def _check_fwd(pol, fmt, qkv, B, T, H, gO, gPfull):
+    scale = 1.0 / math.sqrt(HD)
+    O_or, (q, k, v, P_or, _) = ops.attention_fwd(pol, qkv, B, T, H, HD)
+    assert np.all(gPfull[..., T:] == 0.0), "P padding columns must be 0"
+    gP = gPfull[..., :T]
+    kt = np.swapaxes(k, -1, -2)
+    S_or = pol.R(pol.mm(q, kt))
+    dS = ulp(S_or, fmt) + 2 * HD * 2.0 ** -24 * (_abs(q) @ _abs(kt))
+    Pv = _abs(P_or)
+    bP = Pv * scale * (dS + (Pv * dS).sum(-1, keepdims=True)) * 1.1 + Pv * 2.0 ** -18 + ulp(P_or, fmt)
+    assert_within(gP, P_or, bP, "P")
+    dPm = np.abs(gP.astype(np.float64) - np.asarray(P_or, np.float64))
+    O4 = np.asarray(O_or).reshape(B, T, H, HD).transpose(0, 2, 1, 3)
+    bO = ulp(O4, fmt) + 2 * T * 2.0 ** -24 * (_abs(gP) @ _abs(v)) + dPm @ _abs(v)
+    gO4 = gO.reshape(B, T, H, HD).transpose(0, 2, 1, 3)
+    assert_within(gO4, O4, bO, "O")
+    return q, k, v, gP
+
+
+def _check_bwd(pol, fmt, qkv, dout, B, T, H, gP, gdq):
+    scale = 1.0 / math.sqrt(HD)
+    q, k, v = ops.split_heads(qkv, B, T, H, HD)
+    P = np.asarray(gP, np.float64)
+    ref = ops.attention_bwd(pol, (q, k, v, P, scale), dout, B, T, H, HD)
+    rq, rk, rv = ops.split_heads(ref, B, T, H, HD)
+    gq, gk, gv = ops.split_heads(gdq, B, T, H, HD)
+    do = np.asarray(dout).reshape(B, T, H, HD).transpose(0, 2, 1, 3)
+    vt = np.swapaxes(v, -1, -2)
+    dP = pol.R(pol.mm(do, vt))
+    ddP = ulp(dP, fmt) + 2 * HD * 2.0 ** -24 * (_abs(do) @ _abs(vt))
+    dPv = np.asarray(dP, np.float64)
+    rs = (dPv * P).sum(-1, keepdims=True)
+    dS = pol.R(scale * P * (dPv - rs))
+    ddS = (scale * P * (ddP + (P * ddP).sum(-1, keepdims=True)) * 1.1
+           + scale * P * (np.abs(dPv) + np.abs(rs)) * 2.0 ** -21 + ulp(dS, fmt))
+    Pt = np.swapaxes(P, -1, -2)
+    bv = ulp(rv, fmt) + 2 * T * 2.0 ** -24 * (_abs(Pt) @ _abs(do))
+    assert_within(gv, rv, bv, "dV")
+    bq = ulp(rq, fmt) + 2 * T * 2.0 ** -24 * (_abs(dS) @ _abs(k)) + ddS @ _abs(k)
+    assert_within(gq, rq, bq, "dQ")
+    dSt, ddSt = np.swapaxes(dS, -1, -2), np.swapaxes(ddS, -1, -2)
+    bk = ulp(rk, fmt) + 2 * T * 2.0 ** -24 * (_abs(dSt) @ _abs(q)) + ddSt @ _abs(q)
+    assert_within(gk, rk, bk, "dK")
+
+
+@pytest.mark.parametrize("fmt", ["f16", "bf16"])
+@pytest.mark.parametrize("bth", SHAPES, ids=lambda s: "x".join(map(str, s)))
+def test_fused_attention(fmt, bth):
+    B, H, T = bth
+    pol, qkv, dout, gO, gPfull, gdq = _run(B, T, H, fmt, seed=T)
+    _, _, _, gP = _check_fwd(pol, fmt, qkv, B, T, H, gO, gPfull)
+    _check_bwd(pol, fmt, qkv, dout, B, T, H, gP, gdq)
+
+
+@pytest.mark.parametrize("fmt,bth", [("bf16", (128, 6, 65)), ("f16", (256, 6, 65))],
+                         ids=lambda s: str(s))
+def test_fused_attention_full_size(fmt, bth):
+    """The ViT-block and ViT-S attention shapes, every element checked."""
+    B, H, T = bth
+    pol, qkv, dout, gO, gPfull, gdq = _run(B, T, H, fmt, seed=3)
+    _, _, _, gP = _check_fwd(pol, fmt, qkv, B, T, H, gO, gPfull)
+    _check_bwd(pol, fmt, qkv, dout, B, T, H, gP, gdq)
+
+
+def test_fused_attention_limits():
+    t = _empty((64, 3 * 64), "bf16")
+    with pytest.raises(mx.MPXError, match="implemented for"):
+        mx.mpx_attention_fwd(t.data_ptr(), t.data_ptr(), t.data_ptr(), 1, 129, 1, 64, mx.MPX_BF16, _s())
+    with pytest.raises(mx.MPXError, match="implemented for"):
+        mx.mpx_attention_bwd(t.data_ptr(), t.data_ptr(), t.data_ptr(), t.data_ptr(), 1, 8, 1, 32,
+                             mx.MPX_BF16, _s())
