@@ -874,6 +874,7 @@ static hipError_t launch_dma(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipSt
 //   5  direct-to-LDS 128 x 256, 4 waves, 3 stages
 //   6  direct-to-LDS 128 x 128, 4 waves, 4 stages
 //   7  direct-to-LDS 128 x 128, 4 waves, 2 stages, two workgroups per CU
+//   8  skinny products: one wave (K > 32) or one lane (K <= 32) per output
 extern int g_forced_config;  // defined in gemm.hip
 
 // The direct-to-LDS kernel needs 16-byte aligned operands and whole k tiles
@@ -891,21 +892,79 @@ static bool dma_ok(const GemmArgs& g, bool vec, bool ak, bool bk) {
 // each other's epilogue and pipeline bubbles) is the fastest direct-to-LDS
 // variant for every shape, forward and backward; the register-staged
 // kernels serve operands the copies cannot take.
-static int choose_config(const GemmArgs& g, bool vec, bool ak, bool bk) {
+static bool small_ok(const GemmArgs& g, int64_t nbatch);
+
+static int choose_config(const GemmArgs& g, bool vec, bool ak, bool bk, int64_t nbatch) {
   const bool dma = dma_ok(g, vec, ak, bk);
+  const bool small = small_ok(g, nbatch);
   const int f = g_forced_config;
-  if (f >= 3 && dma) return f;
+  if (f == 8 && small) return 8;
+  if (f >= 3 && f <= 7 && dma) return f;
   if (f == 1 || (f == 2 && vec)) return f;
+  if (small && (g.M <= 32 || g.N <= 32 || g.K <= 32)) return 8;
   if (g.M <= 64 || g.N <= 64) return 1;
   if (dma) return 7;
   return vec ? 2 : 0;
+}
+
+// ----------------------------------------------------------- skinny GEMMs --
+//
+// Products with a dimension of 32 or less (a classifier head: 10 outputs, or
+// a reduction over 10 classes) waste most of a 32x32 MFMA tile and run a
+// long dependent k loop on very few workgroups.  Here every output element
+// gets its own wave when K > 32 (lane l sums k = l, l + 64, ... in float32,
+// then a fixed butterfly adds the 64 lane sums) or its own lane when K <= 32
+// (a plain k loop).  Both orders are fixed, so results are reproducible.
+// Epilogue: bias and residual, h = half(acc + bias[n]), then half(h + R[m,n]).
+template <int DT, bool WAVE>
+__global__ __launch_bounds__(256) void gemm_small_kernel(GemmArgs g, bool ak, bool bk) {
+  const int64_t MN = g.M * g.N;
+  const int64_t idx = WAVE ? ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6))
+                           : ((int64_t)blockIdx.x * 256 + threadIdx.x);
+  if (idx >= MN) return;
+  const int64_t m = idx / g.N, n = idx % g.N;
+  // opA(m,k) = A[m*lda + k] (k-major) or A[k*lda + m]; opB(n,k) likewise
+  const int64_t sam = ak ? g.lda : 1, sak = ak ? 1 : g.lda;
+  const int64_t sbn = bk ? g.ldb : 1, sbk = bk ? 1 : g.ldb;
+  const uint16_t* a = g.A + m * sam;
+  const uint16_t* b = g.B + n * sbn;
+  float acc = 0.0f;
+  if constexpr (WAVE) {
+    const int lane = threadIdx.x & 63;
+    for (int64_t k = lane; k < g.K; k += 64) acc += h2f<DT>(a[k * sak]) * h2f<DT>(b[k * sbk]);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
+    if (lane != 0) return;
+  } else {
+    for (int64_t k = 0; k < g.K; ++k) acc += h2f<DT>(a[k * sak]) * h2f<DT>(b[k * sbk]);
+  }
+  const float bias = g.bias ? h2f<DT>(g.bias[n]) : 0.0f;
+  uint16_t h = f2h<DT>(acc + bias);
+  if (g.resid) h = f2h<DT>(h2f<DT>(h) + h2f<DT>(g.resid[m * g.ldr + n]));
+  g.C[m * g.ldc + n] = h;
+}
+
+static bool small_ok(const GemmArgs& g, int64_t nbatch) {
+  return nbatch == 1 && g.splits == 1 && !g.pre && !g.dact && g.act == MPX_ACT_NONE &&
+         g.M * g.N <= ((int64_t)1 << 22);
+}
+
+template <int DT>
+static hipError_t launch_small(const GemmArgs& g, bool ak, bool bk, hipStream_t s) {
+  const int64_t MN = g.M * g.N;
+  if (g.K > 32)
+    gemm_small_kernel<DT, true><<<(unsigned)((MN + 3) / 4), 256, 0, s>>>(g, ak, bk);
+  else
+    gemm_small_kernel<DT, false><<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(g, ak, bk);
+  return hipGetLastError();
 }
 
 // ak: A is k-major; bk: B is k-major.
 template <int DT>
 static hipError_t run_gemm(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipStream_t s) {
   const bool vec = aligned_vec(g.A, g.lda, g.sA0, g.sA1) && aligned_vec(g.B, g.ldb, g.sB0, g.sB1);
-  switch (choose_config(g, vec, ak, bk)) {
+  switch (choose_config(g, vec, ak, bk, nbatch)) {
+    case 8: return launch_small<DT>(g, ak, bk, s);
     case 1: return launch_cfg<DT, 64, 64, 32, 32>(g, ak, bk, vec, nbatch, s);
     case 2: return launch_cfg<DT, 128, 128, 64, 32, 64, 4>(g, ak, bk, vec, nbatch, s);
     case 3: return launch_dma<DT, 256, 256, 128, 128, 2, 1>(g, ak, bk, nbatch, s);

@@ -288,3 +288,32 @@ def test_every_tile_config(gemm_config, fmt):
     bnd = ulp(kt_v, fmt) + 2 * T * 2.0 ** -24 * (np.abs(k_t.astype(np.float64)) @ np.abs(v.astype(np.float64)))
     got = to_host(out_o).reshape(B, T, H, hd)[:, :hd].transpose(0, 2, 1, 3)
     assert_within(got, kt_v, bnd, "K^T V")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_skinny_path_forced(fmt):
+    """The one-wave / one-lane-per-output path (configuration 8) on shapes that
+    are not skinny, both reduction branches and all operand layouts."""
+    pol = Policy(fmt)
+    dt = mx.DTYPES[fmt]
+    mx.mpx_gemm_set_config(8)
+    try:
+        for (M, N, K) in [(70, 100, 72), (300, 50, 16), (64, 96, 40)]:
+            x, w = _rand((M, K), fmt, 51), _rand((N, K), fmt, 52, 0.05)
+            b, dy = _rand((N,), fmt, 53, 0.5), _rand((M, N), fmt, 54)
+            tx, tw, tb, tdy = (to_dev_half(a, fmt) for a in (x, w, b, dy))
+            y, gdx, gdw = _empty((M, N), fmt), _empty((M, K), fmt), _empty((N, K), fmt)
+            mx.mpx_linear_fwd(tx.data_ptr(), tw.data_ptr(), tb.data_ptr(), None, y.data_ptr(), None,
+                              M, N, K, dt, mx.MPX_ACT_NONE, _s())
+            ref = ops.linear_fwd(pol, x, w, b)
+            assert_within(to_host(y), ref, gemm_bound(x, w.T, ref, fmt, K), f"Y {M}x{N}x{K}")
+            ws_n = mx.mpx_linear_bwd_workspace(M, N, K)
+            ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+            mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), None, mx.MPX_ACT_NONE,
+                              gdx.data_ptr(), gdw.data_ptr(), None, M, N, K, dt, ws.data_ptr(), ws_n,
+                              _s())
+            rdx, rdw, _ = ops.linear_bwd(pol, x, w, dy)
+            assert_within(to_host(gdx), rdx, gemm_bound(dy, w, rdx, fmt, N), f"dX {M}x{N}x{K}")
+            assert_within(to_host(gdw), rdw, gemm_bound(dy.T, x, rdw, fmt, M), f"dW {M}x{N}x{K}")
+    finally:
+        mx.mpx_gemm_set_config(0)
