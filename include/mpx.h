@@ -193,7 +193,7 @@ int mpx_gemm_set_config(int32_t config);
  * each third.  O [B*T, H*hd].  P [B*H, T, ldP] with ldP = T rounded up to a
  * multiple of 8: the probabilities, kept for the backward pass (columns
  * T..ldP-1 are written as 0).  Buffers are caller-owned device memory.
- * Implemented for hd == 64 and 1 <= T <= 128 (else MPX_ERR_UNSUPPORTED);
+ * Implemented for hd == 64 and 1 <= T <= 256 (else MPX_ERR_UNSUPPORTED);
  * qkv and O 16-byte aligned, P 8-byte aligned (else MPX_ERR_INVALID). */
 int mpx_attention_fwd(const void* qkv, void* O, void* P, int64_t B, int64_t T, int64_t H,
                       int64_t hd, mpx_dtype dt, void* stream);
@@ -203,9 +203,14 @@ int mpx_attention_fwd(const void* qkv, void* O, void* P, int64_t B, int64_t T, i
  *   dS = half(scale P (dP - rowsum(dP P))) (float32 math, scale = 1/sqrt(hd));
  *   dQ = half(dS K);  dK = half(dS^T Q),
  * written into dqkv [B*T, 3*H*hd] in the layout of qkv.  Same limits and
- * alignment as the forward (dO and dqkv 16-byte aligned). */
+ * alignment as the forward (dO and dqkv 16-byte aligned).  For T > 128 dS
+ * passes through a caller-owned, 16-byte aligned workspace of
+ * mpx_attention_bwd_workspace(B, T, H, hd) bytes (0 for T <= 128, where
+ * workspace may be NULL); a smaller one returns MPX_ERR_WORKSPACE. */
 int mpx_attention_bwd(const void* qkv, const void* P, const void* dO, void* dqkv, int64_t B,
-                      int64_t T, int64_t H, int64_t hd, mpx_dtype dt, void* stream);
+                      int64_t T, int64_t H, int64_t hd, mpx_dtype dt, void* workspace,
+                      size_t ws_bytes, void* stream);
+size_t mpx_attention_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t hd);
 
 /* ---- Support ops of the half forward/backward (full-precision islands,
  * MPX §3.2 force_full_precision: sums, means, softmax) ---- */

@@ -64,7 +64,8 @@ _SIGS = {
                                    I64, I64, P, I64, I64, I64, I32, P]),
     "mpx_gemm_set_config": (C.c_int, [I32]),
     "mpx_attention_fwd": (C.c_int, [P, P, P, I64, I64, I64, I64, I32, P]),
-    "mpx_attention_bwd": (C.c_int, [P, P, P, P, I64, I64, I64, I64, I32, P]),
+    "mpx_attention_bwd": (C.c_int, [P, P, P, P, I64, I64, I64, I64, I32, P, SZ, P]),
+    "mpx_attention_bwd_workspace": (SZ, [I64, I64, I64, I64]),
     "mpx_layernorm_fwd": (C.c_int, [P, I64, P, P, P, P, I64, I64, I32, P]),
     "mpx_layernorm_bwd": (C.c_int, [P, I64, P, P, P, P, I64, P, P, I64, I64, I32, P, SZ, P]),
     "mpx_layernorm_bwd_workspace": (SZ, [I64, I64]),
@@ -179,6 +180,10 @@ mpx_zero = _call("mpx_zero")
 
 def mpx_linear_bwd_workspace(M: int, N: int, K: int) -> int:
     return int(lib.mpx_linear_bwd_workspace(M, N, K))
+
+
+def mpx_attention_bwd_workspace(B: int, T: int, H: int, hd: int) -> int:
+    return int(lib.mpx_attention_bwd_workspace(B, T, H, hd))
 
 
 def mpx_loss_workspace(n: int) -> int:

@@ -1,4 +1,4 @@
-// Fused multi-head self-attention core for short sequences (T <= 128, head
+// Fused multi-head self-attention core for short sequences (T <= 256, head
 // dimension 64), forward and backward, with the half-precision policy of
 // MPX (§2.1: products in half with float32 accumulation; §3.2: the softmax
 // and its backward run in full precision as a force_full_precision island):
@@ -10,14 +10,18 @@
 //             dQ = half(dS K),  dK = half(dS^T Q)
 //
 // One workgroup per (batch, head) with one wave per 32-row block of the
-// sequence.  Each wave computes the transposed score block S^T = K Q^T for
+// sequence (up to 8 waves).  Each wave computes the transposed score block S^T = K Q^T for
 // its 32 queries, so that a lane holds one query (column) and half of every
 // key block (rows): the softmax reductions over keys are lane-local plus one
 // exchange with the lane 32 apart.  The probabilities then feed the P V
 // product straight from registers: a v_permlane32_swap turns the
 // accumulator layout into the MFMA B-operand layout (8 consecutive keys per
 // lane).  V, and in the backward K, Q, dO, P and dS, are staged in LDS and
-// read as transposed MFMA operands with ds_read_b64_tr_b16.
+// read as transposed MFMA operands with ds_read_b64_tr_b16.  Up to T = 128
+// the backward is one kernel; beyond, the [T, T] probability and dS blocks no
+// longer fit in LDS next to K, Q and dO, so dS goes through a workspace: one
+// kernel per query block (dS, dQ), then one per key block (dK, dV, reducing
+// over queries in blocks of 32 staged through LDS).
 //
 // Layouts: qkv [B*T, 3*H*64] (Q | K | V, head h at columns h*64 of each
 // third), O and dO [B*T, H*64], dqkv like qkv, P [B*H, T, ldP] with
@@ -178,37 +182,15 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_kernel(const uint16_t* __res
 
 // ---------------------------------------------------------------- backward --
 
+// Per query block (the wave's 32 queries q): dP^T = V dO^T rounded to half,
+// the probabilities P of query q, and dS = half(scale P (dP - rowsum(dP P)))
+// (0 for keys >= T and for queries >= T).  Pr / Sr hold 4 consecutive keys
+// 32 j + 8 gq + 4 hi + (0..3) per entry, as in the forward.
 template <int DT, int NB>
-__global__ __launch_bounds__(NB * 64) void attn_bwd_kernel(const uint16_t* __restrict__ qkv,
-                                                           const uint16_t* __restrict__ P,
-                                                           const uint16_t* __restrict__ dO,
-                                                           uint16_t* __restrict__ dqkv, int T, int H,
-                                                           int ldP, float scale) {
-  constexpr int TK = 32 * NB;
-  constexpr int PK = TK + 16;  // pitch (halves) of the [query][key] arrays
-  __shared__ __attribute__((aligned(16))) uint16_t sK[TK * PD];
-  __shared__ __attribute__((aligned(16))) uint16_t sQ[TK * PD];
-  __shared__ __attribute__((aligned(16))) uint16_t sdO[TK * PD];
-  __shared__ __attribute__((aligned(16))) uint16_t sP[TK * PK];
-  __shared__ __attribute__((aligned(16))) uint16_t sdS[TK * PK];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hi = lane >> 5;
-  const int bh = blockIdx.x, b = bh / H, h = bh % H;
-  const int dm = H * HD;
-  const int64_t ld = 3 * (int64_t)dm;
-  const uint16_t* Q = qkv + (int64_t)b * T * ld + h * HD;
-  const uint16_t* K = Q + dm;
-  const uint16_t* V = Q + 2 * dm;
-  const uint16_t* G = dO + (int64_t)b * T * dm + h * HD;
-  uint16_t* dQ = dqkv + (int64_t)b * T * ld + h * HD;
-  uint16_t* dK = dQ + dm;
-  uint16_t* dV = dQ + 2 * dm;
-
-  stage_rows(sK, K, ld, T, TK, tid, NB * 64);
-  stage_rows(sQ, Q, ld, T, TK, tid, NB * 64);
-  stage_rows(sdO, G, dm, T, TK, tid, NB * 64);
-
-  // ---- per query block (wave w): dP^T, dS, dQ
-  const int q = 32 * w + (lane & 31);
+__device__ __forceinline__ void bwd_query_block(const uint16_t* V, int64_t ld, const uint16_t* G, int dm,
+                                                const uint16_t* Prow, int q, int T, float scale,
+                                                int lane, u32x2 (&Pr)[NB][4], u32x2 (&Sr)[NB][4]) {
+  const int hi = lane >> 5;
   const int qc = min(q, T - 1);
   uint4 gf[4];
 #pragma unroll
@@ -223,14 +205,12 @@ __global__ __launch_bounds__(NB * 64) void attn_bwd_kernel(const uint16_t* __res
     for (int kk = 0; kk < 4; ++kk) acc = mfma32<DT>(ld_u4(V + key * ld + 16 * kk + 8 * hi), gf[kk], acc);
     dp[j] = acc;
   });
-  // P of query q (keys >= T hold 0; queries >= T read as 0)
-  u32x2 Pr[NB][4];
   float rs = 0.0f;
   static_for<NB>([&](auto j) {
 #pragma unroll
     for (int gq = 0; gq < 4; ++gq) {
       const int key0 = 32 * j + 8 * gq + 4 * hi;
-      Pr[j][gq] = (q < T && key0 < T) ? ld_u2(P + ((int64_t)bh * T + q) * ldP + key0) : u32x2{0u, 0u};
+      Pr[j][gq] = (q < T && key0 < T) ? ld_u2(Prow + key0) : u32x2{0u, 0u};
       const uint16_t ph[4] = {(uint16_t)(Pr[j][gq].x & 0xFFFFu), (uint16_t)(Pr[j][gq].x >> 16),
                               (uint16_t)(Pr[j][gq].y & 0xFFFFu), (uint16_t)(Pr[j][gq].y >> 16)};
 #pragma unroll
@@ -242,7 +222,6 @@ __global__ __launch_bounds__(NB * 64) void attn_bwd_kernel(const uint16_t* __res
     }
   });
   rs += __shfl_xor(rs, 32);
-  u32x2 Sr[NB][4];
   static_for<NB>([&](auto j) {
 #pragma unroll
     for (int gq = 0; gq < 4; ++gq) {
@@ -256,40 +235,107 @@ __global__ __launch_bounds__(NB * 64) void attn_bwd_kernel(const uint16_t* __res
         ds[c] = ok ? f2h<DT>((scale * h2f<DT>(ph[c])) * (dp[j][4 * gq + c] - rs)) : (uint16_t)0;
       }
       Sr[j][gq] = pack4(ds[0], ds[1], ds[2], ds[3]);
-      // the [query][key] copies for the dK / dV products (rows >= T are 0)
+    }
+  });
+}
+
+// dQ^T = K^T dS^T for the wave's queries (K staged in LDS as [key][d]),
+// stored for queries < T.
+template <int DT, int NB>
+__device__ __forceinline__ void bwd_dq(uint32_t kbase, const u32x2 (&Sr)[NB][4], uint16_t* dQrow, int q,
+                                       int T, int lane) {
+  const int hi = lane >> 5;
+  f32x16 o[2];
+#pragma unroll
+  for (int db = 0; db < 2; ++db)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) o[db][e] = 0.0f;
+  static_for<2 * NB>([&](auto ks) {
+    const uint4 bf = keys_operand<NB>(Sr, ks);
+#pragma unroll
+    for (int db = 0; db < 2; ++db) o[db] = mfma32<DT>(frag_tr(kbase, PD, 16 * ks, 32 * db, lane), bf, o[db]);
+  });
+  if (q < T) {
+#pragma unroll
+    for (int db = 0; db < 2; ++db)
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq)
+        st_u2(dQrow + 32 * db + 8 * gq + 4 * hi,
+              pack4(f2h<DT>(o[db][4 * gq]), f2h<DT>(o[db][4 * gq + 1]), f2h<DT>(o[db][4 * gq + 2]),
+                    f2h<DT>(o[db][4 * gq + 3])));
+  }
+}
+
+// Store dK and dV rows of the wave's key block (accumulator runs of 4
+// consecutive keys of one d, transposed to 4 consecutive d of one key).
+template <int DT>
+__device__ __forceinline__ void store_kv_block(const f32x16 (&dk)[2], const f32x16 (&dv)[2], uint16_t* dK,
+                                               uint16_t* dV, int64_t ld, int key_base, int T, int lane) {
+  const int hi = lane >> 5, q4 = lane & 3;
+  const int col = 4 * ((lane & 31) >> 2);
+#pragma unroll
+  for (int db = 0; db < 2; ++db)
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      float a[4] = {dk[db][4 * gq], dk[db][4 * gq + 1], dk[db][4 * gq + 2], dk[db][4 * gq + 3]};
+      float c[4] = {dv[db][4 * gq], dv[db][4 * gq + 1], dv[db][4 * gq + 2], dv[db][4 * gq + 3]};
+      quad_transpose(a, q4);
+      quad_transpose(c, q4);
+      const int key = key_base + 8 * gq + 4 * hi + q4;
+      if (key < T) {
+        st_u2(dK + key * ld + 32 * db + col, pack4(f2h<DT>(a[0]), f2h<DT>(a[1]), f2h<DT>(a[2]), f2h<DT>(a[3])));
+        st_u2(dV + key * ld + 32 * db + col, pack4(f2h<DT>(c[0]), f2h<DT>(c[1]), f2h<DT>(c[2]), f2h<DT>(c[3])));
+      }
+    }
+}
+
+// T <= 128: the whole backward of one (batch, head) in one workgroup.
+template <int DT, int NB>
+__global__ __launch_bounds__(NB * 64) void attn_bwd_kernel(const uint16_t* __restrict__ qkv,
+                                                           const uint16_t* __restrict__ P,
+                                                           const uint16_t* __restrict__ dO,
+                                                           uint16_t* __restrict__ dqkv, int T, int H,
+                                                           int ldP, float scale) {
+  constexpr int TK = 32 * NB;
+  constexpr int PK = TK + 16;  // pitch (halves) of the [query][key] arrays
+  __shared__ __attribute__((aligned(16))) uint16_t sK[TK * PD];
+  __shared__ __attribute__((aligned(16))) uint16_t sQ[TK * PD];
+  __shared__ __attribute__((aligned(16))) uint16_t sdO[TK * PD];
+  __shared__ __attribute__((aligned(16))) uint16_t sP[TK * PK];
+  __shared__ __attribute__((aligned(16))) uint16_t sdS[TK * PK];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int bh = blockIdx.x, b = bh / H, h = bh % H;
+  const int dm = H * HD;
+  const int64_t ld = 3 * (int64_t)dm;
+  const uint16_t* Q = qkv + (int64_t)b * T * ld + h * HD;
+  const uint16_t* K = Q + dm;
+  const uint16_t* V = Q + 2 * dm;
+  const uint16_t* G = dO + (int64_t)b * T * dm + h * HD;
+  uint16_t* dQ = dqkv + (int64_t)b * T * ld + h * HD;
+
+  stage_rows(sK, K, ld, T, TK, tid, NB * 64);
+  stage_rows(sQ, Q, ld, T, TK, tid, NB * 64);
+  stage_rows(sdO, G, dm, T, TK, tid, NB * 64);
+
+  const int q = 32 * w + (lane & 31);
+  u32x2 Pr[NB][4], Sr[NB][4];
+  bwd_query_block<DT, NB>(V, ld, G, dm, P + ((int64_t)bh * T + min(q, T - 1)) * ldP, q, T, scale, lane,
+                          Pr, Sr);
+  // the [query][key] copies for the dK / dV products (rows >= T are 0)
+  static_for<NB>([&](auto j) {
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const int key0 = 32 * j + 8 * gq + 4 * (lane >> 5);
       *reinterpret_cast<u32x2*>(sP + q * PK + key0) = Pr[j][gq];
       *reinterpret_cast<u32x2*>(sdS + q * PK + key0) = Sr[j][gq];
     }
   });
   __syncthreads();  // sK / sQ / sdO staged, sP / sdS complete
 
-  // dQ^T = K^T dS^T: rows = d, columns = the wave's queries
-  const uint32_t kbase = lds_u32(sK), qbase = lds_u32(sQ), gbase = lds_u32(sdO);
-  const uint32_t pbase = lds_u32(sP), sbase = lds_u32(sdS);
-  {
-    f32x16 o[2];
-#pragma unroll
-    for (int db = 0; db < 2; ++db)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) o[db][e] = 0.0f;
-    static_for<2 * NB>([&](auto ks) {
-      const uint4 bf = keys_operand<NB>(Sr, ks);
-#pragma unroll
-      for (int db = 0; db < 2; ++db) o[db] = mfma32<DT>(frag_tr(kbase, PD, 16 * ks, 32 * db, lane), bf, o[db]);
-    });
-    if (q < T) {
-#pragma unroll
-      for (int db = 0; db < 2; ++db)
-#pragma unroll
-        for (int gq = 0; gq < 4; ++gq)
-          st_u2(dQ + q * ld + 32 * db + 8 * gq + 4 * hi,
-                pack4(f2h<DT>(o[db][4 * gq]), f2h<DT>(o[db][4 * gq + 1]), f2h<DT>(o[db][4 * gq + 2]),
-                      f2h<DT>(o[db][4 * gq + 3])));
-    }
-  }
+  bwd_dq<DT, NB>(lds_u32(sK), Sr, dQ + q * ld, q, T, lane);
 
-  // ---- per key block (wave w): dK = dS^T Q and dV = P^T dO, rows = keys of
-  // block w, columns = d, reduced over all queries
+  // per key block (wave w): dK = dS^T Q and dV = P^T dO over all queries
+  const uint32_t qbase = lds_u32(sQ), gbase = lds_u32(sdO), pbase = lds_u32(sP), sbase = lds_u32(sdS);
   f32x16 dk[2], dv[2];
 #pragma unroll
   for (int db = 0; db < 2; ++db)
@@ -304,48 +350,148 @@ __global__ __launch_bounds__(NB * 64) void attn_bwd_kernel(const uint16_t* __res
       dv[db] = mfma32<DT>(pa, frag_tr(gbase, PD, 16 * ks, 32 * db, lane), dv[db]);
     }
   });
-  // accumulator runs (4 consecutive keys of one d) -> 4 consecutive d of one key
-  const int q4 = lane & 3;
-  const int col = 4 * ((lane & 31) >> 2);
+  store_kv_block<DT>(dk, dv, dQ + dm, dQ + 2 * dm, ld, 32 * w, T, lane);
+}
+
+// 128 < T <= 256, first kernel: per query block dS (kept in the workspace,
+// [B*H, T, ldP] like P) and dQ.
+template <int DT, int NB>
+__global__ __launch_bounds__(NB * 64) void attn_bwd_dq_kernel(const uint16_t* __restrict__ qkv,
+                                                              const uint16_t* __restrict__ P,
+                                                              const uint16_t* __restrict__ dO,
+                                                              uint16_t* __restrict__ dqkv,
+                                                              uint16_t* __restrict__ dS, int T, int H,
+                                                              int ldP, float scale) {
+  constexpr int TK = 32 * NB;
+  __shared__ __attribute__((aligned(16))) uint16_t sK[TK * PD];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int bh = blockIdx.x, b = bh / H, h = bh % H;
+  const int dm = H * HD;
+  const int64_t ld = 3 * (int64_t)dm;
+  const uint16_t* Q = qkv + (int64_t)b * T * ld + h * HD;
+  const uint16_t* G = dO + (int64_t)b * T * dm + h * HD;
+  stage_rows(sK, Q + dm, ld, T, TK, tid, NB * 64);
+
+  const int q = 32 * w + (lane & 31);
+  const int64_t row = (int64_t)bh * T + min(q, T - 1);
+  u32x2 Pr[NB][4], Sr[NB][4];
+  bwd_query_block<DT, NB>(Q + 2 * dm, ld, G, dm, P + row * ldP, q, T, scale, lane, Pr, Sr);
+  if (q < T) {
+    static_for<NB>([&](auto j) {
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        const int key0 = 32 * j + 8 * gq + 4 * (lane >> 5);
+        if (key0 < ldP) st_u2(dS + row * ldP + key0, Sr[j][gq]);
+      }
+    });
+  }
+  __syncthreads();  // sK staged
+  bwd_dq<DT, NB>(lds_u32(sK), Sr, dqkv + (int64_t)b * T * ld + h * HD + q * ld, q, T, lane);
+}
+
+// 128 < T <= 256, second kernel: per key block (wave w) dK = dS^T Q and
+// dV = P^T dO, reduced over the queries in blocks of 32 staged through LDS.
+template <int DT, int NB>
+__global__ __launch_bounds__(NB * 64) void attn_bwd_dkv_kernel(const uint16_t* __restrict__ qkv,
+                                                               const uint16_t* __restrict__ P,
+                                                               const uint16_t* __restrict__ dO,
+                                                               const uint16_t* __restrict__ dS,
+                                                               uint16_t* __restrict__ dqkv, int T, int H,
+                                                               int ldP) {
+  constexpr int TK = 32 * NB;
+  constexpr int PK = TK + 16;
+  __shared__ __attribute__((aligned(16))) uint16_t sQ[32 * PD];
+  __shared__ __attribute__((aligned(16))) uint16_t sdO[32 * PD];
+  __shared__ __attribute__((aligned(16))) uint16_t sP[32 * PK];
+  __shared__ __attribute__((aligned(16))) uint16_t sdS[32 * PK];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int nthreads = NB * 64;
+  const int bh = blockIdx.x, b = bh / H, h = bh % H;
+  const int dm = H * HD;
+  const int64_t ld = 3 * (int64_t)dm;
+  const uint16_t* Q = qkv + (int64_t)b * T * ld + h * HD;
+  const uint16_t* G = dO + (int64_t)b * T * dm + h * HD;
+  const uint16_t* Pb = P + (int64_t)bh * T * ldP;
+  const uint16_t* Sb = dS + (int64_t)bh * T * ldP;
+  const uint32_t qbase = lds_u32(sQ), gbase = lds_u32(sdO), pbase = lds_u32(sP), sbase = lds_u32(sdS);
+  f32x16 dk[2], dv[2];
 #pragma unroll
   for (int db = 0; db < 2; ++db)
 #pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      float a[4] = {dk[db][4 * gq], dk[db][4 * gq + 1], dk[db][4 * gq + 2], dk[db][4 * gq + 3]};
-      float c[4] = {dv[db][4 * gq], dv[db][4 * gq + 1], dv[db][4 * gq + 2], dv[db][4 * gq + 3]};
-      quad_transpose(a, q4);
-      quad_transpose(c, q4);
-      const int key = 32 * w + 8 * gq + 4 * hi + q4;
-      if (key < T) {
-        st_u2(dK + key * ld + 32 * db + col, pack4(f2h<DT>(a[0]), f2h<DT>(a[1]), f2h<DT>(a[2]), f2h<DT>(a[3])));
-        st_u2(dV + key * ld + 32 * db + col, pack4(f2h<DT>(c[0]), f2h<DT>(c[1]), f2h<DT>(c[2]), f2h<DT>(c[3])));
+    for (int e = 0; e < 16; ++e) dk[db][e] = dv[db][e] = 0.0f;
+  for (int q0 = 0; q0 < T; q0 += 32) {
+    __syncthreads();  // the previous block's reads are done
+    stage_rows(sQ, Q + q0 * ld, ld, T - q0, 32, tid, nthreads);
+    stage_rows(sdO, G + q0 * dm, dm, T - q0, 32, tid, nthreads);
+    for (int c = tid; c < 32 * (TK / 8); c += nthreads) {
+      const int r = c / (TK / 8), col = (c % (TK / 8)) * 8;
+      u32x4 pv = {0u, 0u, 0u, 0u}, sv = {0u, 0u, 0u, 0u};
+      if (q0 + r < T && col < ldP) {
+        pv = *reinterpret_cast<const u32x4*>(Pb + (int64_t)(q0 + r) * ldP + col);
+        sv = *reinterpret_cast<const u32x4*>(Sb + (int64_t)(q0 + r) * ldP + col);
+      }
+      *reinterpret_cast<u32x4*>(sP + r * PK + col) = pv;
+      *reinterpret_cast<u32x4*>(sdS + r * PK + col) = sv;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const uint4 sa = frag_tr(sbase, PK, 16 * ks, 32 * w, lane);
+      const uint4 pa = frag_tr(pbase, PK, 16 * ks, 32 * w, lane);
+#pragma unroll
+      for (int db = 0; db < 2; ++db) {
+        dk[db] = mfma32<DT>(sa, frag_tr(qbase, PD, 16 * ks, 32 * db, lane), dk[db]);
+        dv[db] = mfma32<DT>(pa, frag_tr(gbase, PD, 16 * ks, 32 * db, lane), dv[db]);
       }
     }
+  }
+  uint16_t* dQ = dqkv + (int64_t)b * T * ld + h * HD;
+  store_kv_block<DT>(dk, dv, dQ + dm, dQ + 2 * dm, ld, 32 * w, T, lane);
 }
 
 template <int DT>
 hipError_t launch_fwd(const uint16_t* qkv, uint16_t* O, uint16_t* P, int B, int T, int H, int ldP,
                       float scale, hipStream_t s) {
   const dim3 grid((unsigned)(B * H));
-  switch ((T + 31) / 32) {
-    case 1: attn_fwd_kernel<DT, 1><<<grid, 64, 0, s>>>(qkv, O, P, T, H, ldP, scale); break;
-    case 2: attn_fwd_kernel<DT, 2><<<grid, 128, 0, s>>>(qkv, O, P, T, H, ldP, scale); break;
-    case 3: attn_fwd_kernel<DT, 3><<<grid, 192, 0, s>>>(qkv, O, P, T, H, ldP, scale); break;
-    default: attn_fwd_kernel<DT, 4><<<grid, 256, 0, s>>>(qkv, O, P, T, H, ldP, scale); break;
+  const int nb = (T + 31) / 32;
+#define MPX_F(NBv) attn_fwd_kernel<DT, NBv><<<grid, NBv * 64, 0, s>>>(qkv, O, P, T, H, ldP, scale)
+  switch (nb) {
+    case 1: MPX_F(1); break;
+    case 2: MPX_F(2); break;
+    case 3: MPX_F(3); break;
+    case 4: MPX_F(4); break;
+    case 5: MPX_F(5); break;
+    case 6: MPX_F(6); break;
+    case 7: MPX_F(7); break;
+    default: MPX_F(8); break;
   }
+#undef MPX_F
   return hipGetLastError();
 }
 
 template <int DT>
 hipError_t launch_bwd(const uint16_t* qkv, const uint16_t* P, const uint16_t* dO, uint16_t* dqkv,
-                      int B, int T, int H, int ldP, float scale, hipStream_t s) {
+                      uint16_t* dS, int B, int T, int H, int ldP, float scale, hipStream_t s) {
   const dim3 grid((unsigned)(B * H));
-  switch ((T + 31) / 32) {
-    case 1: attn_bwd_kernel<DT, 1><<<grid, 64, 0, s>>>(qkv, P, dO, dqkv, T, H, ldP, scale); break;
-    case 2: attn_bwd_kernel<DT, 2><<<grid, 128, 0, s>>>(qkv, P, dO, dqkv, T, H, ldP, scale); break;
-    case 3: attn_bwd_kernel<DT, 3><<<grid, 192, 0, s>>>(qkv, P, dO, dqkv, T, H, ldP, scale); break;
-    default: attn_bwd_kernel<DT, 4><<<grid, 256, 0, s>>>(qkv, P, dO, dqkv, T, H, ldP, scale); break;
+  const int nb = (T + 31) / 32;
+#define MPX_B(NBv) attn_bwd_kernel<DT, NBv><<<grid, NBv * 64, 0, s>>>(qkv, P, dO, dqkv, T, H, ldP, scale)
+#define MPX_B2(NBv)                                                                              \
+  do {                                                                                           \
+    attn_bwd_dq_kernel<DT, NBv><<<grid, NBv * 64, 0, s>>>(qkv, P, dO, dqkv, dS, T, H, ldP, scale); \
+    attn_bwd_dkv_kernel<DT, NBv><<<grid, NBv * 64, 0, s>>>(qkv, P, dO, dS, dqkv, T, H, ldP);       \
+  } while (0)
+  switch (nb) {
+    case 1: MPX_B(1); break;
+    case 2: MPX_B(2); break;
+    case 3: MPX_B(3); break;
+    case 4: MPX_B(4); break;
+    case 5: MPX_B2(5); break;
+    case 6: MPX_B2(6); break;
+    case 7: MPX_B2(7); break;
+    default: MPX_B2(8); break;
   }
+#undef MPX_B
+#undef MPX_B2
   return hipGetLastError();
 }
 
@@ -363,8 +509,8 @@ extern "C" int mpx_attention_fwd(const void* qkv, void* O, void* P, int64_t B, i
   MPX_REQUIRE(B >= 1 && T >= 1 && H >= 1, "B, T, H must be >= 1");
   MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
   MPX_REQUIRE(B * H <= INT32_MAX && B * T * H * 3 * 64 < ((int64_t)1 << 31), "problem too large");
-  if (hd != 64 || T > 128) {
-    set_error("mpx_attention_fwd: implemented for head dimension 64 and T <= 128");
+  if (hd != 64 || T > 256) {
+    set_error("mpx_attention_fwd: implemented for head dimension 64 and T <= 256");
     return MPX_ERR_UNSUPPORTED;
   }
   MPX_REQUIRE(aligned16(qkv) && aligned16(O) && (reinterpret_cast<uintptr_t>(P) & 7u) == 0,
@@ -381,28 +527,42 @@ extern "C" int mpx_attention_fwd(const void* qkv, void* O, void* P, int64_t B, i
   return MPX_OK;
 }
 
+extern "C" size_t mpx_attention_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t hd) {
+  if (B < 1 || T <= 128 || H < 1 || hd != 64 || T > 256) return 0;
+  return (size_t)(B * H * T * ((T + 7) / 8 * 8)) * 2;
+}
+
 extern "C" int mpx_attention_bwd(const void* qkv, const void* P, const void* dO, void* dqkv, int64_t B,
-                                 int64_t T, int64_t H, int64_t hd, mpx_dtype dt, void* stream) {
+                                 int64_t T, int64_t H, int64_t hd, mpx_dtype dt, void* workspace,
+                                 size_t ws_bytes, void* stream) {
   clear_error();
   MPX_REQUIRE(qkv && P && dO && dqkv, "NULL operand");
   MPX_REQUIRE(B >= 1 && T >= 1 && H >= 1, "B, T, H must be >= 1");
   MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
   MPX_REQUIRE(B * H <= INT32_MAX && B * T * H * 3 * 64 < ((int64_t)1 << 31), "problem too large");
-  if (hd != 64 || T > 128) {
-    set_error("mpx_attention_bwd: implemented for head dimension 64 and T <= 128");
+  if (hd != 64 || T > 256) {
+    set_error("mpx_attention_bwd: implemented for head dimension 64 and T <= 256");
     return MPX_ERR_UNSUPPORTED;
   }
   MPX_REQUIRE(aligned16(qkv) && aligned16(dO) && aligned16(dqkv) &&
                   (reinterpret_cast<uintptr_t>(P) & 7u) == 0,
               "qkv, dO and dqkv must be 16-byte aligned, P 8-byte aligned");
+  const size_t need = mpx_attention_bwd_workspace(B, T, H, hd);
+  if (need && (!workspace || ws_bytes < need || !aligned16(workspace))) {
+    set_error("mpx_attention_bwd: a 16-byte aligned workspace of " + std::to_string(need) +
+              " bytes is required");
+    return MPX_ERR_WORKSPACE;
+  }
   const int ldP = (int)((T + 7) / 8 * 8);
   const float scale = (float)(1.0 / std::sqrt((double)hd));
   hipStream_t s = (hipStream_t)stream;
   if (dt == MPX_F16)
     MPX_HIP(launch_bwd<MPX_F16>((const uint16_t*)qkv, (const uint16_t*)P, (const uint16_t*)dO,
-                                (uint16_t*)dqkv, (int)B, (int)T, (int)H, ldP, scale, s));
+                                (uint16_t*)dqkv, (uint16_t*)workspace, (int)B, (int)T, (int)H, ldP, scale,
+                                s));
   else
     MPX_HIP(launch_bwd<MPX_BF16>((const uint16_t*)qkv, (const uint16_t*)P, (const uint16_t*)dO,
-                                 (uint16_t*)dqkv, (int)B, (int)T, (int)H, ldP, scale, s));
+                                 (uint16_t*)dqkv, (uint16_t*)workspace, (int)B, (int)T, (int)H, ldP,
+                                 scale, s));
   return MPX_OK;
 }

@@ -336,7 +336,8 @@ class ViTStep(TrainStep):
         if cfg.image:
             shapes.append((B * cfg.n_patches, d, cfg.patch_dim))
         ws = max(mx.mpx_linear_bwd_workspace(*s) for s in shapes)
-        ws = max(ws, mx.mpx_layernorm_bwd_workspace(M, d), mx.mpx_loss_workspace(B))
+        ws = max(ws, mx.mpx_layernorm_bwd_workspace(M, d), mx.mpx_loss_workspace(B),
+                 mx.mpx_attention_bwd_workspace(B, T, H, cfg.head_dim))
         self.ws = torch.zeros(ws, dtype=torch.uint8, device=dev)
 
     def _dominant_call(self, s):
@@ -368,12 +369,12 @@ class ViTStep(TrainStep):
             self.tok32.copy_(torch.from_numpy(batch["x"].reshape(c.batch * c.tokens, c.d_model)))
         self.labels.copy_(torch.from_numpy(batch["labels"].astype(np.int32)))
 
-    # attention core of one block: S = Q K^T, P = softmax, O = P V.  Short
-    # sequences (T <= 128, head dim 64) run the fused kernels; longer ones
-    # the batched GEMMs around the row softmax.
+    # attention core of one block: S = Q K^T, P = softmax, O = P V.  Sequences
+    # up to 256 tokens with head dim 64 run the fused kernels; others the
+    # batched GEMMs around the row softmax.
     def _fused_attention(self):
         c = self.cfg
-        return c.tokens <= 128 and c.head_dim == 64
+        return c.tokens <= 256 and c.head_dim == 64
 
     def _attn_fwd(self, blk, s):
         c, dt = self.cfg, self.dt
@@ -397,7 +398,8 @@ class ViTStep(TrainStep):
         B, T, d, H, hd, ldT = c.batch, c.tokens, c.d_model, c.heads, c.head_dim, self.ldT
         qkv, P, dO, dqkv = blk["qkv"], blk["P"], self.dO, self.dqkv
         if self._fused_attention():
-            mx.mpx_attention_bwd(_ptr(qkv), _ptr(P), _ptr(dO), _ptr(dqkv), B, T, H, hd, dt, s)
+            mx.mpx_attention_bwd(_ptr(qkv), _ptr(P), _ptr(dO), _ptr(dqkv), B, T, H, hd, dt,
+                                 _ptr(self.ws), self.ws.numel(), s)
             return
         # dP = dO V^T
         mx.mpx_gemm_batched(0, 1, T, T, hd, B, H, _ptr(dO), d, T * d, hd,

@@ -27,7 +27,8 @@ if HAVE_GPU:
     from paper_2507_03312_amd import binding as mx
 
 HD = 64
-SHAPES = [(2, 2, 1), (2, 3, 5), (1, 2, 32), (2, 2, 33), (2, 3, 65), (1, 2, 97), (1, 2, 128)]
+SHAPES = [(2, 2, 1), (2, 3, 5), (1, 2, 32), (2, 2, 33), (2, 3, 65), (1, 2, 97), (1, 2, 128),
+          (1, 2, 129), (2, 2, 197), (1, 1, 200), (1, 2, 256)]
 
 
 def _s():
@@ -60,8 +61,10 @@ def _run(B, T, H, fmt, seed=0):
     tO, tP, tdq = _empty((B * T, d), fmt), _empty((B * H * T, ldP), fmt), _empty((B * T, 3 * d), fmt)
     tP.fill_(7.0)  # padding must be overwritten with 0
     mx.mpx_attention_fwd(tq.data_ptr(), tO.data_ptr(), tP.data_ptr(), B, T, H, HD, dt, _s())
+    ws_n = mx.mpx_attention_bwd_workspace(B, T, H, HD)
+    ws = torch.zeros(max(ws_n, 16), dtype=torch.uint8, device="cuda")
     mx.mpx_attention_bwd(tq.data_ptr(), tP.data_ptr(), tdo.data_ptr(), tdq.data_ptr(), B, T, H, HD,
-                         dt, _s())
+                         dt, ws.data_ptr() if ws_n else None, ws_n, _s())
     torch.cuda.synchronize()
     return pol, qkv, dout, to_host(tO), to_host(tP).reshape(B, H, T, ldP), to_host(tdq)
 
@@ -120,10 +123,10 @@ def test_fused_attention(fmt, bth):
     _check_bwd(pol, fmt, qkv, dout, B, T, H, gP, gdq)
 
 
-@pytest.mark.parametrize("fmt,bth", [("bf16", (128, 6, 65)), ("f16", (256, 6, 65))],
+@pytest.mark.parametrize("fmt,bth", [("bf16", (128, 6, 65)), ("f16", (256, 6, 65)), ("bf16", (64, 12, 197))],
                          ids=lambda s: str(s))
 def test_fused_attention_full_size(fmt, bth):
-    """The ViT-block and ViT-S attention shapes, every element checked."""
+    """The ViT-block, ViT-S and ViT-B attention shapes, every element checked."""
     B, H, T = bth
     pol, qkv, dout, gO, gPfull, gdq = _run(B, T, H, fmt, seed=3)
     _, _, _, gP = _check_fwd(pol, fmt, qkv, B, T, H, gO, gPfull)
@@ -133,7 +136,10 @@ def test_fused_attention_full_size(fmt, bth):
 def test_fused_attention_limits():
     t = _empty((64, 3 * 64), "bf16")
     with pytest.raises(mx.MPXError, match="implemented for"):
-        mx.mpx_attention_fwd(t.data_ptr(), t.data_ptr(), t.data_ptr(), 1, 129, 1, 64, mx.MPX_BF16, _s())
+        mx.mpx_attention_fwd(t.data_ptr(), t.data_ptr(), t.data_ptr(), 1, 257, 1, 64, mx.MPX_BF16, _s())
     with pytest.raises(mx.MPXError, match="implemented for"):
         mx.mpx_attention_bwd(t.data_ptr(), t.data_ptr(), t.data_ptr(), t.data_ptr(), 1, 8, 1, 32,
-                             mx.MPX_BF16, _s())
+                             mx.MPX_BF16, None, 0, _s())
+    with pytest.raises(mx.MPXError, match="workspace"):
+        mx.mpx_attention_bwd(t.data_ptr(), t.data_ptr(), t.data_ptr(), t.data_ptr(), 1, 200, 1, 64,
+                             mx.MPX_BF16, None, 0, _s())
