@@ -73,13 +73,13 @@ template <> __device__ __forceinline__ bool h_nonfinite<MPX_BF16>(uint16_t h) {
 // sigma = (1 + tanh(u)) / 2 = 1 / (1 + exp(-2u)), u = c (x + a x^3):
 //   gelu(x) = x sigma,  gelu'(x) = sigma + 2 x sigma (1 - sigma) c (1 + 3 a x^2).
 // The sigmoid form avoids the cancellation of 1 + tanh(u) for negative x.
-// sigma = 1 / (1 + exp(-2u)) with the hardware exp2 and reciprocal (about
-// 1e-6 relative error in float32, far inside one half-precision ulp; exp
-// overflowing to +inf gives sigma = 0 as it should).
+// sigma = 1 / (1 + exp(-2u)) = 1 / (1 + 2^(x (k1 + k2 x^2))) with
+// k1 = -2 c log2(e), k2 = -2 c a log2(e), on the hardware exp2 and
+// reciprocal (about 1e-6 relative error in float32, far inside one
+// half-precision ulp; exp2 overflowing to +inf gives sigma = 0 as it should).
 __device__ __forceinline__ float gelu_sigma(float x) {
-  const float c = 0.7978845608028654f, a = 0.044715f;
-  const float u = c * (x + a * x * x * x);
-  return __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * u));
+  const float k1 = -2.302208198144325f, k2 = -0.1029432395800235f;
+  return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * __builtin_fmaf(k2, x * x, k1)));
 }
 __device__ __forceinline__ float gelu_tanh(float x) { return x * gelu_sigma(x); }
 __device__ __forceinline__ float gelu_tanh_grad(float x) {

@@ -49,7 +49,7 @@ struct GemmArgs {
   uint16_t* pre;
   const uint16_t* dact;
   int32_t act;
-  int32_t full_epi;  // set by the dispatcher: whole tiles may use gemm_epilogue_full
+  int32_t full_epi;  // set by the dispatcher: whole tiles may use gemm_epilogue_lds
 };
 
 // Loader of one operand tile (ROWS output rows x BK reduction values) into
@@ -213,16 +213,18 @@ struct TileLoader {
 // being fetched again for every tile row.
 template <int BM, int BN>
 __device__ __forceinline__ void tile_origin(int64_t M, int64_t N, int64_t& m0, int64_t& n0) {
-  constexpr int64_t GM = 8;
-  const int64_t tiles_m = (M + BM - 1) / BM, tiles_n = (N + BN - 1) / BN;
-  const int64_t ntiles = gridDim.x;
-  const int64_t xcd = blockIdx.x % 8, local = blockIdx.x / 8;
-  const int64_t t = xcd * (ntiles / 8) + min(xcd, ntiles % 8) + local;
-  const int64_t first = (t / (GM * tiles_n)) * GM;
-  const int64_t gm = min(tiles_m - first, GM);
-  const int64_t r = t - first * tiles_n;
-  m0 = (first + r % gm) * BM;
-  n0 = (r / gm) * BN;
+  // 32-bit index arithmetic (tile counts stay far below 2^32; a 64-bit
+  // division is a long software sequence)
+  constexpr uint32_t GM = 8;
+  const uint32_t tiles_m = (uint32_t)((M + BM - 1) / BM), tiles_n = (uint32_t)((N + BN - 1) / BN);
+  const uint32_t ntiles = gridDim.x;
+  const uint32_t xcd = blockIdx.x % 8, local = blockIdx.x / 8;
+  const uint32_t t = xcd * (ntiles / 8) + min(xcd, ntiles % 8) + local;
+  const uint32_t first = (t / (GM * tiles_n)) * GM;
+  const uint32_t gm = min(tiles_m - first, GM);
+  const uint32_t r = t - first * tiles_n;
+  m0 = (int64_t)(first + r % gm) * BM;
+  n0 = (int64_t)(r / gm) * BN;
 }
 
 // Epilogue variants chosen at compile time (a mask of these bits), used for
@@ -232,123 +234,115 @@ __device__ __forceinline__ void tile_origin(int64_t M, int64_t N, int64_t& m0, i
 // epilogue's, step for step, so both give identical bits.
 enum : int { EPI_BIAS = 1, EPI_GELU = 2, EPI_DACT = 4, EPI_RESID = 8, EPI_GENERIC = -1 };
 
+// Whole-tile epilogue through LDS, for the transposed accumulator layout and
+// 64 x 64 wave tiles.  Step 1 (accumulator layout: lane = one row, runs of 4
+// consecutive columns): h = half(acc + bias), written to the wave's own
+// [64][68] half region of the LDS the main loop no longer needs.  Step 2 (row
+// layout: lane = 8 consecutive columns of one row): the pre-activation store,
+// GELU, GELU' of the previous layer and the residual add with 16-byte
+// accesses, each store writing 8 rows x 128 contiguous bytes.
 template <int DT, int TM, int TN, int E>
-__device__ __forceinline__ void gemm_epilogue_full(const GemmArgs& g, const f32x16 (&acc)[TM][TN],
-                                                   int64_t mw, int64_t nw, int lane, int64_t offC) {
-  static_assert(TN % 2 == 0, "column blocks are paired");
-  const int q4 = lane & 3;
-  const int hi = lane >> 5;
-  const int row_l = 4 * hi + q4;
-  const int col_l = 4 * ((lane & 31) >> 2);
-  const int64_t ldc = g.ldc;
-  uint16_t* C = g.C + (offC + mw * ldc + nw);         // wave-uniform bases
-  uint16_t* pre = (E & EPI_GELU) ? g.pre + (mw * ldc + nw) : nullptr;
-  const uint16_t* dact = (E & EPI_DACT) ? g.dact + (mw * ldc + nw) : nullptr;
-  const uint16_t* res = (E & EPI_RESID) ? g.resid + (mw * g.ldr + nw) : nullptr;
-  // inputs are read where the accumulators sit: row row_l, columns col_l..+3
-  const uint32_t in_off = (uint32_t)(row_l * ldc + col_l);
-  const uint32_t res_off = (E & EPI_RESID) ? (uint32_t)(row_l * g.ldr + col_l) : 0u;
-  // outputs are written after pairing the column blocks (2p, 2p + 1): a lane
-  // then holds row q4 (first block of the pair) or 4 + q4 (second) of the
-  // 8-row group, columns 32 * hi + col_l, so one store covers 4 rows x 64
-  // columns = whole 128-byte row segments
-  const uint32_t out_off = (uint32_t)(q4 * ldc + 32 * hi + col_l);
+__device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, const f32x16 (&acc)[TM][TN],
+                                                  int64_t mw, int64_t nw, int lane, int64_t offC,
+                                                  uint16_t* lds) {
+  static_assert(TM == 2 && TN == 2, "64 x 64 wave tiles");
+  constexpr int PITCH = 68;  // halves (34 banks): a column of 32 rows spreads over all banks
+  const int hi = lane >> 5, r32 = lane & 31;
   auto unpack = [](u32x2 w, float (&f)[4]) {
     f[0] = h2f<DT>((uint16_t)(w.x & 0xFFFFu));
     f[1] = h2f<DT>((uint16_t)(w.x >> 16));
     f[2] = h2f<DT>((uint16_t)(w.y & 0xFFFFu));
     f[3] = h2f<DT>((uint16_t)(w.y >> 16));
   };
-  auto pack = [](const uint16_t (&h)[4]) {
-    return u32x2{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16)};
+  static_for<TN>([&](auto j) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int col = 32 * j + 8 * q + 4 * hi;
+      float b[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+      if constexpr ((E & EPI_BIAS) != 0) unpack(ld_u2(g.bias + nw + col), b);
+      static_for<TM>([&](auto i) {
+        const int row = 32 * i + r32;
+        uint16_t h[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(acc[i][j][4 * q + c] + b[c]);
+        *reinterpret_cast<u32x2*>(lds + row * PITCH + col) =
+            u32x2{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16)};
+      });
+    }
+  });
+  const int c8 = 8 * (lane & 7);
+  const int64_t ldc = g.ldc;
+  uint16_t* C = g.C + (offC + mw * ldc + nw);
+  uint16_t* pre = (E & EPI_GELU) ? g.pre + (mw * ldc + nw) : nullptr;
+  const uint16_t* dact = (E & EPI_DACT) ? g.dact + (mw * ldc + nw) : nullptr;
+  const uint16_t* res = (E & EPI_RESID) ? g.resid + (mw * g.ldr + nw) : nullptr;
+  auto h8 = [](u32x4 w, uint16_t (&h)[8]) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      h[2 * k] = (uint16_t)(w[k] & 0xFFFFu);
+      h[2 * k + 1] = (uint16_t)(w[k] >> 16);
+    }
   };
-  // the epilogue of one 4-value run of block (i, j): returns the packed
-  // output and (with GELU) the packed pre-activation
-  auto run = [&](const f32x16& a, int i, int j, int qd, const float (&bias)[4], u32x2& out,
-                 u32x2& pre_out) {
-    float v[4] = {a[4 * qd], a[4 * qd + 1], a[4 * qd + 2], a[4 * qd + 3]};
-    quad_transpose(v, q4);
-    const uint32_t rofs = (uint32_t)((i * 32 + 8 * qd) * ldc + j * 32);
-    uint16_t h[4];
+  auto p8 = [](const uint16_t (&h)[8]) {
+    return u32x4{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16),
+                 h[4] | ((uint32_t)h[5] << 16), h[6] | ((uint32_t)h[7] << 16)};
+  };
 #pragma unroll
-    for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(v[c] + bias[c]);
+  for (int t = 0; t < 8; ++t) {
+    const int row = (lane >> 3) + 8 * t;
+    const u32x2 w0 = *reinterpret_cast<const u32x2*>(lds + row * PITCH + c8);
+    const u32x2 w1 = *reinterpret_cast<const u32x2*>(lds + row * PITCH + c8 + 4);
+    uint16_t h[8];
+    h8(u32x4{w0.x, w0.y, w1.x, w1.y}, h);
+    const uint32_t off = (uint32_t)(row * ldc + c8);
     if constexpr ((E & EPI_GELU) != 0) {
-      pre_out = pack(h);
+      *reinterpret_cast<u32x4*>(pre + off) = p8(h);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(gelu_tanh(h2f<DT>(h[c])));
+      for (int c = 0; c < 8; ++c) h[c] = f2h<DT>(gelu_tanh(h2f<DT>(h[c])));
     }
     if constexpr ((E & EPI_DACT) != 0) {
-      float da[4];
-      unpack(*reinterpret_cast<const u32x2*>(dact + in_off + rofs), da);
+      uint16_t da[8];
+      h8(*reinterpret_cast<const u32x4*>(dact + off), da);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) * gelu_tanh_grad(da[c]));
+      for (int c = 0; c < 8; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) * gelu_tanh_grad(h2f<DT>(da[c])));
     }
     if constexpr ((E & EPI_RESID) != 0) {
-      float r[4];
-      unpack(*reinterpret_cast<const u32x2*>(
-                 res + res_off + (uint32_t)((i * 32 + 8 * qd) * g.ldr + j * 32)), r);
+      uint16_t rv[8];
+      h8(*reinterpret_cast<const u32x4*>(res + (uint32_t)(row * g.ldr + c8)), rv);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) + r[c]);
+      for (int c = 0; c < 8; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) + h2f<DT>(rv[c]));
     }
-    out = pack(h);
-  };
-  static_for<TN / 2>([&](auto p) {
-    constexpr int j0 = 2 * p, j1 = 2 * p + 1;
-    float b0[4] = {0.0f, 0.0f, 0.0f, 0.0f}, b1[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-    if constexpr ((E & EPI_BIAS) != 0) {
-      unpack(*reinterpret_cast<const u32x2*>(g.bias + nw + j0 * 32 + col_l), b0);
-      unpack(*reinterpret_cast<const u32x2*>(g.bias + nw + j1 * 32 + col_l), b1);
-    }
-    static_for<TM>([&](auto i) {
-#pragma unroll
-      for (int qd = 0; qd < 4; ++qd) {
-        u32x2 x, y, px{0u, 0u}, py{0u, 0u};
-        run(acc[i][j0], i, j0, qd, b0, x, px);
-        run(acc[i][j1], i, j1, qd, b1, y, py);
-        half_swap(x, y);
-        const uint32_t o = out_off + (uint32_t)((i * 32 + 8 * qd) * ldc + j0 * 32);
-        const uint32_t o4 = o + (uint32_t)(4 * ldc);
-        if constexpr ((E & EPI_GELU) != 0) {
-          half_swap(px, py);
-          *reinterpret_cast<u32x2*>(pre + o) = px;
-          *reinterpret_cast<u32x2*>(pre + o4) = py;
-        }
-        *reinterpret_cast<u32x2*>(C + o) = x;
-        *reinterpret_cast<u32x2*>(C + o4) = y;
-      }
-    });
-  });
+    *reinterpret_cast<u32x4*>(C + off) = p8(h);
+  }
 }
 
-// Epilogue shared by the GEMM kernels: the wave's TM x TN accumulator
-// blocks of 32 x 32 start at output row mw and column nw.
-template <int DT, int TM, int TN>
+// Generic epilogue shared by the GEMM kernels: any tile, any operand
+// alignment, split-K partials.  The wave's TM x TN accumulator blocks of
+// 32 x 32 start at output row mw and column nw.  Two accumulator layouts:
+//   TRANS = false (C = A B^T blocks): lane l holds column l % 32 and 4 runs of
+//     4 consecutive rows; a 4x4 transpose across lane quads (two DPP
+//     butterfly exchanges) turns each run into 4 consecutive columns of one row;
+//   TRANS = true (the MFMA operands swapped, C^T blocks): lane l already holds
+//     row l % 32, columns 8 q + 4 (l / 32) + (0..3) for q = 0..3.
+// Either way bias / residual / activation inputs are read and outputs written
+// 4 elements (8 bytes; 16 for float partials) at a time.
+template <int DT, int TM, int TN, bool TRANS = false>
 __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const f32x16 (&acc)[TM][TN],
                                               int64_t mw, int64_t nw, int lane, int split,
                                               int64_t offC) {
-  // The accumulators of a 32x32 block hold, per lane, one column and 4 runs
-  // of 4 consecutive rows.  A 4x4 transpose across each group of 4 lanes
-  // (two butterfly exchanges) turns every run into 4 consecutive columns of
-  // one row, so bias / residual / activation inputs are read and outputs
-  // written 4 elements (8 bytes; 16 for float partials) at a time.
   const int q4 = lane & 3;
-  const int row_l = 4 * (lane >> 5) + q4;        // row within an 8-row group
-  const int col_l = 4 * ((lane & 31) >> 2);      // first of the lane's 4 columns
-  // exchange (p, p + st) pairs with the lane st apart (st = 1 or 2) through a
-  // DPP quad permutation (lane ^ 1: quad_perm [1,0,3,2]; lane ^ 2: [2,3,0,1])
-  auto xchg = [&](float& lo, float& hi_v, int st) {
-    const bool hi = (q4 & st) != 0;
-    const int send = __builtin_bit_cast(int, hi ? lo : hi_v);
-    const int got = st == 1 ? __builtin_amdgcn_mov_dpp(send, 0xB1, 0xF, 0xF, false)
-                            : __builtin_amdgcn_mov_dpp(send, 0x4E, 0xF, 0xF, false);
-    if (hi) lo = __builtin_bit_cast(float, got);
-    else hi_v = __builtin_bit_cast(float, got);
-  };
-  auto transpose4 = [&](float (&v)[4]) {
-    xchg(v[0], v[1], 1);
-    xchg(v[2], v[3], 1);
-    xchg(v[0], v[2], 2);
-    xchg(v[1], v[3], 2);
+  // run q of block (i, j): its 4 values, output row and first column
+  auto run = [&](const f32x16& a, int i, int j, int q, float (&v)[4], int64_t& m, int64_t& n) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) v[c] = a[4 * q + c];
+    if constexpr (TRANS) {
+      m = mw + i * 32 + (lane & 31);
+      n = nw + j * 32 + 8 * q + 4 * (lane >> 5);
+    } else {
+      quad_transpose(v, q4);
+      m = mw + i * 32 + 8 * q + 4 * (lane >> 5) + q4;
+      n = nw + j * 32 + 4 * ((lane & 31) >> 2);
+    }
   };
   auto al8 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; };
   if (g.splits > 1) {
@@ -356,13 +350,11 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const f32x16 (&
     const bool v16 = g.N % 4 == 0 && (reinterpret_cast<uintptr_t>(W) & 15u) == 0;
     static_for<TM>([&](auto i) {
       static_for<TN>([&](auto j) {
-        const f32x16 a = acc[i][j];
 #pragma unroll
-        for (int qd = 0; qd < 4; ++qd) {
-          float v[4] = {a[4 * qd], a[4 * qd + 1], a[4 * qd + 2], a[4 * qd + 3]};
-          transpose4(v);
-          const int64_t m = mw + i * 32 + 8 * qd + row_l;
-          const int64_t n = nw + j * 32 + col_l;
+        for (int q = 0; q < 4; ++q) {
+          float v[4];
+          int64_t m, n;
+          run(acc[i][j], i, j, q, v, m, n);
           if (m < g.M && n < g.N) {
             float* out = W + m * g.N + n;
             if (v16 && n + 4 <= g.N) *reinterpret_cast<f32x4*>(out) = f32x4{v[0], v[1], v[2], v[3]};
@@ -402,19 +394,16 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const f32x16 (&
   };
   static_for<TM>([&](auto i) {
     static_for<TN>([&](auto j) {
-      const f32x16 a = acc[i][j];
-      const int64_t n = nw + j * 32 + col_l;
-      const int nv = (int)max<int64_t>(0, min<int64_t>(4, g.N - n));
-      const bool vec = v8 && nv == 4;
-      uint16_t bias[4] = {0, 0, 0, 0};
-      if (g.bias && nv > 0) ld4(g.bias + n, vec, nv, bias);
 #pragma unroll
-      for (int qd = 0; qd < 4; ++qd) {
-        float v[4] = {a[4 * qd], a[4 * qd + 1], a[4 * qd + 2], a[4 * qd + 3]};
-        transpose4(v);
-        const int64_t m = mw + i * 32 + 8 * qd + row_l;
+      for (int q = 0; q < 4; ++q) {
+        float v[4];
+        int64_t m, n;
+        run(acc[i][j], i, j, q, v, m, n);
+        const int nv = (int)max<int64_t>(0, min<int64_t>(4, g.N - n));
         if (m >= g.M || nv == 0) continue;
-        uint16_t h[4], da[4], res[4];
+        const bool vec = v8 && nv == 4;
+        uint16_t bias[4] = {0, 0, 0, 0}, h[4], da[4], res[4];
+        if (g.bias) ld4(g.bias + n, vec, nv, bias);
         if (g.dact) ld4(g.dact + m * g.ldc + n, vec, nv, da);
         if (g.resid) ld4(g.resid + m * g.ldr + n, vec, nv, res);
 #pragma unroll
@@ -465,7 +454,7 @@ void gemm_kernel(GemmArgs g) {
   if (g.splits > 1) {
     split = (int)z;
   } else {
-    const int64_t i0 = z / g.nb1, i1 = z % g.nb1;
+    const int64_t i0 = (uint32_t)z / (uint32_t)g.nb1, i1 = (uint32_t)z % (uint32_t)g.nb1;
     offA = i0 * g.sA0 + i1 * g.sA1;
     offB = i0 * g.sB0 + i1 * g.sB1;
     offC = i0 * g.sC0 + i1 * g.sC1;
@@ -613,11 +602,17 @@ struct DmaOperand {
       }
     }
   }
-  // copy the tile whose first element is at base into LDS at lds
+  // copy the tile whose first element is at base into LDS at lds (both
+  // wave-uniform; made explicitly scalar for the copy instruction)
   __device__ __forceinline__ void issue(const uint16_t* base, uint32_t lds, int wave) const {
+    const uint64_t p = reinterpret_cast<uint64_t>(base);
+    const uint64_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)p);
+    const uint64_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(p >> 32));
+    const void* sbase = reinterpret_cast<const void*>(lo | (hi << 32));
+    const uint32_t slds = (uint32_t)__builtin_amdgcn_readfirstlane((int)lds);
 #pragma unroll
     for (int q = 0; q < Q; ++q)
-      dma16(base, off[q], lds + 1024u * (uint32_t)(wave + NWAVES * q));
+      dma16(sbase, off[q], slds + 1024u * (uint32_t)(wave + NWAVES * q));
   }
 };
 
@@ -684,7 +679,7 @@ void gemm_dma_kernel(GemmArgs g) {
   if (g.splits > 1) {
     split = (int)z;
   } else {
-    const int64_t i0 = z / g.nb1, i1 = z % g.nb1;
+    const int64_t i0 = (uint32_t)z / (uint32_t)g.nb1, i1 = (uint32_t)z % (uint32_t)g.nb1;
     offA = i0 * g.sA0 + i1 * g.sA1;
     offB = i0 * g.sB0 + i1 * g.sB1;
     offC = i0 * g.sC0 + i1 * g.sC1;
@@ -745,18 +740,21 @@ void gemm_dma_kernel(GemmArgs g) {
       }
       __builtin_amdgcn_sched_barrier(0);
       static_for<TM>([&](auto i) {
-        static_for<TN>([&](auto j) { acc[i][j] = mfma32<DT>(af[cur][i], bf[cur][j], acc[i][j]); });
+        static_for<TN>([&](auto j) { acc[i][j] = mfma32<DT>(bf[cur][j], af[cur][i], acc[i][j]); });
       });
       __builtin_amdgcn_sched_barrier(0);
     });
   }
+  // the accumulators hold C^T blocks (the MFMA operands are swapped above)
   if constexpr (E != EPI_GENERIC) {
-    if (g.full_epi && m0 + BM <= g.M && n0 + BN <= g.N) {
-      gemm_epilogue_full<DT, TM, TN, E>(g, acc, m0 + wm0, n0 + wn0, lane, offC);
+    if (g.full_epi && m0 + BM <= g.M && n0 + BN <= g.N) {  // uniform over the workgroup
+      __syncthreads();  // every wave is done reading the stage buffers
+      gemm_epilogue_lds<DT, TM, TN, E>(g, acc, m0 + wm0, n0 + wn0, lane, offC,
+                                       reinterpret_cast<uint16_t*>(smem) + wave * (WM * 68));
       return;
     }
   }
-  gemm_epilogue<DT, TM, TN>(g, acc, m0 + wm0, n0 + wn0, lane, split, offC);
+  gemm_epilogue<DT, TM, TN, true>(g, acc, m0 + wm0, n0 + wn0, lane, split, offC);
 }
 
 // Sum of split-K partials in split order, one rounding: C = half(sum_s W[s]).
@@ -812,15 +810,17 @@ static int epilogue_mask(const GemmArgs& g) {
          (g.dact ? EPI_DACT : 0) | (g.resid ? EPI_RESID : 0);
 }
 
-// Whole-tile epilogue preconditions that do not depend on the tile: every
-// epilogue operand 8-byte aligned with row strides a multiple of 4, and the
-// per-lane 32-bit offsets in range.
+// Whole-tile epilogue preconditions that do not depend on the tile: output,
+// pre-activation, GELU' and residual operands 16-byte aligned with row
+// strides a multiple of 8, the bias 8-byte aligned, and the per-lane 32-bit
+// offsets in range.
 static bool full_epilogue_ok(const GemmArgs& g, int bm) {
   auto al8 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; };
-  const bool strides = g.sC0 % 4 == 0 && g.sC1 % 4 == 0;
-  return g.splits == 1 && strides && g.ldc % 4 == 0 && al8(g.C) && (!g.bias || al8(g.bias)) &&
-         (!g.pre || al8(g.pre)) && (!g.dact || al8(g.dact)) &&
-         (!g.resid || (al8(g.resid) && g.ldr % 4 == 0)) && g.ldc * bm < ((int64_t)1 << 30) &&
+  auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
+  const bool strides = g.sC0 % 8 == 0 && g.sC1 % 8 == 0;
+  return g.splits == 1 && strides && g.ldc % 8 == 0 && al16(g.C) && (!g.bias || al8(g.bias)) &&
+         (!g.pre || al16(g.pre)) && (!g.dact || al16(g.dact)) &&
+         (!g.resid || (al16(g.resid) && g.ldr % 8 == 0)) && g.ldc * bm < ((int64_t)1 << 30) &&
          g.ldr * bm < ((int64_t)1 << 30);
 }
 
