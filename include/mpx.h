@@ -148,13 +148,17 @@ int mpx_linear_fwd(const void* X, const void* W, const void* b, const void* R, v
 
 /* Half-precision linear layer backward (MPX §2.1: gradients of the scaled
  * loss, in half precision).  For Y = X W^T + b and the half cotangent dY:
- *   dX = half(dY W)            [M,K] (skipped when dX is NULL)
- *   dW = half(dY^T X)          [N,K]
+ *   dX = half(dY W)            [M,K] (skipped when dX is NULL; needs W)
+ *   dW = half(dY^T X)          [N,K] (skipped when dW is NULL; needs X)
  *   db = half(sum_m dY[m,:])   [N]   (skipped when db is NULL)
- * If x_act == MPX_ACT_GELU_TANH, X was produced as X = gelu(Xpre) and dX is
- * returned for Xpre instead: dX = half(half(dY W) * gelu'(Xpre)).
- * `workspace` (device, ws_bytes) holds split-K partial sums; its required size
- * is mpx_linear_bwd_workspace(M, N, K). */
+ * At least one of dX, dW, db.  If x_act == MPX_ACT_GELU_TANH, X was produced
+ * as X = gelu(Xpre) and dX is returned for Xpre instead:
+ * dX = half(half(dY W) * gelu'(Xpre)).  Any subset may be requested, so dX
+ * (on the critical path) and dW / db can run on different streams.
+ * `workspace` (device, ws_bytes) holds split-K partial sums and column
+ * partials; its required size is mpx_linear_bwd_workspace(M, N, K) when dW
+ * or db is requested (a dX-only call needs none).  Concurrent calls need
+ * separate workspaces. */
 int mpx_linear_bwd(const void* X, const void* W, const void* dY, const void* Xpre,
                    int32_t x_act, void* dX, void* dW, void* db, int64_t M, int64_t N,
                    int64_t K, mpx_dtype dt, void* workspace, size_t ws_bytes, void* stream);

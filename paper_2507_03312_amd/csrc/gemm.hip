@@ -69,16 +69,20 @@ extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, cons
                               int32_t x_act, void* dX, void* dW, void* db, int64_t M, int64_t N,
                               int64_t K, mpx_dtype dt, void* workspace, size_t ws_bytes, void* stream) {
   clear_error();
-  MPX_REQUIRE(X && dY && dW, "NULL operand");
+  MPX_REQUIRE(dY, "NULL dY");
+  MPX_REQUIRE(dX || dW || db, "nothing to compute: dX, dW and db are all NULL");
   MPX_REQUIRE(!dX || W, "W is required for dX");
+  MPX_REQUIRE(!dW || X, "X is required for dW");
   MPX_REQUIRE(M >= 1 && N >= 1 && K >= 1, "M, N, K must be >= 1");
   MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
   MPX_REQUIRE(x_act == MPX_ACT_NONE || x_act == MPX_ACT_GELU_TANH, "unknown activation");
   MPX_REQUIRE(x_act == MPX_ACT_NONE || !dX || Xpre, "Xpre is required with x_act");
-  const size_t need = mpx_linear_bwd_workspace(M, N, K);
-  if (ws_bytes < need || !workspace) {
-    set_error("mpx_linear_bwd: workspace of " + std::to_string(need) + " bytes required");
-    return MPX_ERR_WORKSPACE;
+  if (dW || db) {  // only the weight and bias gradients use the workspace
+    const size_t need = mpx_linear_bwd_workspace(M, N, K);
+    if (ws_bytes < need || !workspace) {
+      set_error("mpx_linear_bwd: workspace of " + std::to_string(need) + " bytes required");
+      return MPX_ERR_WORKSPACE;
+    }
   }
   hipStream_t s = (hipStream_t)stream;
   // dX[M,K] = dY[M,N] W[N,K]: A = dY (k-major over N), B(n=k', k=n) = W[n*K + k'] (mn-major)
@@ -93,7 +97,7 @@ extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, cons
     MPX_HIP(gemm_dispatch(dt, g, true, false, 1, s));
   }
   // dW[N,K] = dY^T X: A(m=n, k=m_tok) = dY[m_tok*N + n] (mn-major), B(n=k', k=m_tok) = X[m_tok*K + k']
-  {
+  if (dW) {
     GemmArgs g = base_args();
     g.A = (const uint16_t*)dY;
     g.B = (const uint16_t*)X;

@@ -323,22 +323,28 @@ class ViTStep(TrainStep):
         self.logits = z(B, Cn)
         self.dlogits = z(B, Cn)
         self.dz = z(B, d)
-        self.dxa = z(M, d)
-        self.dxb = z(M, d)
-        self.du_pre = z(M, F)
+        # cotangents read by the weight-gradient stream are double (triple for
+        # the residual stream) buffered, so the critical path of block k-1
+        # never overwrites what the side stream still reads for block k
+        self.dx = [z(M, d) for _ in range(3)]
+        self.du_pre = [z(M, F) for _ in range(2)]
+        self.dx1 = [z(M, d) for _ in range(2)]
+        self.dqkv = [z(M, 3 * d) for _ in range(2)]
         self.dc = z(M, d)
-        self.dx1 = z(M, d)
         self.dO = z(M, d)
-        self.dqkv = z(M, 3 * d)
         self.da = z(M, d)
         self.labels = torch.zeros(B, dtype=torch.int32, device=dev)
         shapes = [(M, 3 * d, d), (M, d, d), (M, F, d), (M, d, F), (B, Cn, d)]
         if cfg.image:
             shapes.append((B * cfg.n_patches, d, cfg.patch_dim))
-        ws = max(mx.mpx_linear_bwd_workspace(*s) for s in shapes)
-        ws = max(ws, mx.mpx_layernorm_bwd_workspace(M, d), mx.mpx_loss_workspace(B),
+        # workspaces: the main stream's (LayerNorm, loss, attention) and the
+        # weight-gradient stream's (split-K partials, bias column sums)
+        ws = max(mx.mpx_layernorm_bwd_workspace(M, d), mx.mpx_loss_workspace(B),
                  mx.mpx_attention_bwd_workspace(B, T, H, cfg.head_dim))
         self.ws = torch.zeros(ws, dtype=torch.uint8, device=dev)
+        ws2 = max(mx.mpx_linear_bwd_workspace(*s) for s in shapes)
+        self.ws2 = torch.zeros(ws2, dtype=torch.uint8, device=dev)
+        self.side = torch.cuda.Stream(device=dev)  # default priority
 
     def _dominant_call(self, s):
         c, a, blk = self.cfg, self.arena, self.blocks[0]
@@ -393,10 +399,10 @@ class ViTStep(TrainStep):
                             _off(qkv, 2 * d), 3 * d, T * 3 * d, hd,
                             _ptr(O), d, T * d, hd, dt, s)
 
-    def _attn_bwd(self, blk, s):
+    def _attn_bwd(self, blk, dqkv, s):
         c, dt = self.cfg, self.dt
         B, T, d, H, hd, ldT = c.batch, c.tokens, c.d_model, c.heads, c.head_dim, self.ldT
-        qkv, P, dO, dqkv = blk["qkv"], blk["P"], self.dO, self.dqkv
+        qkv, P, dO = blk["qkv"], blk["P"], self.dO
         if self._fused_attention():
             mx.mpx_attention_bwd(_ptr(qkv), _ptr(P), _ptr(dO), _ptr(dqkv), B, T, H, hd, dt,
                                  _ptr(self.ws), self.ws.numel(), s)
@@ -463,44 +469,63 @@ class ViTStep(TrainStep):
         mx.mpx_cross_entropy(_ptr(self.logits), Cn, _ptr(self.labels), B, Cn, _ptr(self.d_state),
                              _ptr(self.d_loss), _ptr(self.dlogits), dt, wsp, wsb, s)
         # ---- backward ----
-        mx.mpx_linear_bwd(_ptr(self.zf), _ptr(W("head.w")), _ptr(self.dlogits), None, NONE,
-                          _ptr(self.dz), _ptr(G("head.w")), _ptr(G("head.b")), B, Cn, d, dt,
-                          wsp, wsb, s)
-        dx = self.dxa
+        # The critical path (dX of every layer, LayerNorm and attention
+        # backward) runs on the step's stream; the weight and bias gradients
+        # of each linear layer, which nothing later in the backward reads, run
+        # on a second stream forked at the point their cotangent is ready.
+        main = torch.cuda.current_stream()
+        side, sh = self.side, self.side.cuda_stream
+        ws2p, ws2b = _ptr(self.ws2), self.ws2.numel()
+
+        def wgrad(X, dY, dW, db, Mr, N, K):
+            side.wait_stream(main)
+            mx.mpx_linear_bwd(_ptr(X), None, _ptr(dY), None, NONE, None, _ptr(dW), _ptr(db),
+                              Mr, N, K, dt, ws2p, ws2b, sh)
+
+        def dgrad(W_, dY, Xpre, act, dX, Mr, N, K):
+            mx.mpx_linear_bwd(None, _ptr(W_), _ptr(dY), None if Xpre is None else _ptr(Xpre), act,
+                              _ptr(dX), None, None, Mr, N, K, dt, None, 0, s)
+
+        wgrad(self.zf, self.dlogits, G("head.w"), G("head.b"), B, Cn, d)
+        dgrad(W("head.w"), self.dlogits, None, NONE, self.dz, B, Cn, d)
+        dx = self.dx[0]
         mx.mpx_zero(_ptr(dx), dx.numel() * 2, s)
         mx.mpx_layernorm_bwd(_ptr(x), T * d, _ptr(W("lnf.g")), _ptr(self.dz), None, _ptr(dx),
                              T * d, _ptr(G("lnf.g")), _ptr(G("lnf.b")), B, d, dt, wsp, wsb, s)
-        for i in reversed(range(c.depth)):
+        done = []  # side-stream completion of each block's weight gradients
+        for k, i in enumerate(reversed(range(c.depth))):
             blk = self.blocks[i]
             p = f"blk{i}."
             xin = self.x0 if i == 0 else self.blocks[i - 1]["x2"]
-            dx_out = self.dxb if dx is self.dxa else self.dxa
-            mx.mpx_linear_bwd(_ptr(blk["u"]), _ptr(W(p + "down.w")), _ptr(dx), _ptr(blk["u_pre"]),
-                              GELU, _ptr(self.du_pre), _ptr(G(p + "down.w")), _ptr(G(p + "down.b")),
-                              M, d, F, dt, wsp, wsb, s)
-            mx.mpx_linear_bwd(_ptr(blk["c"]), _ptr(W(p + "up.w")), _ptr(self.du_pre), None, NONE,
-                              _ptr(self.dc), _ptr(G(p + "up.w")), _ptr(G(p + "up.b")),
-                              M, F, d, dt, wsp, wsb, s)
+            if k >= 2:  # block k-2's side work read the buffers block k is about to reuse
+                main.wait_event(done[k - 2])
+            dx, dx_out = self.dx[k % 3], self.dx[(k + 1) % 3]
+            du_pre, dx1, dqkv = self.du_pre[k % 2], self.dx1[k % 2], self.dqkv[k % 2]
+            wgrad(blk["u"], dx, G(p + "down.w"), G(p + "down.b"), M, d, F)
+            dgrad(W(p + "down.w"), dx, blk["u_pre"], GELU, du_pre, M, d, F)
+            wgrad(blk["c"], du_pre, G(p + "up.w"), G(p + "up.b"), M, F, d)
+            dgrad(W(p + "up.w"), du_pre, None, NONE, self.dc, M, F, d)
             mx.mpx_layernorm_bwd(_ptr(blk["x1"]), d, _ptr(W(p + "ln2.g")), _ptr(self.dc), _ptr(dx),
-                                 _ptr(self.dx1), d, _ptr(G(p + "ln2.g")), _ptr(G(p + "ln2.b")),
+                                 _ptr(dx1), d, _ptr(G(p + "ln2.g")), _ptr(G(p + "ln2.b")),
                                  M, d, dt, wsp, wsb, s)
-            mx.mpx_linear_bwd(_ptr(blk["O"]), _ptr(W(p + "proj.w")), _ptr(self.dx1), None, NONE,
-                              _ptr(self.dO), _ptr(G(p + "proj.w")), _ptr(G(p + "proj.b")),
-                              M, d, d, dt, wsp, wsb, s)
-            self._attn_bwd(blk, s)
-            mx.mpx_linear_bwd(_ptr(blk["a"]), _ptr(W(p + "qkv.w")), _ptr(self.dqkv), None, NONE,
-                              _ptr(self.da), _ptr(G(p + "qkv.w")), _ptr(G(p + "qkv.b")),
-                              M, 3 * d, d, dt, wsp, wsb, s)
-            mx.mpx_layernorm_bwd(_ptr(xin), d, _ptr(W(p + "ln1.g")), _ptr(self.da), _ptr(self.dx1),
+            wgrad(blk["O"], dx1, G(p + "proj.w"), G(p + "proj.b"), M, d, d)
+            dgrad(W(p + "proj.w"), dx1, None, NONE, self.dO, M, d, d)
+            self._attn_bwd(blk, dqkv, s)
+            wgrad(blk["a"], dqkv, G(p + "qkv.w"), G(p + "qkv.b"), M, 3 * d, d)
+            dgrad(W(p + "qkv.w"), dqkv, None, NONE, self.da, M, 3 * d, d)
+            mx.mpx_layernorm_bwd(_ptr(xin), d, _ptr(W(p + "ln1.g")), _ptr(self.da), _ptr(dx1),
                                  _ptr(dx_out), d, _ptr(G(p + "ln1.g")), _ptr(G(p + "ln1.b")),
                                  M, d, dt, wsp, wsb, s)
+            ev = torch.cuda.Event()
+            ev.record(side)
+            done.append(ev)
             dx = dx_out
         if c.image:
             mx.mpx_embed_assemble_bwd(_ptr(dx), _ptr(self.dE), _ptr(G("cls")), _ptr(G("pos")),
                                       B, T, d, dt, s)
-            mx.mpx_linear_bwd(_ptr(self.patches), _ptr(W("patch.w")), _ptr(self.dE), None, NONE,
-                              None, _ptr(G("patch.w")), _ptr(G("patch.b")), B * c.n_patches, d,
-                              c.patch_dim, dt, wsp, wsb, s)
+            wgrad(self.patches, self.dE, G("patch.w"), G("patch.b"), B * c.n_patches, d,
+                  c.patch_dim)
+        main.wait_stream(side)  # join: the optimizer reads every gradient
 
 
 def make_step(cfg, device="cuda") -> TrainStep:

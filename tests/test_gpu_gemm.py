@@ -317,3 +317,33 @@ def test_skinny_path_forced(fmt):
             assert_within(to_host(gdw), rdw, gemm_bound(dy.T, x, rdw, fmt, M), f"dW {M}x{N}x{K}")
     finally:
         mx.mpx_gemm_set_config(0)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_linear_bwd_subsets_match_full_call(fmt):
+    """dX alone (no workspace) and dW + db alone, as the two-stream backward
+    issues them, give the bits of the full call; an empty request is rejected."""
+    M, N, K = 2112, 448, 320
+    dt = mx.DTYPES[fmt]
+    x, w = _rand((M, K), fmt, 61), _rand((N, K), fmt, 62, 0.05)
+    dy, xp = _rand((M, N), fmt, 63), _rand((M, K), fmt, 64)
+    tx, tw, tdy, txp = (to_dev_half(a, fmt) for a in (x, w, dy, xp))
+    full = [_empty((M, K), fmt), _empty((N, K), fmt), _empty((N,), fmt)]
+    part = [_empty((M, K), fmt), _empty((N, K), fmt), _empty((N,), fmt)]
+    ws_n = mx.mpx_linear_bwd_workspace(M, N, K)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), txp.data_ptr(),
+                      mx.MPX_ACT_GELU_TANH, *(t.data_ptr() for t in full), M, N, K, dt,
+                      ws.data_ptr(), ws_n, _s())
+    mx.mpx_linear_bwd(None, tw.data_ptr(), tdy.data_ptr(), txp.data_ptr(), mx.MPX_ACT_GELU_TANH,
+                      part[0].data_ptr(), None, None, M, N, K, dt, None, 0, _s())
+    mx.mpx_linear_bwd(tx.data_ptr(), None, tdy.data_ptr(), None, mx.MPX_ACT_NONE, None,
+                      part[1].data_ptr(), part[2].data_ptr(), M, N, K, dt, ws.data_ptr(), ws_n, _s())
+    for f, q, what in zip(full, part, ("dX", "dW", "db")):
+        assert torch.equal(f, q), what
+    with pytest.raises(mx.MPXError, match="nothing to compute"):
+        mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), None, 0, None, None, None,
+                          M, N, K, dt, ws.data_ptr(), ws_n, _s())
+    with pytest.raises(mx.MPXError, match="workspace"):
+        mx.mpx_linear_bwd(tx.data_ptr(), None, tdy.data_ptr(), None, 0, None, part[1].data_ptr(),
+                          None, M, N, K, dt, None, 0, _s())
