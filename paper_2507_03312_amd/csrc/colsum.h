@@ -65,23 +65,30 @@ template <int DT>
 __global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restrict__ part, int nparts,
                                                            int64_t cols, uint16_t* __restrict__ out0,
                                                            uint16_t* __restrict__ out1, int64_t split) {
-  __shared__ float red[4][64];
-  const int c = threadIdx.x & 63, q = threadIdx.x >> 6;
-  const int64_t col = (int64_t)blockIdx.x * 64 + c;
+  // 32 columns per workgroup, 8 lanes per column: lane group q sums partials
+  // q, q + 8, ... in order, then the 8 group sums are added pairwise in a
+  // fixed tree
+  __shared__ float red[8][32];
+  const int c = threadIdx.x & 31, q = threadIdx.x >> 5;
+  const int64_t col = (int64_t)blockIdx.x * 32 + c;
   float s = 0.0f;
   if (col < cols) {
 #pragma unroll 8
-    for (int p = q; p < nparts; p += 4) s += part[(int64_t)p * cols + col];
+    for (int p = q; p < nparts; p += 8) s += part[(int64_t)p * cols + col];
   }
   red[q][c] = s;
   __syncthreads();
   if (q == 0 && col < cols) {
-    const float t = ((red[0][c] + red[1][c]) + red[2][c]) + red[3][c];
+    const float t = ((red[0][c] + red[1][c]) + (red[2][c] + red[3][c])) +
+                    ((red[4][c] + red[5][c]) + (red[6][c] + red[7][c]));
     // columns [0, split) go to out0, [split, cols) to out1 (two results of one pass)
     if (col < split) out0[col] = f2h<DT>(t);
     else out1[col - split] = f2h<DT>(t);
   }
 }
+
+// launch shape of colsum_final_kernel for `cols` columns
+inline unsigned colsum_final_blocks(int64_t cols) { return (unsigned)((cols + 31) / 32); }
 
 inline int64_t colsum_slices(int64_t rows, int64_t cols) {
   const int64_t gx = (cols + 255) / 256;
@@ -105,7 +112,7 @@ inline hipError_t colsum_run(const uint16_t* X, int64_t rows, int64_t cols, floa
     colsum_partial_kernel<DT, true><<<g1, 256, 0, s>>>(X, rows, cols, per, ws);
   else
     colsum_partial_kernel<DT, false><<<g1, 256, 0, s>>>(X, rows, cols, per, ws);
-  colsum_final_kernel<DT><<<(unsigned)((cols + 63) / 64), 256, 0, s>>>(ws, (int)sl, cols, out, nullptr,
+  colsum_final_kernel<DT><<<colsum_final_blocks(cols), 256, 0, s>>>(ws, (int)sl, cols, out, nullptr,
                                                                        cols);
   return hipGetLastError();
 }

@@ -90,20 +90,41 @@ __device__ __forceinline__ float gelu_tanh_grad(float x) {
 
 // ------------------------------------------------------------ reductions --
 
+// Wave-wide reductions in a fixed order, on DPP lane permutations (no LDS
+// round trips): pairs (lane ^ 1), then lane ^ 2 (quad permutes), then the
+// mirror within 8 lanes and within 16 lanes give every lane its 16-lane row
+// total; the four row totals are then read out of lanes 0, 16, 32, 48 and
+// combined as (r0 + r1) + (r2 + r3).  The result is the same on every lane.
+template <typename T, typename Op>
+__device__ __forceinline__ T wave_reduce(T v, Op op) {
+  auto dpp = [](T x, int ctrl) {
+    const int b = __builtin_bit_cast(int, x);
+    int r;
+    switch (ctrl) {  // the control word must be a constant
+      case 0xB1: r = __builtin_amdgcn_mov_dpp(b, 0xB1, 0xF, 0xF, false); break;   // quad_perm [1,0,3,2]
+      case 0x4E: r = __builtin_amdgcn_mov_dpp(b, 0x4E, 0xF, 0xF, false); break;   // quad_perm [2,3,0,1]
+      case 0x141: r = __builtin_amdgcn_mov_dpp(b, 0x141, 0xF, 0xF, false); break; // row_half_mirror
+      default: r = __builtin_amdgcn_mov_dpp(b, 0x140, 0xF, 0xF, false); break;   // row_mirror
+    }
+    return __builtin_bit_cast(T, r);
+  };
+  v = op(v, dpp(v, 0xB1));
+  v = op(v, dpp(v, 0x4E));
+  v = op(v, dpp(v, 0x141));
+  v = op(v, dpp(v, 0x140));
+  auto lane_val = [&](int l) {
+    return __builtin_bit_cast(T, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), l));
+  };
+  return op(op(lane_val(0), lane_val(16)), op(lane_val(32), lane_val(48)));
+}
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  return wave_reduce(v, [](float a, float b) { return a + b; });
 }
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
+  return wave_reduce(v, [](float a, float b) { return fmaxf(a, b); });
 }
 __device__ __forceinline__ int wave_sum_int(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  return wave_reduce(v, [](int a, int b) { return a + b; });
 }
 
 inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }

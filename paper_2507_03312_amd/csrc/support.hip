@@ -130,9 +130,15 @@ __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const uint16_t* __re
 
 // dX for each row (optionally plus a residual cotangent), and per-workgroup
 // column partials of dgamma (sum dy*xhat) and dbeta (sum dy) into
-// part[blockIdx][0:d] and part[blockIdx][d:2d].
+// part[blockIdx][0:d] and part[blockIdx][d:2d].  4 waves of kLnBwdRows rows
+// each: every load of a wave's rows is issued before any reduction, and one
+// workgroup covers 8 * kLnBwdRows rows, so a single pass over the rows keeps
+// the number of partial rows (and the final column reduction) small.
+constexpr int kLnBwdRows = 4;
+constexpr int kLnBwdWaves = 4;
+
 template <int DT, int VPL>
-__global__ __launch_bounds__(256) void layernorm_bwd_kernel(
+__global__ __launch_bounds__(64 * kLnBwdWaves) void layernorm_bwd_kernel(
     const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __restrict__ gamma,
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ Rg, uint16_t* __restrict__ dX,
     int64_t ldo, int64_t rows, int64_t d, float* __restrict__ part) {
@@ -146,17 +152,18 @@ __global__ __launch_bounds__(256) void layernorm_bwd_kernel(
 #pragma unroll
     for (int j = 0; j < 8; ++j) pg[v][j] = pb[v][j] = 0.0f;
 
-  for (int64_t r = ((int64_t)blockIdx.x * 4 + wave) * kLnRows; r < rows;
-       r += (int64_t)gridDim.x * 4 * kLnRows) {
-    RowVec<VPL> x[kLnRows], dy[kLnRows];
+  for (int64_t r = ((int64_t)blockIdx.x * kLnBwdWaves + wave) * kLnBwdRows; r < rows;
+       r += (int64_t)gridDim.x * kLnBwdWaves * kLnBwdRows) {
+    RowVec<VPL> x[kLnBwdRows], dy[kLnBwdRows], rg[kLnBwdRows];
 #pragma unroll
-    for (int i = 0; i < kLnRows; ++i)
+    for (int i = 0; i < kLnBwdRows; ++i)
       if (r + i < rows) {
         load_row<DT, VPL>(X + (r + i) * ldx, d, lane, x[i]);
         load_row<DT, VPL>(dY + (r + i) * d, d, lane, dy[i]);
+        if (Rg) load_row<DT, VPL>(Rg + (r + i) * ldo, d, lane, rg[i]);
       }
 #pragma unroll
-    for (int i = 0; i < kLnRows; ++i) {
+    for (int i = 0; i < kLnBwdRows; ++i) {
       if (r + i >= rows) break;
       float mean, rstd;
       row_stats<VPL>(x[i], d, lane, mean, rstd);
@@ -175,8 +182,6 @@ __global__ __launch_bounds__(256) void layernorm_bwd_kernel(
         }
       s1 = wave_sum(s1) / (float)d;
       s2 = wave_sum(s2) / (float)d;
-      RowVec<VPL> rg;
-      if (Rg) load_row<DT, VPL>(Rg + (r + i) * ldo, d, lane, rg);
       uint16_t h[VPL][8];
 #pragma unroll
       for (int v = 0; v < VPL; ++v)
@@ -184,14 +189,14 @@ __global__ __launch_bounds__(256) void layernorm_bwd_kernel(
         for (int j = 0; j < 8; ++j) {
           const float dx = rstd * (dy[i].x[v][j] * g.x[v][j] - s1 - x[i].x[v][j] * s2);
           uint16_t o = f2h<DT>(dx);
-          if (Rg) o = f2h<DT>(rg.x[v][j] + h2f<DT>(o));
+          if (Rg) o = f2h<DT>(rg[i].x[v][j] + h2f<DT>(o));
           h[v][j] = o;
         }
       store_row<DT, VPL>(dX + (r + i) * ldo, d, lane, h);
     }
   }
-  // the 4 waves' column partials, combined in wave order through LDS
-  __shared__ float red[4][2][512];
+  // the waves' column partials, combined in wave order through LDS
+  __shared__ float red[kLnBwdWaves][2][512];
   float* out = part + (int64_t)blockIdx.x * 2 * d;
 #pragma unroll
   for (int v = 0; v < VPL; ++v) {
@@ -202,18 +207,21 @@ __global__ __launch_bounds__(256) void layernorm_bwd_kernel(
       red[wave][1][lane * 8 + j] = pb[v][j];
     }
     __syncthreads();
-    for (int i = threadIdx.x; i < 1024; i += 256) {
+    for (int i = threadIdx.x; i < 1024; i += 64 * kLnBwdWaves) {
       const int which = i >> 9, c = i & 511;
       const int64_t col = (int64_t)v * 512 + c;
-      if (col < d)
-        out[which * d + col] =
-            ((red[0][which][c] + red[1][which][c]) + red[2][which][c]) + red[3][which][c];
+      if (col < d) {
+        float t = red[0][which][c];
+#pragma unroll
+        for (int w = 1; w < kLnBwdWaves; ++w) t += red[w][which][c];
+        out[which * d + col] = t;
+      }
     }
   }
 }
 
 static int ln_bwd_blocks(int64_t rows) {
-  return (int)std::max<int64_t>(1, std::min<int64_t>((rows + 4 * kLnRows - 1) / (4 * kLnRows), 480));
+  return (int)std::max<int64_t>(1, (rows + kLnBwdWaves * kLnBwdRows - 1) / (kLnBwdWaves * kLnBwdRows));
 }
 
 // --------------------------------------------------------------- softmax --
@@ -480,9 +488,10 @@ template <int DT>
 static void ln_bwd_launch(int vpl, unsigned grid, hipStream_t s, const uint16_t* X, int64_t ldx,
                           const uint16_t* g, const uint16_t* dY, const uint16_t* Rg, uint16_t* dX,
                           int64_t ldo, int64_t rows, int64_t d, float* part) {
-  if (vpl == 1) layernorm_bwd_kernel<DT, 1><<<grid, 256, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part);
-  else if (vpl == 2) layernorm_bwd_kernel<DT, 2><<<grid, 256, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part);
-  else layernorm_bwd_kernel<DT, 4><<<grid, 256, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part);
+  constexpr int NT = 64 * kLnBwdWaves;
+  if (vpl == 1) layernorm_bwd_kernel<DT, 1><<<grid, NT, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part);
+  else if (vpl == 2) layernorm_bwd_kernel<DT, 2><<<grid, NT, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part);
+  else layernorm_bwd_kernel<DT, 4><<<grid, NT, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part);
 }
 
 extern "C" int mpx_layernorm_fwd(const void* X, int64_t ldx, const void* gamma, const void* beta,
@@ -525,7 +534,7 @@ extern "C" int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, 
   const int nb = ln_bwd_blocks(rows);
   hipStream_t s = (hipStream_t)stream;
   float* part = (float*)workspace;
-  const unsigned fin = (unsigned)((2 * d + 63) / 64);
+  const unsigned fin = colsum_final_blocks(2 * d);
   if (dt == MPX_F16) {
     ln_bwd_launch<MPX_F16>(vpl_for(d), (unsigned)nb, s, (const uint16_t*)X, ldx, (const uint16_t*)gamma,
                            (const uint16_t*)dY, (const uint16_t*)Rgrad, (uint16_t*)dX, ldo, rows, d, part);
