@@ -43,20 +43,20 @@ DEFAULT_CONFIG = "vit_block"
 # they no longer match, the figure is stale and reported as null.
 TRAFFIC = {
     "blk0.up.fwd": {
-        "fetch_kib": 13994.8, "write_kib": 49920.0,
-        "fetch_factor": 262144.0 / 131088.6, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 13959.5, "write_kib": 49920.0,
+        "fetch_factor": 262144.0 / 131088.3, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/gemm_kernels.h": "290d2bf38b0ff78b4fb37c8da4991480ae63762574f71d06f1350ac8ce932e43",
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "2b599c8e25c529458bb5e7f6794fbea3c5f0f23a18bc325715c3ee544e783906",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
-            "paper_2507_03312_amd/csrc/common.h": "83e7f522d517c4c7c1f7c1fc0aa065821a162c75b2b9b3b48e68173ad8300ccb",
+            "paper_2507_03312_amd/csrc/common.h": "730b9a02e1fa63f557d2c496e7263b42acecd1543d8f7cb787b1a2929e4bbeee",
         },
     },
     "sweep": {
-        "fetch_kib": 685321.4, "write_kib": 1367231.7,
-        "fetch_factor": 262144.0 / 131086.6, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 685321.4, "write_kib": 1367242.2,
+        "fetch_factor": 262144.0 / 131086.2, "write_factor": 262144.0 / 262144.0,
         "sources": {
             "paper_2507_03312_amd/csrc/sweep.hip": "834620fdf6a477404ce1056458cbd2dc253f85bcb8cd2999e23dd108cedfecfb",
-            "paper_2507_03312_amd/csrc/common.h": "83e7f522d517c4c7c1f7c1fc0aa065821a162c75b2b9b3b48e68173ad8300ccb",
+            "paper_2507_03312_amd/csrc/common.h": "730b9a02e1fa63f557d2c496e7263b42acecd1543d8f7cb787b1a2929e4bbeee",
         },
     },
 }
