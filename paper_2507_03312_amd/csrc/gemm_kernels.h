@@ -235,9 +235,9 @@ __device__ __forceinline__ void tile_origin(int64_t M, int64_t N, int64_t& m0, i
 enum : int { EPI_BIAS = 1, EPI_GELU = 2, EPI_DACT = 4, EPI_RESID = 8, EPI_GENERIC = -1 };
 
 // Whole-tile epilogue through LDS, for the transposed accumulator layout and
-// 64 x 64 wave tiles.  Step 1 (accumulator layout: lane = one row, runs of 4
+// 32 x 64 or 64 x 64 wave tiles.  Step 1 (accumulator layout: lane = one row, runs of 4
 // consecutive columns): h = half(acc + bias), written to the wave's own
-// [64][68] half region of the LDS the main loop no longer needs.  Step 2 (row
+// [rows][68] half region of the LDS the main loop no longer needs.  Step 2 (row
 // layout: lane = 8 consecutive columns of one row): the pre-activation store,
 // GELU, GELU' of the previous layer and the residual add with 16-byte
 // accesses, each store writing 8 rows x 128 contiguous bytes.
@@ -245,7 +245,7 @@ template <int DT, int TM, int TN, int E>
 __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, const f32x16 (&acc)[TM][TN],
                                                   int64_t mw, int64_t nw, int lane, int64_t offC,
                                                   uint16_t* lds) {
-  static_assert(TM == 2 && TN == 2, "64 x 64 wave tiles");
+  static_assert((TM == 1 || TM == 2) && TN == 2, "32 x 64 or 64 x 64 wave tiles");
   constexpr int PITCH = 68;  // halves (34 banks): a column of 32 rows spreads over all banks
   const int hi = lane >> 5, r32 = lane & 31;
   auto unpack = [](u32x2 w, float (&f)[4]) {
@@ -288,7 +288,7 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, const f32x1
                  h[4] | ((uint32_t)h[5] << 16), h[6] | ((uint32_t)h[7] << 16)};
   };
 #pragma unroll
-  for (int t = 0; t < 8; ++t) {
+  for (int t = 0; t < 4 * TM; ++t) {
     const int row = (lane >> 3) + 8 * t;
     const u32x2 w0 = *reinterpret_cast<const u32x2*>(lds + row * PITCH + c8);
     const u32x2 w1 = *reinterpret_cast<const u32x2*>(lds + row * PITCH + c8 + 4);
@@ -832,7 +832,26 @@ static hipError_t launch_dma(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipSt
   g.full_epi = full_epilogue_ok(g, BM) ? 1 : 0;
   const int e = g.full_epi ? epilogue_mask(g) : EPI_GENERIC;
 #define MPX_D(AKv, BKv, Ev) gemm_dma_kernel<DT, BM, BN, WM, WN, S, OCC, AKv, BKv, Ev><<<grid, NT, 0, s>>>(g)
-  if constexpr (BM == 128 && BN == 128 && S == 2) {
+  if constexpr (BM == 64) {
+    // 64 x 128 tiles (outputs too small to fill the CUs with 128 x 128): the
+    // A operand must be k-major (dma_ok rejects the rest)
+    if (!ak) return hipErrorInvalidValue;
+    if (bk) {
+      switch (e) {
+        case 0: MPX_D(true, true, 0); break;
+        case EPI_BIAS: MPX_D(true, true, EPI_BIAS); break;
+        case EPI_BIAS | EPI_GELU: MPX_D(true, true, EPI_BIAS | EPI_GELU); break;
+        case EPI_BIAS | EPI_RESID: MPX_D(true, true, EPI_BIAS | EPI_RESID); break;
+        default: MPX_D(true, true, EPI_GENERIC);
+      }
+    } else {
+      switch (e) {
+        case 0: MPX_D(true, false, 0); break;
+        case EPI_DACT: MPX_D(true, false, EPI_DACT); break;
+        default: MPX_D(true, false, EPI_GENERIC);
+      }
+    }
+  } else if constexpr (BM == 128 && BN == 128 && S == 2) {
     // the configuration the dispatcher picks: whole tiles get the
     // specialised epilogue of each call pattern of the training step
     if (ak && bk) {
@@ -875,6 +894,8 @@ static hipError_t launch_dma(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipSt
 //   6  direct-to-LDS 128 x 128, 4 waves, 4 stages
 //   7  direct-to-LDS 128 x 128, 4 waves, 2 stages, two workgroups per CU
 //   8  skinny products: one wave (K > 32) or one lane (K <= 32) per output
+//   9  direct-to-LDS 64 x 128, 4 waves of 32 x 64, 2 stages, three workgroups
+//      per CU (A k-major only)
 extern int g_forced_config;  // defined in gemm.hip
 
 // The direct-to-LDS kernel needs 16-byte aligned operands and whole k tiles
@@ -899,11 +920,19 @@ static int choose_config(const GemmArgs& g, bool vec, bool ak, bool bk, int64_t 
   const bool small = small_ok(g, nbatch);
   const int f = g_forced_config;
   if (f == 8 && small) return 8;
+  if (f == 9 && dma && ak) return 9;
   if (f >= 3 && f <= 7 && dma) return f;
   if (f == 1 || (f == 2 && vec)) return f;
   if (small && (g.M <= 32 || g.N <= 32 || g.K <= 32)) return 8;
   if (g.M <= 64 || g.N <= 64) return 1;
-  if (dma) return 7;
+  if (dma) {
+    // fewer 128 x 128 tiles than CUs: halve the tile height (measured on the
+    // M = 8320, N = 384 layer products: 195 tiles -> 390)
+    const int64_t tiles = ((g.M + 127) / 128) * ((g.N + 127) / 128) *
+                          (g.splits > 1 ? g.splits : nbatch);
+    if (ak && tiles < 256) return 9;
+    return 7;
+  }
   return vec ? 2 : 0;
 }
 
@@ -972,6 +1001,7 @@ static hipError_t run_gemm(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipStre
     case 5: return launch_dma<DT, 128, 256, 64, 128, 3, 1>(g, ak, bk, nbatch, s);
     case 6: return launch_dma<DT, 128, 128, 64, 64, 4, 1>(g, ak, bk, nbatch, s);
     case 7: return launch_dma<DT, 128, 128, 64, 64, 2, 2>(g, ak, bk, nbatch, s);
+    case 9: return launch_dma<DT, 64, 128, 32, 64, 2, 3>(g, ak, bk, nbatch, s);
     default:  // unaligned operands (rare: odd leading dimensions)
       return launch_cfg<DT, 128, 128, 64, 64>(g, ak, bk, vec, nbatch, s);
   }

@@ -219,7 +219,7 @@ def test_full_size_linear_sampled(fmt, mnk):
     assert_within(to_host(gdw)[np.ix_(cols, kc)], ref, gemm_bound(dy[:, cols].T, x[:, kc], ref, fmt, M), "dW")
 
 
-CONFIGS = [1, 2, 3, 4, 5, 6, 7]
+CONFIGS = [1, 2, 3, 4, 5, 6, 7, 9]
 
 
 @pytest.fixture
