@@ -231,8 +231,10 @@ int mpx_layernorm_fwd(const void* X, int64_t ldx, const void* gamma, const void*
  * half(dLN)) (the residual branch's cotangent added after the LN cotangent is
  * rounded).  X has row stride ldx; dX, dY, Rgrad are dense [rows, d] unless
  * ldo (row stride of dX and Rgrad) says otherwise.  dgamma, dbeta [d] half =
- * half(column sums); partial sums use `workspace` (float32,
- * mpx_layernorm_bwd_workspace bytes). */
+ * half(column sums); their partial sums use `workspace` (float32,
+ * mpx_layernorm_bwd_workspace bytes).  dX (NULL: skipped) and the pair
+ * dgamma / dbeta (both NULL: skipped, no workspace needed) may be requested
+ * in separate calls, e.g. on two streams; at least one must be given. */
 int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, const void* dY,
                       const void* Rgrad, void* dX, int64_t ldo, void* dgamma, void* dbeta,
                       int64_t rows, int64_t d, mpx_dtype dt, void* workspace,

@@ -137,7 +137,8 @@ __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const uint16_t* __re
 constexpr int kLnBwdRows = 4;
 constexpr int kLnBwdWaves = 4;
 
-template <int DT, int VPL>
+// DX: compute dX; PART: write the gamma / beta column partials (either or both).
+template <int DT, int VPL, bool DX, bool PART>
 __global__ __launch_bounds__(64 * kLnBwdWaves) void layernorm_bwd_kernel(
     const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __restrict__ gamma,
     const uint16_t* __restrict__ dY, const uint16_t* __restrict__ Rg, uint16_t* __restrict__ dX,
@@ -160,7 +161,7 @@ __global__ __launch_bounds__(64 * kLnBwdWaves) void layernorm_bwd_kernel(
       if (r + i < rows) {
         load_row<DT, VPL>(X + (r + i) * ldx, d, lane, x[i]);
         load_row<DT, VPL>(dY + (r + i) * d, d, lane, dy[i]);
-        if (Rg) load_row<DT, VPL>(Rg + (r + i) * ldo, d, lane, rg[i]);
+        if (DX && Rg) load_row<DT, VPL>(Rg + (r + i) * ldo, d, lane, rg[i]);
       }
 #pragma unroll
     for (int i = 0; i < kLnBwdRows; ++i) {
@@ -177,9 +178,12 @@ __global__ __launch_bounds__(64 * kLnBwdWaves) void layernorm_bwd_kernel(
           const float dxh = dy[i].x[v][j] * g.x[v][j];
           s1 += dxh;
           s2 += dxh * xh;
-          pg[v][j] += dy[i].x[v][j] * xh;
-          pb[v][j] += dy[i].x[v][j];
+          if (PART) {
+            pg[v][j] += dy[i].x[v][j] * xh;
+            pb[v][j] += dy[i].x[v][j];
+          }
         }
+      if (!DX) continue;
       s1 = wave_sum(s1) / (float)d;
       s2 = wave_sum(s2) / (float)d;
       uint16_t h[VPL][8];
@@ -195,6 +199,7 @@ __global__ __launch_bounds__(64 * kLnBwdWaves) void layernorm_bwd_kernel(
       store_row<DT, VPL>(dX + (r + i) * ldo, d, lane, h);
     }
   }
+  if (!PART) return;
   // the waves' column partials, combined in wave order through LDS
   __shared__ float red[kLnBwdWaves][2][512];
   float* out = part + (int64_t)blockIdx.x * 2 * d;
@@ -489,9 +494,19 @@ static void ln_bwd_launch(int vpl, unsigned grid, hipStream_t s, const uint16_t*
                           const uint16_t* g, const uint16_t* dY, const uint16_t* Rg, uint16_t* dX,
                           int64_t ldo, int64_t rows, int64_t d, float* part) {
   constexpr int NT = 64 * kLnBwdWaves;
-  if (vpl == 1) layernorm_bwd_kernel<DT, 1><<<grid, NT, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part);
-  else if (vpl == 2) layernorm_bwd_kernel<DT, 2><<<grid, NT, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part);
-  else layernorm_bwd_kernel<DT, 4><<<grid, NT, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part);
+#define MPX_LNB(V, DXv, PARTv) \
+  layernorm_bwd_kernel<DT, V, DXv, PARTv><<<grid, NT, 0, s>>>(X, ldx, g, dY, Rg, dX, ldo, rows, d, part)
+#define MPX_LNB_V(V)                        \
+  do {                                      \
+    if (dX && part) MPX_LNB(V, true, true); \
+    else if (dX) MPX_LNB(V, true, false);   \
+    else MPX_LNB(V, false, true);           \
+  } while (0)
+  if (vpl == 1) MPX_LNB_V(1);
+  else if (vpl == 2) MPX_LNB_V(2);
+  else MPX_LNB_V(4);
+#undef MPX_LNB_V
+#undef MPX_LNB
 }
 
 extern "C" int mpx_layernorm_fwd(const void* X, int64_t ldx, const void* gamma, const void* beta,
@@ -523,26 +538,33 @@ extern "C" int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, 
                                  int64_t rows, int64_t d, mpx_dtype dt, void* workspace,
                                  size_t ws_bytes, void* stream) {
   clear_error();
-  MPX_REQUIRE(X && gamma && dY && dX && dgamma && dbeta, "NULL argument");
+  MPX_REQUIRE(X && gamma && dY, "NULL X, gamma or dY");
+  MPX_REQUIRE((dgamma == nullptr) == (dbeta == nullptr), "dgamma and dbeta go together");
+  MPX_REQUIRE(dX || dgamma, "nothing to compute: dX, dgamma and dbeta are all NULL");
   MPX_REQUIRE(rows >= 1 && d >= 1 && d <= 2048 && ldx >= d && ldo >= d, "bad sizes");
   MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
-  const size_t need = mpx_layernorm_bwd_workspace(rows, d);
-  if (!workspace || ws_bytes < need) {
-    set_error("mpx_layernorm_bwd: workspace of " + std::to_string(need) + " bytes required");
-    return MPX_ERR_WORKSPACE;
+  float* part = nullptr;
+  if (dgamma) {  // only the gamma / beta gradients use the workspace
+    const size_t need = mpx_layernorm_bwd_workspace(rows, d);
+    if (!workspace || ws_bytes < need) {
+      set_error("mpx_layernorm_bwd: workspace of " + std::to_string(need) + " bytes required");
+      return MPX_ERR_WORKSPACE;
+    }
+    part = (float*)workspace;
   }
   const int nb = ln_bwd_blocks(rows);
   hipStream_t s = (hipStream_t)stream;
-  float* part = (float*)workspace;
   const unsigned fin = colsum_final_blocks(2 * d);
   if (dt == MPX_F16) {
     ln_bwd_launch<MPX_F16>(vpl_for(d), (unsigned)nb, s, (const uint16_t*)X, ldx, (const uint16_t*)gamma,
                            (const uint16_t*)dY, (const uint16_t*)Rgrad, (uint16_t*)dX, ldo, rows, d, part);
-    colsum_final_kernel<MPX_F16><<<fin, 256, 0, s>>>(part, nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d);
+    if (part)
+      colsum_final_kernel<MPX_F16><<<fin, 256, 0, s>>>(part, nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d);
   } else {
     ln_bwd_launch<MPX_BF16>(vpl_for(d), (unsigned)nb, s, (const uint16_t*)X, ldx, (const uint16_t*)gamma,
                             (const uint16_t*)dY, (const uint16_t*)Rgrad, (uint16_t*)dX, ldo, rows, d, part);
-    colsum_final_kernel<MPX_BF16><<<fin, 256, 0, s>>>(part, nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d);
+    if (part)
+      colsum_final_kernel<MPX_BF16><<<fin, 256, 0, s>>>(part, nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d);
   }
   MPX_LAUNCHED();
   return MPX_OK;

@@ -75,6 +75,37 @@ def test_layernorm_fwd_bwd(fmt, rows, d):
     assert_within(to_host(db), rdb, _sum_bound(dy, fmt, rdb), "LN dbeta")
 
 
+@pytest.mark.parametrize("fmt", FMTS)
+def test_layernorm_bwd_subsets_match_full_call(fmt):
+    """dX alone (no workspace) and dgamma / dbeta alone, as the two-stream
+    backward issues them, give the bits of the full call."""
+    rows, d = 8321, 384
+    x = _rand((rows, d), fmt, 11, 2.0, 0.5)
+    g = _rand((d,), fmt, 12, 0.2, 1.0)
+    dy, rg = _rand((rows, d), fmt, 13), _rand((rows, d), fmt, 14)
+    tx, tg, tdy, trg = (to_dev_half(a, fmt) for a in (x, g, dy, rg))
+    dt = mx.DTYPES[fmt]
+    full = [_empty((rows, d), fmt), _empty((d,), fmt), _empty((d,), fmt)]
+    part = [_empty((rows, d), fmt), _empty((d,), fmt), _empty((d,), fmt)]
+    wsn = mx.mpx_layernorm_bwd_workspace(rows, d)
+    ws = torch.zeros(wsn, dtype=torch.uint8, device="cuda")
+    mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), trg.data_ptr(),
+                         full[0].data_ptr(), d, full[1].data_ptr(), full[2].data_ptr(), rows, d, dt,
+                         ws.data_ptr(), wsn, _s())
+    mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), trg.data_ptr(),
+                         part[0].data_ptr(), d, None, None, rows, d, dt, None, 0, _s())
+    mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), None, None, d,
+                         part[1].data_ptr(), part[2].data_ptr(), rows, d, dt, ws.data_ptr(), wsn, _s())
+    for f, q, what in zip(full, part, ("dX", "dgamma", "dbeta")):
+        assert torch.equal(f, q), what
+    with pytest.raises(mx.MPXError, match="nothing to compute"):
+        mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), None, None, d, None,
+                             None, rows, d, dt, None, 0, _s())
+    with pytest.raises(mx.MPXError, match="together"):
+        mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), None, None, d,
+                             part[1].data_ptr(), None, rows, d, dt, ws.data_ptr(), wsn, _s())
+
+
 def test_layernorm_strided_rows_cls_pooling():
     """Final LayerNorm on the CLS rows of a [B, T, d] token matrix."""
     fmt, B, T, d = "bf16", 6, 5, 384
