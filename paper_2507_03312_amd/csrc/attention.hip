@@ -37,8 +37,8 @@ namespace mpx {
 namespace {
 
 constexpr int HD = 64;               // head dimension
-constexpr int PD = HD + 16;          // LDS row pitch (halves) of [row][d] arrays:
-                                     // 160 B, so 4 consecutive rows of a
+constexpr int PD = HD + 8;           // LDS row pitch (halves) of [row][d] arrays:
+                                     // 144 B, so the 4 consecutive rows of a
                                      // transposed read fall in distinct banks
 
 // MFMA operand fragment (32 rows of m or n, 16 k) from an LDS array stored
@@ -297,7 +297,10 @@ __global__ __launch_bounds__(NB * 64) void attn_bwd_kernel(const uint16_t* __res
                                                            uint16_t* __restrict__ dqkv, int T, int H,
                                                            int ldP, float scale) {
   constexpr int TK = 32 * NB;
-  constexpr int PK = TK + 16;  // pitch (halves) of the [query][key] arrays
+  // pitch (halves) of the [query][key] arrays: 4 consecutive rows of a
+  // transposed read land in distinct banks, and at T <= 96 the whole LDS
+  // footprint stays under 80 KiB, so two workgroups share a CU
+  constexpr int PK = TK + 8;
   __shared__ __attribute__((aligned(16))) uint16_t sK[TK * PD];
   __shared__ __attribute__((aligned(16))) uint16_t sQ[TK * PD];
   __shared__ __attribute__((aligned(16))) uint16_t sdO[TK * PD];
