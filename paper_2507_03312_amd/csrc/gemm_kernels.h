@@ -911,9 +911,26 @@ static bool dma_ok(const GemmArgs& g, bool vec, bool ak, bool bk) {
 // Measured on MI355X over the transformer layer shapes (M 8320..25216, N and K
 // 384..3072) and 8192^3: configuration 7 (two co-resident workgroups hide
 // each other's epilogue and pipeline bubbles) is the fastest direct-to-LDS
-// variant for every shape, forward and backward; the register-staged
-// kernels serve operands the copies cannot take.
+// variant at full occupancy, forward and backward; the register-staged
+// kernels serve operands the copies cannot take.  What remains is tile
+// quantisation: 128 x 128 tiles run 512 at a time (2 per CU), 64 x 128
+// tiles 768 at a time (3 per CU) with half the work each, so an output
+// whose 128 x 128 tile count sits just above a multiple of 512 runs a
+// nearly empty last round.  Cost of a configuration = rounds x
+// (workgroups per CU) x (tile area), with 5% added for the smaller tiles'
+// lower MFMA efficiency; the 64 x 128 tiles are taken when they save more
+// than 3% (on the ViT layer shapes this picks the faster of the two in
+// every measured case, e.g. 12608 x 768 outputs: 22 us instead of 29).
 static bool small_ok(const GemmArgs& g, int64_t nbatch);
+
+static bool prefer_64x128(const GemmArgs& g, int64_t nbatch) {
+  const int64_t nb = g.splits > 1 ? g.splits : nbatch;
+  const int64_t tn = (g.N + 127) / 128;
+  const int64_t t128 = ((g.M + 127) / 128) * tn * nb, t64 = ((g.M + 63) / 64) * tn * nb;
+  const double cost128 = (double)((t128 + 511) / 512) * 2.0 * 2.0;
+  const double cost64 = (double)((t64 + 767) / 768) * 3.0 * 1.05;
+  return cost64 < 0.97 * cost128;
+}
 
 static int choose_config(const GemmArgs& g, bool vec, bool ak, bool bk, int64_t nbatch) {
   const bool dma = dma_ok(g, vec, ak, bk);
@@ -925,14 +942,7 @@ static int choose_config(const GemmArgs& g, bool vec, bool ak, bool bk, int64_t 
   if (f == 1 || (f == 2 && vec)) return f;
   if (small && (g.M <= 32 || g.N <= 32 || g.K <= 32)) return 8;
   if (g.M <= 64 || g.N <= 64) return 1;
-  if (dma) {
-    // fewer 128 x 128 tiles than CUs: halve the tile height (measured on the
-    // M = 8320, N = 384 layer products: 195 tiles -> 390)
-    const int64_t tiles = ((g.M + 127) / 128) * ((g.N + 127) / 128) *
-                          (g.splits > 1 ? g.splits : nbatch);
-    if (ak && tiles < 256) return 9;
-    return 7;
-  }
+  if (dma) return ak && prefer_64x128(g, nbatch) ? 9 : 7;
   return vec ? 2 : 0;
 }
 

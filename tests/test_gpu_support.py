@@ -42,7 +42,7 @@ def _sum_bound(x, fmt, ref):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
-@pytest.mark.parametrize("rows,d", [(130, 384), (7, 768), (33, 100), (5, 2048), (8321, 384)])
+@pytest.mark.parametrize("rows,d", [(130, 384), (7, 768), (33, 100), (5, 2048), (8321, 384), (3001, 768)])
 def test_layernorm_fwd_bwd(fmt, rows, d):
     pol = Policy(fmt)
     x = _rand((rows, d), fmt, 1, 2.0, 0.5)
