@@ -158,6 +158,27 @@ def calibration_copy(args, dev):
     torch.cuda.synchronize()
 
 
+def gemm_table(st, peak):
+    """TFLOP/s of each distinct linear-layer GEMM call of the step (forward,
+    dX, dW + db), each timed like the dominant kernel, and the FLOP-weighted
+    aggregate over one block's calls, against the dense MFMA peak."""
+    sites = st.gemm_sites()
+    if not sites:
+        return None
+    out, fl, tm = {}, 0.0, 0.0
+    for name, M, N, K, call in sites:
+        ms = st.time_call(call)
+        f = 2.0 * M * N * K
+        out[name] = {"M": M, "N": N, "K": K, "us": round(ms * 1e3, 2),
+                     "tflops": round(f / (ms * 1e-3) / 1e12, 1)}
+        if name.startswith("blk0."):
+            fl += f
+            tm += ms
+    agg = fl / (tm * 1e-3) / 1e12
+    return {"sites": out, "block_aggregate_tflops": round(agg, 1), "peak": peak,
+            "block_aggregate_frac": round(agg / peak, 4)}
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -248,6 +269,7 @@ def main():
                 "frac": round(tflops / peak, 4), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
     roof.update({"traffic": traffic_bytes(site["name"]), "algorithmic_bytes": site["bytes"],
                  "flops": site["flops"], "kernel": site["desc"], "avg_launch_ms": round(k_ms, 5)})
+    gemm = gemm_table(st, peak)
     line = {"metric": "train steps/s", "value": round(1000.0 / ms, 3), "unit": "steps/s",
             "n_gpus": 1, "steps": steps, "warmup": warm, "ms_per_step": round(ms, 4),
             "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
@@ -255,6 +277,8 @@ def main():
             "config": {"workload": st.describe(), "global_batch": cfg.batch,
                        "seq_len": cfg.tokens or None, "parallelism": "none"},
             "roofline": roof}
+    if gemm:
+        line["gemm"] = gemm
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline_train(cfg, args.cpu_seconds)
     print(json.dumps(line))

@@ -178,15 +178,17 @@ int mpx_gemm_batched(int32_t trans_a, int32_t trans_b, int64_t M, int64_t N, int
                      void* stream);
 
 /* Tile configuration of the GEMMs above, for tuning and tests: 0 (default)
- * picks per call from the problem shape; 1..9 force one configuration
+ * picks per call from the problem shape; 1..11 force one configuration
  * (1: 64x64 register-staged; 2: 128x128 register-staged; 3: 256x256,
  * 4: 256x128, 5: 128x256, 6: 128x128 four-stage, 7: 128x128 two-stage
  * direct-to-LDS; 8: one wave or lane per output, for skinny products with
- * at most bias and residual epilogues; 9: 64x128 direct-to-LDS, A k-major).
+ * at most bias and residual epilogues; 9: 64x128 direct-to-LDS, A k-major;
+ * 10 and 11: 7 and 9 with persistent workgroups that walk the tiles, for
+ * products without split-K or batching).
  * A forced configuration that a call's operands do not allow (alignment,
  * k not a multiple of 64, layout, epilogue) falls back to the automatic
  * choice.  Process-wide setting; not synchronised with concurrent calls.
- * Errors: MPX_ERR_INVALID for a value outside [0, 9]. */
+ * Errors: MPX_ERR_INVALID for a value outside [0, 11]. */
 int mpx_gemm_set_config(int32_t config);
 
 /* Fused multi-head self-attention core (MPX §2.1 half products with float32

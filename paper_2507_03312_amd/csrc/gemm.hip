@@ -163,7 +163,7 @@ extern "C" int mpx_gemm_batched(int32_t trans_a, int32_t trans_b, int64_t M, int
 
 extern "C" int mpx_gemm_set_config(int32_t config) {
   clear_error();
-  MPX_REQUIRE(config >= 0 && config <= 9, "config must be in [0, 9]");
+  MPX_REQUIRE(config >= 0 && config <= 11, "config must be in [0, 11]");
   g_forced_config = config;
   return MPX_OK;
 }

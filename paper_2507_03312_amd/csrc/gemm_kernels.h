@@ -212,19 +212,24 @@ struct TileLoader {
 // column panels are shared through that XCD's L2 instead of each B panel
 // being fetched again for every tile row.
 template <int BM, int BN>
-__device__ __forceinline__ void tile_origin(int64_t M, int64_t N, int64_t& m0, int64_t& n0) {
+__device__ __forceinline__ void tile_origin_of(uint32_t tile, uint32_t ntiles, int64_t M, int64_t N,
+                                               int64_t& m0, int64_t& n0) {
   // 32-bit index arithmetic (tile counts stay far below 2^32; a 64-bit
   // division is a long software sequence)
   constexpr uint32_t GM = 8;
   const uint32_t tiles_m = (uint32_t)((M + BM - 1) / BM), tiles_n = (uint32_t)((N + BN - 1) / BN);
-  const uint32_t ntiles = gridDim.x;
-  const uint32_t xcd = blockIdx.x % 8, local = blockIdx.x / 8;
+  const uint32_t xcd = tile % 8, local = tile / 8;
   const uint32_t t = xcd * (ntiles / 8) + min(xcd, ntiles % 8) + local;
   const uint32_t first = (t / (GM * tiles_n)) * GM;
   const uint32_t gm = min(tiles_m - first, GM);
   const uint32_t r = t - first * tiles_n;
   m0 = (int64_t)(first + r % gm) * BM;
   n0 = (int64_t)(r / gm) * BN;
+}
+
+template <int BM, int BN>
+__device__ __forceinline__ void tile_origin(int64_t M, int64_t N, int64_t& m0, int64_t& n0) {
+  tile_origin_of<BM, BN>(blockIdx.x, gridDim.x, M, N, m0, n0);
 }
 
 // Epilogue variants chosen at compile time (a mask of these bits), used for
@@ -757,6 +762,110 @@ void gemm_dma_kernel(GemmArgs g) {
   gemm_epilogue<DT, TM, TN, true>(g, acc, m0 + wm0, n0 + wn0, lane, split, offC);
 }
 
+// Persistent form of the direct-to-LDS kernel for one product without
+// split-K or batching: a grid of (workgroups per CU) x 256 workgroups walks
+// the tiles in strides of the grid, so every workgroup stays on one XCD and
+// its tiles keep the XCD-contiguous order of tile_origin.  Between two tiles
+// the next tile's first k tile is copied into stage 0 while the current
+// tile's epilogue stages its output through the LDS above stage 0, so the
+// copy's latency overlaps the epilogue instead of opening the next tile.
+template <int DT, int BM, int BN, int WM, int WN, int OCC, bool AK, bool BKM, int E>
+__global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
+__attribute__((amdgpu_waves_per_eu(OCC, OCC)))
+void gemm_dma_persistent_kernel(GemmArgs g) {
+  constexpr int NWAVES = (BM / WM) * (BN / WN);
+  constexpr int TM = WM / 32, TN = WN / 32;
+  constexpr int A_BYTES = BM * 64 * 2, B_BYTES = BN * 64 * 2;
+  constexpr int STAGE = A_BYTES + B_BYTES;
+  constexpr int EPI = NWAVES * WM * 68 * 2;  // epilogue staging, from the start of stage 1
+  constexpr int SMEM = STAGE + (STAGE > EPI ? STAGE : EPI);
+  __shared__ __attribute__((aligned(1024))) uint8_t smem[SMEM];
+  const uint32_t lds0 = lds_u32(smem);
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm0 = (wave / (BN / WN)) * WM;
+  const int wn0 = (wave % (BN / WN)) * WN;
+  const uint32_t ntiles = (uint32_t)(((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN));
+  const int nk = (int)(g.K / 64);
+
+  FragReader<BM, AK, TM> fa;
+  FragReader<BN, BKM, TN> fb;
+  fa.init(wm0, lane);
+  fb.init(wn0, lane);
+  DmaOperand<BM, AK, NWAVES> da;
+  DmaOperand<BN, BKM, NWAVES> db;
+  int64_t m0, n0;
+  const uint16_t* Ab;
+  const uint16_t* Bb;
+  auto setup = [&](uint32_t t) {
+    tile_origin_of<BM, BN>(t, ntiles, g.M, g.N, m0, n0);
+    Ab = g.A + (AK ? m0 * g.lda : m0);
+    Bb = g.B + (BKM ? n0 * g.ldb : n0);
+    da.init(g.lda, (int)min<int64_t>(BM, g.M - m0), wave, lane);
+    db.init(g.ldb, (int)min<int64_t>(BN, g.N - n0), wave, lane);
+  };
+  auto issue = [&](int kt) {
+    const uint32_t st = lds0 + (uint32_t)((kt & 1) * STAGE);
+    da.issue(reinterpret_cast<const uint16_t*>(reinterpret_cast<const uint8_t*>(Ab) + kt * da.step), st, wave);
+    db.issue(reinterpret_cast<const uint16_t*>(reinterpret_cast<const uint8_t*>(Bb) + kt * db.step),
+             st + A_BYTES, wave);
+  };
+
+  uint32_t t = blockIdx.x;
+  if (t >= ntiles) return;  // uniform over the workgroup
+  setup(t);
+  issue(0);
+  for (;;) {
+    f32x16 acc[TM][TN];
+    static_for<TM>([&](auto i) {
+      static_for<TN>([&](auto j) {
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
+      });
+    });
+    for (int kt = 0; kt < nk; ++kt) {
+      wait_vmcnt<0>();  // k tile kt (and everything issued before it) has landed
+      __syncthreads();
+      if (kt + 1 < nk) issue(kt + 1);
+      const uint32_t sa = lds0 + (uint32_t)((kt & 1) * STAGE), sb = sa + A_BYTES;
+      uint4 af[2][TM], bf[2][TN];
+      static_for<TM>([&](auto i) { af[0][i] = fa.template read<i, 0>(sa); });
+      static_for<TN>([&](auto j) { bf[0][j] = fb.template read<j, 0>(sb); });
+      static_for<4>([&](auto kk) {
+        constexpr int cur = kk & 1, nxt = cur ^ 1;
+        if constexpr (kk + 1 < 4) {
+          static_for<TM>([&](auto i) { af[nxt][i] = fa.template read<i, kk + 1>(sa); });
+          static_for<TN>([&](auto j) { bf[nxt][j] = fb.template read<j, kk + 1>(sb); });
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        static_for<TM>([&](auto i) {
+          static_for<TN>([&](auto j) { acc[i][j] = mfma32<DT>(bf[cur][j], af[cur][i], acc[i][j]); });
+        });
+        __builtin_amdgcn_sched_barrier(0);
+      });
+    }
+    const int64_t me = m0, ne = n0;
+    const uint32_t tn = t + gridDim.x;
+    __syncthreads();  // every wave is done reading the stage buffers
+    if (tn < ntiles) {
+      setup(tn);
+      issue(0);  // lands in stage 0 while this tile's epilogue runs above it
+    }
+    if (E != EPI_GENERIC && g.full_epi && me + BM <= g.M && ne + BN <= g.N) {
+      if constexpr (E != EPI_GENERIC)
+        gemm_epilogue_lds<DT, TM, TN, E>(g, acc, me + wm0, ne + wn0, lane, 0,
+                                         reinterpret_cast<uint16_t*>(smem + STAGE) + wave * (WM * 68));
+    } else {
+      gemm_epilogue<DT, TM, TN, true>(g, acc, me + wm0, ne + wn0, lane, 0, 0);
+    }
+    if (tn >= ntiles) break;
+    t = tn;
+    __syncthreads();  // the epilogue's LDS (stage 1) is free for the next copies
+  }
+}
+
 // Sum of split-K partials in split order, one rounding: C = half(sum_s W[s]).
 template <int DT>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ ws, int splits,
@@ -885,6 +994,34 @@ static hipError_t launch_dma(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipSt
   return hipGetLastError();
 }
 
+template <int DT, int BM, int BN, int WM, int WN, int OCC>
+static hipError_t launch_persistent(GemmArgs g, bool ak, bool bk, hipStream_t s) {
+  constexpr int NT = (BM / WM) * (BN / WN) * 64;
+  const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
+  const unsigned grid = (unsigned)std::min<int64_t>(tiles, 256 * OCC);
+  g.full_epi = full_epilogue_ok(g, BM) ? 1 : 0;
+  const int e = g.full_epi ? epilogue_mask(g) : EPI_GENERIC;
+  if (!ak) return hipErrorInvalidValue;
+#define MPX_P(BKv, Ev) gemm_dma_persistent_kernel<DT, BM, BN, WM, WN, OCC, true, BKv, Ev><<<grid, NT, 0, s>>>(g)
+  if (bk) {
+    switch (e) {
+      case 0: MPX_P(true, 0); break;
+      case EPI_BIAS: MPX_P(true, EPI_BIAS); break;
+      case EPI_BIAS | EPI_GELU: MPX_P(true, EPI_BIAS | EPI_GELU); break;
+      case EPI_BIAS | EPI_RESID: MPX_P(true, EPI_BIAS | EPI_RESID); break;
+      default: MPX_P(true, EPI_GENERIC);
+    }
+  } else {
+    switch (e) {
+      case 0: MPX_P(false, 0); break;
+      case EPI_DACT: MPX_P(false, EPI_DACT); break;
+      default: MPX_P(false, EPI_GENERIC);
+    }
+  }
+#undef MPX_P
+  return hipGetLastError();
+}
+
 // Tile configurations (the value of mpx_gemm_set_config):
 //   1  register-staged 64 x 64, 4 waves          (any operands)
 //   2  register-staged 128 x 128, 8 waves        (16-byte aligned operands)
@@ -896,6 +1033,8 @@ static hipError_t launch_dma(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipSt
 //   8  skinny products: one wave (K > 32) or one lane (K <= 32) per output
 //   9  direct-to-LDS 64 x 128, 4 waves of 32 x 64, 2 stages, three workgroups
 //      per CU (A k-major only)
+//  10  configuration 7, persistent (A k-major, no split-K or batch)
+//  11  configuration 9, persistent (A k-major, no split-K or batch)
 extern int g_forced_config;  // defined in gemm.hip
 
 // The direct-to-LDS kernel needs 16-byte aligned operands and whole k tiles
@@ -938,10 +1077,15 @@ static int choose_config(const GemmArgs& g, bool vec, bool ak, bool bk, int64_t 
   const int f = g_forced_config;
   if (f == 8 && small) return 8;
   if (f == 9 && dma && ak) return 9;
+  if ((f == 10 || f == 11) && dma && ak) return g.splits == 1 && nbatch == 1 ? f : (f == 10 ? 7 : 9);
   if (f >= 3 && f <= 7 && dma) return f;
   if (f == 1 || (f == 2 && vec)) return f;
   if (small && (g.M <= 32 || g.N <= 32 || g.K <= 32)) return 8;
   if (g.M <= 64 || g.N <= 64) return 1;
+  // (the persistent forms 10 and 11 are 1-5% faster on a product alone, but
+  // they hold every workgroup slot of the chip until they end, so the
+  // weight-gradient stream of the training step cannot interleave: the ViT
+  // steps ran 2-4% slower with them)
   if (dma) return ak && prefer_64x128(g, nbatch) ? 9 : 7;
   return vec ? 2 : 0;
 }
@@ -1012,6 +1156,8 @@ static hipError_t run_gemm(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipStre
     case 6: return launch_dma<DT, 128, 128, 64, 64, 4, 1>(g, ak, bk, nbatch, s);
     case 7: return launch_dma<DT, 128, 128, 64, 64, 2, 2>(g, ak, bk, nbatch, s);
     case 9: return launch_dma<DT, 64, 128, 32, 64, 2, 3>(g, ak, bk, nbatch, s);
+    case 10: return launch_persistent<DT, 128, 128, 64, 64, 2>(g, ak, bk, s);
+    case 11: return launch_persistent<DT, 64, 128, 32, 64, 3>(g, ak, bk, s);
     default:  // unaligned operands (rare: odd leading dimensions)
       return launch_cfg<DT, 128, 128, 64, 64>(g, ak, bk, vec, nbatch, s);
   }

@@ -199,11 +199,21 @@ class TrainStep:
         """Mean duration (ms) of one launch of the dominant kernel, from HIP
         events around a graph of ``launches`` back-to-back launches of it with
         the step's own operands (so no host launch gap is measured)."""
+        return self.time_call(self._dominant_call, launches, reps)
+
+    def gemm_sites(self):
+        """(site, M, N, K, call) for each distinct linear-layer GEMM call of the
+        step, as the step issues it; each does 2 M N K flops."""
+        return []
+
+    def time_call(self, call, launches: int = 20, reps: int = 5) -> float:
+        """Mean duration (ms) of ``call(stream)`` from HIP events around a graph
+        of ``launches`` back-to-back calls, replayed ``reps`` times."""
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             for _ in range(launches):
-                self._dominant_call(_stream())
+                call(_stream())
         g.replay()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -351,6 +361,45 @@ class ViTStep(TrainStep):
         mx.mpx_linear_fwd(_ptr(blk["c"]), _ptr(a.w("blk0.up.w")), _ptr(a.w("blk0.up.b")), None,
                           _ptr(blk["u"]), _ptr(blk["u_pre"]), c.batch * c.tokens, c.d_mlp,
                           c.d_model, self.dt, mx.MPX_ACT_GELU_TANH, s)
+
+    def gemm_sites(self):
+        """Block 0's four linear layers (forward with the step's epilogue, dX,
+        and dW + db with split-K) and the patch embedding, with the step's own
+        operands and calls."""
+        c, a, dt = self.cfg, self.arena, self.dt
+        B, T, d, F = c.batch, c.tokens, c.d_model, c.d_mlp
+        M = B * T
+        W, G, blk = a.w, a.gr, self.blocks[0]
+        GELU, NONE = mx.MPX_ACT_GELU_TANH, mx.MPX_ACT_NONE
+        ws2p, ws2b = _ptr(self.ws2), self.ws2.numel()
+        sites = []
+
+        def layer(name, X, R, Y, pre, act, dY, Xpre, x_act, dX, Mr, N, K):
+            w, b, gw, gb = W(name + ".w"), W(name + ".b"), G(name + ".w"), G(name + ".b")
+            sites.append((name + ".fwd", Mr, N, K, lambda s: mx.mpx_linear_fwd(
+                _ptr(X), _ptr(w), _ptr(b), _ptr(R), _ptr(Y), _ptr(pre), Mr, N, K, dt, act, s)))
+            if dX is not None:
+                sites.append((name + ".dX", Mr, N, K, lambda s: mx.mpx_linear_bwd(
+                    None, _ptr(w), _ptr(dY), _ptr(Xpre), x_act, _ptr(dX), None, None, Mr, N, K, dt,
+                    None, 0, s)))
+            sites.append((name + ".dW", Mr, N, K, lambda s: mx.mpx_linear_bwd(
+                _ptr(X), None, _ptr(dY), None, NONE, None, _ptr(gw), _ptr(gb), Mr, N, K, dt,
+                ws2p, ws2b, s)))
+
+        dx, du_pre, dx1, dqkv = self.dx[0], self.du_pre[0], self.dx1[0], self.dqkv[0]
+        if c.image:
+            layer("patch", self.patches, None, self.E, None, NONE, self.dE, None, NONE, None,
+                  B * c.n_patches, d, c.patch_dim)
+        p = "blk0."
+        layer(p + "qkv", blk["a"], None, blk["qkv"], None, NONE, dqkv, None, NONE, self.da,
+              M, 3 * d, d)
+        layer(p + "proj", blk["O"], self.x0, blk["x1"], None, NONE, dx1, None, NONE, self.dO,
+              M, d, d)
+        layer(p + "up", blk["c"], None, blk["u"], blk["u_pre"], GELU, du_pre, None, NONE, self.dc,
+              M, F, d)
+        layer(p + "down", blk["u"], blk["x1"], blk["x2"], None, NONE, dx, blk["u_pre"], GELU,
+              du_pre, M, d, F)
+        return sites
 
     def dominant_site(self):
         c = self.cfg

@@ -219,7 +219,7 @@ def test_full_size_linear_sampled(fmt, mnk):
     assert_within(to_host(gdw)[np.ix_(cols, kc)], ref, gemm_bound(dy[:, cols].T, x[:, kc], ref, fmt, M), "dW")
 
 
-CONFIGS = [1, 2, 3, 4, 5, 6, 7, 9]
+CONFIGS = [1, 2, 3, 4, 5, 6, 7, 9, 10, 11]
 
 
 @pytest.fixture
@@ -288,6 +288,48 @@ def test_every_tile_config(gemm_config, fmt):
     bnd = ulp(kt_v, fmt) + 2 * T * 2.0 ** -24 * (np.abs(k_t.astype(np.float64)) @ np.abs(v.astype(np.float64)))
     got = to_host(out_o).reshape(B, T, H, hd)[:, :hd].transpose(0, 2, 1, 3)
     assert_within(got, kt_v, bnd, "K^T V")
+
+
+@pytest.mark.parametrize("persistent,plain", [(10, 7), (11, 9)])
+@pytest.mark.parametrize("fmt", FMTS)
+def test_persistent_configs_walk_many_tiles(fmt, persistent, plain):
+    """The persistent configurations on outputs with more tiles than the grid
+    has workgroups (each walks 2 or 3 tiles, ragged edges included): bit-equal
+    to the same tile shape launched one workgroup per tile, and sampled
+    outputs within the GEMM bar of the oracle.  Forward with bias + GELU and
+    dX through GELU', the two epilogues with an LDS-staged variant."""
+    pol = Policy(fmt)
+    dt = mx.DTYPES[fmt]
+    M, N, K = 4200, 2100, 192
+    x, w, b = _rand((M, K), fmt, 61), _rand((N, K), fmt, 62, 0.05), _rand((N,), fmt, 63, 0.5)
+    dy, xpre = _rand((M, N), fmt, 64), _rand((M, K), fmt, 65)
+    tx, tw, tb, tdy, txp = (to_dev_half(a, fmt) for a in (x, w, b, dy, xpre))
+    out = {}
+    try:
+        for cfg in (plain, persistent):
+            mx.mpx_gemm_set_config(cfg)
+            y, pre, gdx = _empty((M, N), fmt), _empty((M, N), fmt), _empty((M, K), fmt)
+            mx.mpx_linear_fwd(tx.data_ptr(), tw.data_ptr(), tb.data_ptr(), None, y.data_ptr(),
+                              pre.data_ptr(), M, N, K, dt, mx.MPX_ACT_GELU_TANH, _s())
+            mx.mpx_linear_bwd(None, tw.data_ptr(), tdy.data_ptr(), txp.data_ptr(),
+                              mx.MPX_ACT_GELU_TANH, gdx.data_ptr(), None, None, M, N, K, dt,
+                              None, 0, _s())
+            torch.cuda.synchronize()
+            out[cfg] = (y, pre, gdx)
+    finally:
+        mx.mpx_gemm_set_config(0)
+    for a, c, what in zip(out[plain], out[persistent], ("Y", "pre-activation", "dX")):
+        assert torch.equal(a, c), what
+    rng = np.random.default_rng(7)
+    rows, cols = np.unique(rng.integers(0, M, 40)), np.unique(rng.integers(0, N, 40))
+    ref = ops.linear_fwd(pol, x[rows], w[cols], b[cols])
+    assert_within(to_host(out[persistent][1])[np.ix_(rows, cols)], ref,
+                  gemm_bound(x[rows], w[cols].T, ref, fmt, K), "pre-activation")
+    kc = np.unique(rng.integers(0, K, 40))
+    rdx = pol.gemm(dy[rows], w[:, kc])
+    ref = ops.gelu_bwd(pol, xpre[np.ix_(rows, kc)], rdx)
+    assert_within(to_host(out[persistent][2])[np.ix_(rows, kc)], ref,
+                  1.13 * gemm_bound(dy[rows], w[:, kc], rdx, fmt, N) + ulp(ref, fmt), "dX")
 
 
 @pytest.mark.parametrize("fmt", FMTS)
