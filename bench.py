@@ -43,10 +43,10 @@ DEFAULT_CONFIG = "vit_block"
 # they no longer match, the figure is stale and reported as null.
 TRAFFIC = {
     "blk0.up.fwd": {
-        "fetch_kib": 13954.4, "write_kib": 49920.0,
-        "fetch_factor": 262144.0 / 131088.8, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 13975.4, "write_kib": 49920.0,
+        "fetch_factor": 262144.0 / 131088.4, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/gemm_kernels.h": "fecc198a81b2ca6491766100f845c3f17c6d527d69de6b0ba130ea5081969a61",
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "3fba3ac8fb77021bb068716256f7178b1c1a926420d0b42f2a2d29c1712fa920",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
             "paper_2507_03312_amd/csrc/common.h": "730b9a02e1fa63f557d2c496e7263b42acecd1543d8f7cb787b1a2929e4bbeee",
         },
