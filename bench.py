@@ -52,10 +52,10 @@ TRAFFIC = {
         },
     },
     "sweep": {
-        "fetch_kib": 685321.4, "write_kib": 1367242.2,
-        "fetch_factor": 262144.0 / 131086.2, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 686822.2, "write_kib": 1367202.4,
+        "fetch_factor": 262144.0 / 131089.1, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/sweep.hip": "834620fdf6a477404ce1056458cbd2dc253f85bcb8cd2999e23dd108cedfecfb",
+            "paper_2507_03312_amd/csrc/sweep.hip": "c602435f1b696d1b01bd40828d85fbd12bbbce651354540e554f5fb723602496",
             "paper_2507_03312_amd/csrc/common.h": "730b9a02e1fa63f557d2c496e7263b42acecd1543d8f7cb787b1a2929e4bbeee",
         },
     },
