@@ -337,6 +337,9 @@ class ViTStep(TrainStep):
         # the residual stream) buffered, so the critical path of block k-1
         # never overwrites what the side stream still reads for block k
         self.dx = [z(M, d) for _ in range(3)]
+        # the last block's cotangent from the final LayerNorm: only its CLS
+        # rows are ever written, so it is zeroed once here, not every step
+        self.dxf = z(M, d)
         self.du_pre = [z(M, F) for _ in range(2)]
         self.dx1 = [z(M, d) for _ in range(2)]
         self.dqkv = [z(M, 3 * d) for _ in range(2)]
@@ -537,8 +540,7 @@ class ViTStep(TrainStep):
 
         wgrad(self.zf, self.dlogits, G("head.w"), G("head.b"), B, Cn, d)
         dgrad(W("head.w"), self.dlogits, None, NONE, self.dz, B, Cn, d)
-        dx = self.dx[0]
-        mx.mpx_zero(_ptr(dx), dx.numel() * 2, s)
+        dx = self.dxf
         mx.mpx_layernorm_bwd(_ptr(x), T * d, _ptr(W("lnf.g")), _ptr(self.dz), None, _ptr(dx),
                              T * d, _ptr(G("lnf.g")), _ptr(G("lnf.b")), B, d, dt, wsp, wsb, s)
         done = []  # side-stream completion of each block's weight gradients
@@ -548,7 +550,7 @@ class ViTStep(TrainStep):
             xin = self.x0 if i == 0 else self.blocks[i - 1]["x2"]
             if k >= 2:  # block k-2's side work read the buffers block k is about to reuse
                 main.wait_event(done[k - 2])
-            dx, dx_out = self.dx[k % 3], self.dx[(k + 1) % 3]
+            dx_out = self.dx[(k + 1) % 3]
             du_pre, dx1, dqkv = self.du_pre[k % 2], self.dx1[k % 2], self.dqkv[k % 2]
             wgrad(blk["u"], dx, G(p + "down.w"), G(p + "down.b"), M, d, F)
             dgrad(W(p + "down.w"), dx, blk["u_pre"], GELU, du_pre, M, d, F)
