@@ -53,17 +53,31 @@ __device__ __forceinline__ uint4 frag_tr(uint32_t base, int pitch, int k0, int m
   return make_uint4(lo.x, lo.y, hi.x, hi.y);
 }
 
-// Rows [0, rows) of a [T, 64] head slice (row stride ld) into LDS [rows][PD];
-// rows >= T are zero.
-__device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* src, int64_t ld, int T,
-                                           int rows, int tid, int nthreads) {
-  for (int c = tid; c < rows * 8; c += nthreads) {
-    const int r = c >> 3, col = (c & 7) * 8;
-    u32x4 v = {0u, 0u, 0u, 0u};
-    if (r < T) v = *reinterpret_cast<const u32x4*>(src + r * ld + col);
-    *reinterpret_cast<u32x4*>(lds + r * PD + col) = v;
+// Rows [0, rows) of a [T, 64] head slice (row stride ld) staged into LDS
+// [rows][PD] in two steps, PER 16-byte chunks per thread: load() puts every
+// global load of the thread in flight, store() writes them (rows >= T are
+// zero).  A loop that stores each chunk before loading the next waits one
+// memory latency per chunk.  Requires rows * 8 <= PER * nthreads.
+template <int PER>
+struct RowStage {
+  u32x4 v[PER];
+  __device__ __forceinline__ void load(const uint16_t* src, int64_t ld, int T, int rows, int tid,
+                                       int nthreads) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * nthreads;
+      v[i] = u32x4{0u, 0u, 0u, 0u};
+      if (c < rows * 8 && (c >> 3) < T) v[i] = *reinterpret_cast<const u32x4*>(src + (c >> 3) * ld + (c & 7) * 8);
+    }
   }
-}
+  __device__ __forceinline__ void store(uint16_t* lds, int rows, int tid, int nthreads) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * nthreads;
+      if (c < rows * 8) *reinterpret_cast<u32x4*>(lds + (c >> 3) * PD + (c & 7) * 8) = v[i];
+    }
+  }
+};
 
 // Packs 4 halves.
 __device__ __forceinline__ u32x2 pack4(uint16_t a, uint16_t b, uint16_t c, uint16_t d) {
@@ -103,7 +117,8 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_rows_kernel(const uint16_t* 
   const uint16_t* K = Q + dm;
   const uint16_t* V = Q + 2 * dm;
 
-  stage_rows(sV, V, ld, T, TK, tid, NB * 64);
+  RowStage<4> vst;  // V: 32 NB rows over 64 NB threads
+  vst.load(V, ld, T, TK, tid, NB * 64);
 
   // S^T blocks: rows = keys of block j, columns = the wave's 32 queries
   const int q = 32 * w + (lane & 31);
@@ -160,6 +175,7 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_rows_kernel(const uint16_t* 
   });
 
   // O^T = V^T P^T: rows = d (two blocks of 32), columns = the wave's queries
+  vst.store(sV, TK, tid, NB * 64);
   __syncthreads();
   const uint32_t vbase = lds_u32(sV);
   f32x16 o[2];
@@ -224,8 +240,10 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_kernel(const uint16_t* __res
   uint4 qf[4];
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) qf[kk] = ld_u4(Q + qc * ld + 16 * kk + 8 * hi);
-  stage_rows(sK, K, ld, T, TK, tid, NB * 64);
-  stage_rows(sV, V, ld, T, TK, tid, NB * 64);
+  RowStage<4> kst, vst;  // K and V: 32 NB rows over 64 NB threads
+  kst.load(K, ld, T, TK, tid, NB * 64);
+  vst.load(V, ld, T, TK, tid, NB * 64);
+  kst.store(sK, TK, tid, NB * 64);
   __syncthreads();
   const uint32_t kbase = lds_u32(sK), vbase = lds_u32(sV);
 
@@ -260,6 +278,8 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_kernel(const uint16_t* __res
     l = (m == -INFINITY ? 0.0f : l * __expf(m - mn)) + t;
     m = mn;
   }
+  vst.store(sV, TK, tid, NB * 64);
+  __syncthreads();
   const float M = fmaxf(m, __shfl_xor(m, 32));  // finite: key 0 is in every row
   const float lc = m == -INFINITY ? 0.0f : l * __expf(m - M);
   const float inv = 1.0f / (lc + __shfl_xor(lc, 32));
@@ -443,9 +463,15 @@ __global__ __launch_bounds__(NB * 64) void attn_bwd_kernel(const uint16_t* __res
   const uint16_t* G = dO + (int64_t)b * T * dm + h * HD;
   uint16_t* dQ = dqkv + (int64_t)b * T * ld + h * HD;
 
-  stage_rows(sK, K, ld, T, TK, tid, NB * 64);
-  stage_rows(sQ, Q, ld, T, TK, tid, NB * 64);
-  stage_rows(sdO, G, dm, T, TK, tid, NB * 64);
+  {
+    RowStage<4> kst, qst, gst;  // 32 NB rows each over 64 NB threads
+    kst.load(K, ld, T, TK, tid, NB * 64);
+    qst.load(Q, ld, T, TK, tid, NB * 64);
+    gst.load(G, dm, T, TK, tid, NB * 64);
+    kst.store(sK, TK, tid, NB * 64);
+    qst.store(sQ, TK, tid, NB * 64);
+    gst.store(sdO, TK, tid, NB * 64);
+  }
 
   const int q = 32 * w + (lane & 31);
   u32x2 Pr[NB][4], Sr[NB][4];
@@ -500,7 +526,11 @@ __global__ __launch_bounds__(NB * 64) void attn_bwd_dq_kernel(const uint16_t* __
   const int64_t ld = 3 * (int64_t)dm;
   const uint16_t* Q = qkv + (int64_t)b * T * ld + h * HD;
   const uint16_t* G = dO + (int64_t)b * T * dm + h * HD;
-  stage_rows(sK, Q + dm, ld, T, TK, tid, NB * 64);
+  {
+    RowStage<4> kst;
+    kst.load(Q + dm, ld, T, TK, tid, NB * 64);
+    kst.store(sK, TK, tid, NB * 64);
+  }
 
   const int q = 32 * w + (lane & 31);
   const int64_t row = (int64_t)bh * T + min(q, T - 1);
@@ -551,17 +581,33 @@ __global__ __launch_bounds__(NB * 64) void attn_bwd_dkv_kernel(const uint16_t* _
     for (int e = 0; e < 16; ++e) dk[db][e] = dv[db][e] = 0.0f;
   for (int q0 = 0; q0 < T; q0 += 32) {
     __syncthreads();  // the previous block's reads are done
-    stage_rows(sQ, Q + q0 * ld, ld, T - q0, 32, tid, nthreads);
-    stage_rows(sdO, G + q0 * dm, dm, T - q0, 32, tid, nthreads);
-    for (int c = tid; c < 32 * (TK / 8); c += nthreads) {
+    static_assert(NB >= 4 && 32 * (TK / 8) == 2 * NB * 64, "staging shape of the dK / dV kernel");
+    // every load of the block in flight before any LDS write: 32 rows of Q
+    // and dO (one chunk per thread at most: 256 <= 64 NB), 32 x TK of P and
+    // dS (exactly two chunks per thread)
+    RowStage<1> qst, gst;
+    qst.load(Q + q0 * ld, ld, T - q0, 32, tid, nthreads);
+    gst.load(G + q0 * dm, dm, T - q0, 32, tid, nthreads);
+    u32x4 pv[2], sv[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + i * nthreads;
       const int r = c / (TK / 8), col = (c % (TK / 8)) * 8;
-      u32x4 pv = {0u, 0u, 0u, 0u}, sv = {0u, 0u, 0u, 0u};
+      pv[i] = u32x4{0u, 0u, 0u, 0u};
+      sv[i] = u32x4{0u, 0u, 0u, 0u};
       if (q0 + r < T && col < ldP) {
-        pv = *reinterpret_cast<const u32x4*>(Pb + (int64_t)(q0 + r) * ldP + col);
-        sv = *reinterpret_cast<const u32x4*>(Sb + (int64_t)(q0 + r) * ldP + col);
+        pv[i] = *reinterpret_cast<const u32x4*>(Pb + (int64_t)(q0 + r) * ldP + col);
+        sv[i] = *reinterpret_cast<const u32x4*>(Sb + (int64_t)(q0 + r) * ldP + col);
       }
-      *reinterpret_cast<u32x4*>(sP + r * PK + col) = pv;
-      *reinterpret_cast<u32x4*>(sdS + r * PK + col) = sv;
+    }
+    qst.store(sQ, 32, tid, nthreads);
+    gst.store(sdO, 32, tid, nthreads);
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = tid + i * nthreads;
+      const int r = c / (TK / 8), col = (c % (TK / 8)) * 8;
+      *reinterpret_cast<u32x4*>(sP + r * PK + col) = pv[i];
+      *reinterpret_cast<u32x4*>(sdS + r * PK + col) = sv[i];
     }
     __syncthreads();
 #pragma unroll
