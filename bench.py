@@ -182,8 +182,8 @@ def gemm_table(st, peak):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(data-parallel sharding is described in DESIGN.md)", file=sys.stderr)
+        print("bench.py measures one GPU only: the library has no multi-GPU path "
+              "(data-parallel sharding is not implemented)", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2507_03312_amd.train import make_step

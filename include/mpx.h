@@ -46,7 +46,7 @@ typedef enum { MPX_F32 = 0, MPX_F16 = 1, MPX_BF16 = 2 } mpx_dtype;
 enum {
   MPX_OK = 0,
   MPX_ERR_INVALID = -1,     /* null pointer, bad size, bad dtype, mismatched lists */
-  MPX_ERR_UNSUPPORTED = -2, /* a valid request this build does not implement */
+  MPX_ERR_UNSUPPORTED = -2, /* a valid request the library does not implement */
   MPX_ERR_HIP = -3,         /* a HIP runtime call or kernel launch failed */
   MPX_ERR_WORKSPACE = -4    /* workspace missing or smaller than required */
 };

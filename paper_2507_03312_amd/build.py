@@ -22,7 +22,8 @@ SOURCES = ["sweep.hip", "gemm.hip", "gemm_f16.hip", "gemm_bf16.hip", "support.hi
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
-    # packed float32 instructions are never generated
+    # no packed float32 instructions (v_pk_*_f32) are generated: the kernels
+    # are written and checked without them
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", INCLUDE, "-I", CSRC,
 ]
