@@ -270,6 +270,37 @@ int mpx_cross_entropy(const void* Z, int64_t ldz, const int32_t* labels, int64_t
                       int64_t C, const mpx_scale_state* d_state, float* d_loss, void* dZ,
                       mpx_dtype dt, void* workspace, size_t ws_bytes, void* stream);
 
+/* Workspace (bytes) of mpx_classifier_head for B rows of width d: the row
+ * losses and one pair of float32 gamma / beta partial rows per 4 rows,
+ * overwritten by every call. */
+size_t mpx_classifier_head_workspace(int64_t B, int64_t d);
+
+/* The classifier head of a ViT step, forward and backward, one pass per row
+ * (a fusion of mpx_layernorm_fwd, mpx_linear_fwd, mpx_cross_entropy, the dX
+ * half of mpx_linear_bwd and mpx_layernorm_bwd for C <= 32 classes; the
+ * final LayerNorm and the loss run in full precision, MPX §3.2, and the
+ * backward is seeded with the loss scale, §3.4):
+ *   Z = half(LayerNorm(X; gamma, beta))                     [B, d] dense
+ *   logit = half(Z W^T + b)  (W [C, d], b [C])   (not stored)
+ *   *d_loss = mean_b(logsumexp(logit_b) - logit_b[y_b])     (float32)
+ *   dlogits = half(scale * (softmax(logit) - onehot(y)) / B) [B, C] dense
+ *   dZ = half(dlogits W)  (classes summed in order; not stored)
+ *   dX = half(LayerNorm backward of dZ)   rows of stride ldo
+ *   dgamma = half(sum_b dZ * xhat), dbeta = half(sum_b dZ)
+ * X: B rows of width d with row stride ldx (e.g. the CLS rows of a
+ * [B, T, d] activation: ldx = T d); labels: int32 [B]; 1 <= C <= 32,
+ * 1 <= d <= 2048, C * d <= 16384 (W is staged in on-chip memory), B <= 2048.  Every result is the same bits as the separate
+ * calls give (same arithmetic, summation orders and roundings).  The weight
+ * and bias gradients of the linear layer are left to mpx_linear_bwd (from Z
+ * and dlogits).  A label outside [0, C) makes the loss NaN.  Errors:
+ * MPX_ERR_INVALID (NULL, sizes, C outside [1, 32], C * d > 16384, B > 2048),
+ * MPX_ERR_WORKSPACE. */
+int mpx_classifier_head(const void* X, int64_t ldx, const void* gamma, const void* beta,
+                        const void* W, const void* b, const int32_t* labels, int64_t B, int64_t d,
+                        int64_t C, const mpx_scale_state* d_state, void* Z, float* d_loss,
+                        void* dlogits, void* dX, int64_t ldo, void* dgamma, void* dbeta,
+                        mpx_dtype dt, void* workspace, size_t ws_bytes, void* stream);
+
 /* Mean squared error over n elements and its scaled cotangent:
  *   *d_loss = mean((y - t)^2);  dY = half(scale * 2 (y - t) / n). */
 int mpx_mse(const void* Y, const void* T, int64_t n, const mpx_scale_state* d_state,

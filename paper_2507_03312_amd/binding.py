@@ -74,6 +74,9 @@ _SIGS = {
     "mpx_loss_workspace": (SZ, [I64]),
     "mpx_cross_entropy": (C.c_int, [P, I64, P, I64, I64, P, P, P, I32, P, SZ, P]),
     "mpx_mse": (C.c_int, [P, P, I64, P, P, P, I32, P, SZ, P]),
+    "mpx_classifier_head_workspace": (SZ, [I64, I64]),
+    "mpx_classifier_head": (C.c_int, [P, I64, P, P, P, P, P, I64, I64, I64, P, P, P, P, P, I64, P, P,
+                                      I32, P, SZ, P]),
     "mpx_patchify_cast": (C.c_int, [P, P, I64, I64, I64, I64, I64, I32, P]),
     "mpx_embed_assemble": (C.c_int, [P, P, P, P, I64, I64, I64, I32, P]),
     "mpx_embed_assemble_bwd": (C.c_int, [P, P, P, P, I64, I64, I64, I32, P]),
@@ -171,6 +174,7 @@ mpx_softmax_fwd = _call("mpx_softmax_fwd")
 mpx_softmax_bwd = _call("mpx_softmax_bwd")
 mpx_cross_entropy = _call("mpx_cross_entropy")
 mpx_mse = _call("mpx_mse")
+mpx_classifier_head = _call("mpx_classifier_head")
 mpx_patchify_cast = _call("mpx_patchify_cast")
 mpx_embed_assemble = _call("mpx_embed_assemble")
 mpx_embed_assemble_bwd = _call("mpx_embed_assemble_bwd")
@@ -192,6 +196,10 @@ def mpx_loss_workspace(n: int) -> int:
 
 def mpx_layernorm_bwd_workspace(rows: int, d: int) -> int:
     return int(lib.mpx_layernorm_bwd_workspace(rows, d))
+
+
+def mpx_classifier_head_workspace(B: int, d: int) -> int:
+    return int(lib.mpx_classifier_head_workspace(B, d))
 
 
 def mpx_last_error() -> str:

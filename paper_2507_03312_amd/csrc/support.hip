@@ -399,6 +399,177 @@ __global__ __launch_bounds__(256) void mean_kernel(const float* __restrict__ val
   if (threadIdx.x == 0) *loss = red[0] / (float)n;
 }
 
+// The classifier head of a ViT step in one pass per row: the final LayerNorm
+// on the CLS rows, the linear layer to C <= 32 classes, the mean
+// cross-entropy with the backward seeded by the loss scale (§3.3, §3.4),
+// and the backward through the linear layer and the LayerNorm.  One wave per
+// row; every piece repeats the arithmetic, summation order and rounding
+// points of the separate kernels, so the results are the same bits:
+//   Z = half(LN(x)) as the LayerNorm kernel;
+//   logit = half(Z w_c + b_c) as the skinny product kernel (lane l sums
+//     k = l, l + 64, ..., then a fixed xor butterfly; Z read back from LDS);
+//   dlogit = half(scale / B (softmax - onehot)) as the cross-entropy kernel
+//     (lane c holds class c);
+//   dZ = half(sum_c dlogit_c W_c) with the classes in order, as the skinny
+//     product kernel for a reduction of <= 32;
+//   dX = half(LN backward of dZ) as the LayerNorm backward kernel, and the
+//     gamma / beta column partials of the same 4-row workgroups.
+constexpr int kHeadWaves = 4;
+constexpr int kHeadMaxW = 16384;  // C * d halves of W staged in LDS (32 KiB)
+
+template <int DT, int VPL>
+__global__ __launch_bounds__(64 * kHeadWaves) void classifier_head_kernel(
+    const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __restrict__ gamma,
+    const uint16_t* __restrict__ beta, const uint16_t* __restrict__ W, const uint16_t* __restrict__ bias,
+    const int32_t* __restrict__ labels, int64_t B, int64_t d, int C,
+    const mpx_scale_state* __restrict__ st, uint16_t* __restrict__ Z, uint16_t* __restrict__ dlogits,
+    uint16_t* __restrict__ dX, int64_t ldo, float* __restrict__ rowloss, float* __restrict__ part) {
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t r = (int64_t)blockIdx.x * kHeadWaves + wave;
+  __shared__ uint16_t zrow[kHeadWaves][2048];  // the wave's Z row, read back lane-strided
+  __shared__ __attribute__((aligned(16))) uint16_t sW[kHeadMaxW];  // W [C, d], staged once
+  {
+    // the workgroup's copy of W: 16-byte chunks, every load in flight before
+    // the LDS writes (single halves when W is not 16-byte aligned)
+    const int n = C * (int)d;
+    if ((reinterpret_cast<uintptr_t>(W) & 15u) == 0 && n % 8 == 0) {
+      constexpr int PER = kHeadMaxW / 8 / (64 * kHeadWaves);
+      u32x4 wv[PER];
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int e = 8 * ((int)threadIdx.x + i * 64 * kHeadWaves);
+        wv[i] = e < n ? *reinterpret_cast<const u32x4*>(W + e) : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        const int e = 8 * ((int)threadIdx.x + i * 64 * kHeadWaves);
+        if (e < n) *reinterpret_cast<u32x4*>(sW + e) = wv[i];
+      }
+    } else {
+      for (int e = threadIdx.x; e < n; e += 64 * kHeadWaves) sW[e] = W[e];
+    }
+    __syncthreads();
+  }
+  RowVec<VPL> g, be;
+  load_row<DT, VPL>(gamma, d, lane, g);
+  load_row<DT, VPL>(beta, d, lane, be);
+  float pg[VPL][8], pb[VPL][8];
+#pragma unroll
+  for (int v = 0; v < VPL; ++v)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) pg[v][j] = pb[v][j] = 0.0f;
+  if (r < B) {  // uniform over the wave
+    RowVec<VPL> x;
+    load_row<DT, VPL>(X + r * ldx, d, lane, x);
+    float mean, rstd;
+    row_stats<VPL>(x, d, lane, mean, rstd);
+    uint16_t zh[VPL][8];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) zh[v][j] = f2h<DT>((x.x[v][j] - mean) * rstd * g.x[v][j] + be.x[v][j]);
+    store_row<DT, VPL>(Z + r * d, d, lane, zh);
+    uint16_t* zs = zrow[wave];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v)
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+        if (col_ok(d, lane, v, j)) zs[v * 512 + lane * 8 + j] = zh[v][j];
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    float logit = -INFINITY;  // lane c < C: class c
+    for (int c = 0; c < C; ++c) {
+      const uint16_t* wr = sW + c * d;
+      float acc = 0.0f;
+      for (int64_t k = lane; k < d; k += 64) acc += h2f<DT>(zs[k]) * h2f<DT>(wr[k]);
+#pragma unroll
+      for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
+      acc = __shfl(acc, 0);
+      const float lg = h2f<DT>(f2h<DT>(acc + h2f<DT>(bias[c])));
+      if (lane == c) logit = lg;
+    }
+    const float scale = st->scale;
+    const int32_t y = labels[r];
+    const float mx = wave_max(lane < C ? logit : -INFINITY);
+    const float se = wave_sum(lane < C ? expf(logit - mx) : 0.0f);
+    const float k = scale / (float)B;
+    float dl = 0.0f;
+    if (lane < C) {
+      const float pr = expf(logit - mx) / se;
+      const uint16_t h = f2h<DT>(k * (pr - (lane == y ? 1.0f : 0.0f)));
+      dlogits[r * C + lane] = h;
+      dl = h2f<DT>(h);
+    }
+    const bool ok = y >= 0 && y < C;  // an out-of-range label gives a NaN loss, never a read
+    const float ly = __shfl(logit, ok ? y : 0);
+    if (lane == 0) rowloss[r] = ok ? logf(se) - (ly - mx) : NAN;
+
+    float dz[VPL][8];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) dz[v][j] = 0.0f;
+    for (int c = 0; c < C; ++c) {
+      const float dlc = __shfl(dl, c);
+      const uint16_t* wr = sW + c * d;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v)
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+          if (col_ok(d, lane, v, j)) dz[v][j] += dlc * h2f<DT>(wr[v * 512 + lane * 8 + j]);
+    }
+    float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+    for (int v = 0; v < VPL; ++v)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float dyv = h2f<DT>(f2h<DT>(dz[v][j] + 0.0f));  // + 0 as the linear layer's (absent) bias
+        dz[v][j] = dyv;
+        const float xh = col_ok(d, lane, v, j) ? (x.x[v][j] - mean) * rstd : 0.0f;
+        x.x[v][j] = xh;
+        const float dxh = dyv * g.x[v][j];
+        s1 += dxh;
+        s2 += dxh * xh;
+        pg[v][j] += dyv * xh;
+        pb[v][j] += dyv;
+      }
+    s1 = wave_sum(s1) / (float)d;
+    s2 = wave_sum(s2) / (float)d;
+    uint16_t h[VPL][8];
+#pragma unroll
+    for (int v = 0; v < VPL; ++v)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) h[v][j] = f2h<DT>(rstd * (dz[v][j] * g.x[v][j] - s1 - x.x[v][j] * s2));
+    store_row<DT, VPL>(dX + r * ldo, d, lane, h);
+  }
+  // the waves' column partials, combined in wave order through LDS
+  __shared__ float red[kHeadWaves][2][512];
+  float* out = part + (int64_t)blockIdx.x * 2 * d;
+#pragma unroll
+  for (int v = 0; v < VPL; ++v) {
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      red[wave][0][lane * 8 + j] = pg[v][j];
+      red[wave][1][lane * 8 + j] = pb[v][j];
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < 1024; i += 64 * kHeadWaves) {
+      const int which = i >> 9, c = i & 511;
+      const int64_t col = (int64_t)v * 512 + c;
+      if (col < d) {
+        float t = red[0][which][c];
+#pragma unroll
+        for (int w = 1; w < kHeadWaves; ++w) t += red[w][which][c];
+        out[which * d + col] = t;
+      }
+    }
+  }
+}
+
 // Squared errors of 2048-element blocks into part[block]; dY seeded with the scale.
 constexpr int kMseBlock = 2048;
 
@@ -684,6 +855,62 @@ extern "C" int mpx_cross_entropy(const void* Z, int64_t ldz, const int32_t* labe
   MPX_DT_DISPATCH(dt, cross_entropy_kernel, (unsigned)((B + 3) / 4), 256, stream, (const uint16_t*)Z, ldz,
                   labels, B, C, d_state, (float*)workspace, (uint16_t*)dZ);
   mean_kernel<<<1, 256, 0, (hipStream_t)stream>>>((const float*)workspace, B, d_loss);
+  MPX_LAUNCHED();
+  return MPX_OK;
+}
+
+static int64_t head_blocks(int64_t B) { return (B + kHeadWaves - 1) / kHeadWaves; }
+
+extern "C" size_t mpx_classifier_head_workspace(int64_t B, int64_t d) {
+  if (B < 1 || d < 1) return 0;
+  const int64_t loss = (B + 63) / 64 * 64;  // row losses, then the gamma / beta partials
+  return (size_t)(loss + head_blocks(B) * 2 * d) * sizeof(float);
+}
+
+extern "C" int mpx_classifier_head(const void* X, int64_t ldx, const void* gamma, const void* beta,
+                                   const void* W, const void* b, const int32_t* labels, int64_t B,
+                                   int64_t d, int64_t C, const mpx_scale_state* d_state, void* Z,
+                                   float* d_loss, void* dlogits, void* dX, int64_t ldo, void* dgamma,
+                                   void* dbeta, mpx_dtype dt, void* workspace, size_t ws_bytes,
+                                   void* stream) {
+  clear_error();
+  MPX_REQUIRE(X && gamma && beta && W && b && labels && d_state && Z && d_loss && dlogits && dX &&
+                  dgamma && dbeta,
+              "NULL argument");
+  MPX_REQUIRE(B >= 1 && d >= 1 && d <= 2048 && ldx >= d && ldo >= d, "bad sizes (1 <= d <= 2048)");
+  MPX_REQUIRE(C >= 1 && C <= 32, "C must be in [1, 32]");
+  MPX_REQUIRE(B <= 2048, "B must be <= 2048");
+  MPX_REQUIRE(C * d <= kHeadMaxW, "C * d must be <= 16384 (W is staged in 32 KiB of LDS)");
+  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  const size_t need = mpx_classifier_head_workspace(B, d);
+  if (!workspace || ws_bytes < need) {
+    set_error("mpx_classifier_head: workspace of " + std::to_string(need) + " bytes required");
+    return MPX_ERR_WORKSPACE;
+  }
+  float* rowloss = (float*)workspace;
+  float* part = rowloss + (B + 63) / 64 * 64;
+  const int64_t nb = head_blocks(B);
+  hipStream_t s = (hipStream_t)stream;
+#define MPX_HEAD(DTv, V)                                                                              \
+  classifier_head_kernel<DTv, V><<<(unsigned)nb, 64 * kHeadWaves, 0, s>>>(                           \
+      (const uint16_t*)X, ldx, (const uint16_t*)gamma, (const uint16_t*)beta, (const uint16_t*)W,   \
+      (const uint16_t*)b, labels, B, d, (int)C, d_state, (uint16_t*)Z, (uint16_t*)dlogits,          \
+      (uint16_t*)dX, ldo, rowloss, part)
+  const int vpl = vpl_for(d);
+  const unsigned fin = colsum_final_blocks(2 * d);
+  if (dt == MPX_F16) {
+    if (vpl == 1) MPX_HEAD(MPX_F16, 1);
+    else if (vpl == 2) MPX_HEAD(MPX_F16, 2);
+    else MPX_HEAD(MPX_F16, 4);
+    colsum_final_kernel<MPX_F16><<<fin, 256, 0, s>>>(part, (int)nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d);
+  } else {
+    if (vpl == 1) MPX_HEAD(MPX_BF16, 1);
+    else if (vpl == 2) MPX_HEAD(MPX_BF16, 2);
+    else MPX_HEAD(MPX_BF16, 4);
+    colsum_final_kernel<MPX_BF16><<<fin, 256, 0, s>>>(part, (int)nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d);
+  }
+#undef MPX_HEAD
+  mean_kernel<<<1, 256, 0, s>>>(rowloss, B, d_loss);
   MPX_LAUNCHED();
   return MPX_OK;
 }

@@ -353,7 +353,8 @@ class ViTStep(TrainStep):
         # workspaces: the main stream's (LayerNorm, loss, attention) and the
         # weight-gradient stream's (split-K partials, bias column sums)
         ws = max(mx.mpx_layernorm_bwd_workspace(M, d), mx.mpx_loss_workspace(B),
-                 mx.mpx_attention_bwd_workspace(B, T, H, cfg.head_dim))
+                 mx.mpx_attention_bwd_workspace(B, T, H, cfg.head_dim),
+                 mx.mpx_classifier_head_workspace(B, d))
         self.ws = torch.zeros(ws, dtype=torch.uint8, device=dev)
         ws2 = max(max(mx.mpx_linear_bwd_workspace(*s) for s in shapes),
                   mx.mpx_layernorm_bwd_workspace(M, d))
@@ -515,12 +516,25 @@ class ViTStep(TrainStep):
                               _ptr(blk["x1"]), _ptr(blk["x2"]), None, M, d, F, dt, NONE, s)
             x = blk["x2"]
         # ---- head: LN on the CLS rows, linear, cross-entropy seeded with the scale ----
-        mx.mpx_layernorm_fwd(_ptr(x), T * d, _ptr(W("lnf.g")), _ptr(W("lnf.b")), _ptr(self.zf),
-                             None, B, d, dt, s)
-        mx.mpx_linear_fwd(_ptr(self.zf), _ptr(W("head.w")), _ptr(W("head.b")), None,
-                          _ptr(self.logits), None, B, Cn, d, dt, NONE, s)
-        mx.mpx_cross_entropy(_ptr(self.logits), Cn, _ptr(self.labels), B, Cn, _ptr(self.d_state),
-                             _ptr(self.d_loss), _ptr(self.dlogits), dt, wsp, wsb, s)
+        # Up to 32 classes (C d <= 16384, 2048 rows) the head's forward and its backward
+        # down to the final LayerNorm's input are one pass per row, the same
+        # bits as the separate calls (three launches instead of seven on the
+        # critical path); its weight gradients follow below.
+        fused_head = Cn <= 32 and Cn * d <= 16384 and B <= 2048
+        if fused_head:
+            mx.mpx_classifier_head(_ptr(x), T * d, _ptr(W("lnf.g")), _ptr(W("lnf.b")),
+                                   _ptr(W("head.w")), _ptr(W("head.b")), _ptr(self.labels), B, d, Cn,
+                                   _ptr(self.d_state), _ptr(self.zf), _ptr(self.d_loss),
+                                   _ptr(self.dlogits), _ptr(self.dxf), T * d, _ptr(G("lnf.g")),
+                                   _ptr(G("lnf.b")), dt, wsp, wsb, s)
+        else:
+            mx.mpx_layernorm_fwd(_ptr(x), T * d, _ptr(W("lnf.g")), _ptr(W("lnf.b")), _ptr(self.zf),
+                                 None, B, d, dt, s)
+            mx.mpx_linear_fwd(_ptr(self.zf), _ptr(W("head.w")), _ptr(W("head.b")), None,
+                              _ptr(self.logits), None, B, Cn, d, dt, NONE, s)
+            mx.mpx_cross_entropy(_ptr(self.logits), Cn, _ptr(self.labels), B, Cn,
+                                 _ptr(self.d_state), _ptr(self.d_loss), _ptr(self.dlogits), dt, wsp,
+                                 wsb, s)
         # ---- backward ----
         # The critical path (dX of every layer, LayerNorm and attention
         # backward) runs on the step's stream; the weight and bias gradients
@@ -558,9 +572,10 @@ class ViTStep(TrainStep):
                               _ptr(dX), None, None, Mr, N, K, dt, None, 0, s)
 
         wgrad(self.zf, self.dlogits, G("head.w"), G("head.b"), B, Cn, d)
-        dgrad(W("head.w"), self.dlogits, None, NONE, self.dz, B, Cn, d)
+        if not fused_head:
+            dgrad(W("head.w"), self.dlogits, None, NONE, self.dz, B, Cn, d)
+            ln_bwd(x, T * d, W("lnf.g"), self.dz, None, self.dxf, T * d, G("lnf.g"), G("lnf.b"), B)
         dx = self.dxf
-        ln_bwd(x, T * d, W("lnf.g"), self.dz, None, dx, T * d, G("lnf.g"), G("lnf.b"), B)
         done = []  # side-stream completion of each block's weight gradients
         for k, i in enumerate(reversed(range(c.depth))):
             blk = self.blocks[i]

@@ -236,3 +236,65 @@ def test_patchify_embed_assemble_and_backward(fmt):
     rpos = pol.R(d3.astype(np.float64).sum(axis=0))
     assert_within(to_host(dpos), rpos, _sum_bound(d3.reshape(B, -1), fmt, rpos.reshape(-1)).reshape(T, d), "dpos")
     assert_same_values(to_host(dcls), to_host(dpos)[0], "dcls")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("B,T,d,C", [(128, 65, 384, 10), (5, 3, 100, 7), (33, 2, 512, 32),
+                                     (2, 1, 2048, 8)], ids=lambda v: str(v))
+def test_classifier_head_matches_separate_calls(fmt, B, T, d, C):
+    """The fused classifier head (final LayerNorm on the CLS rows, linear,
+    cross-entropy with the scaled seed, backward to the LayerNorm input and
+    gamma / beta) gives the bits of the separate calls, each of which is
+    checked against the oracle above."""
+    from paper_2507_03312_amd.train import pack_scale_state
+    dt = mx.DTYPES[fmt]
+    x = _rand((B * T, d), fmt, 21, 2.0, 0.5)
+    g, be = _rand((d,), fmt, 22, 0.2, 1.0), _rand((d,), fmt, 23, 0.2)
+    w, bias = _rand((C, d), fmt, 24, 0.05), _rand((C,), fmt, 25, 0.5)
+    y = np.random.default_rng(26).integers(0, C, B).astype(np.int32)
+    tx, tg, tb, tw, tbias = (to_dev_half(a, fmt) for a in (x, g, be, w, bias))
+    ty = torch.from_numpy(y).cuda()
+    st = torch.from_numpy(pack_scale_state(2.0 ** 15, 0, 10)).cuda()
+    ld = T * d
+
+    def outs():
+        return ([_empty((B, d), fmt), _empty((B, C), fmt), _empty((B * T, d), fmt), _empty((d,), fmt),
+                 _empty((d,), fmt)], torch.zeros(1, dtype=torch.float32, device="cuda"))
+
+    (z1, dl1, dx1, dg1, db1), loss1 = outs()
+    wsn = mx.mpx_classifier_head_workspace(B, d)
+    ws = torch.zeros(wsn, dtype=torch.uint8, device="cuda")
+    mx.mpx_classifier_head(tx.data_ptr(), ld, tg.data_ptr(), tb.data_ptr(), tw.data_ptr(),
+                           tbias.data_ptr(), ty.data_ptr(), B, d, C, st.data_ptr(), z1.data_ptr(),
+                           loss1.data_ptr(), dl1.data_ptr(), dx1.data_ptr(), ld, dg1.data_ptr(),
+                           db1.data_ptr(), dt, ws.data_ptr(), wsn, _s())
+
+    (z2, dl2, dx2, dg2, db2), loss2 = outs()
+    logits, dz = _empty((B, C), fmt), _empty((B, d), fmt)
+    ws2n = max(mx.mpx_loss_workspace(B), mx.mpx_layernorm_bwd_workspace(B, d))
+    ws2 = torch.zeros(ws2n, dtype=torch.uint8, device="cuda")
+    mx.mpx_layernorm_fwd(tx.data_ptr(), ld, tg.data_ptr(), tb.data_ptr(), z2.data_ptr(), None, B, d,
+                         dt, _s())
+    mx.mpx_linear_fwd(z2.data_ptr(), tw.data_ptr(), tbias.data_ptr(), None, logits.data_ptr(), None,
+                      B, C, d, dt, mx.MPX_ACT_NONE, _s())
+    mx.mpx_cross_entropy(logits.data_ptr(), C, ty.data_ptr(), B, C, st.data_ptr(), loss2.data_ptr(),
+                         dl2.data_ptr(), dt, ws2.data_ptr(), ws2n, _s())
+    mx.mpx_linear_bwd(None, tw.data_ptr(), dl2.data_ptr(), None, mx.MPX_ACT_NONE, dz.data_ptr(),
+                      None, None, B, C, d, dt, None, 0, _s())
+    mx.mpx_layernorm_bwd(tx.data_ptr(), ld, tg.data_ptr(), dz.data_ptr(), None, dx2.data_ptr(), ld,
+                         dg2.data_ptr(), db2.data_ptr(), B, d, dt, ws2.data_ptr(), ws2n, _s())
+    torch.cuda.synchronize()
+    for a, b_, what in ((z1, z2, "Z"), (dl1, dl2, "dlogits"), (dx1, dx2, "dX"), (dg1, dg2, "dgamma"),
+                        (db1, db2, "dbeta"), (loss1, loss2, "loss")):
+        assert torch.equal(a, b_), what
+
+
+def test_classifier_head_limits():
+    t = _empty((64, 64), "bf16")
+    p = t.data_ptr()
+    with pytest.raises(mx.MPXError, match="C must be"):
+        mx.mpx_classifier_head(p, 64, p, p, p, p, p, 4, 64, 33, p, p, p, p, p, 64, p, p, mx.MPX_BF16,
+                               p, 1 << 20, _s())
+    with pytest.raises(mx.MPXError, match="workspace"):
+        mx.mpx_classifier_head(p, 64, p, p, p, p, p, 4, 64, 10, p, p, p, p, p, 64, p, p, mx.MPX_BF16,
+                               p, 16, _s())
