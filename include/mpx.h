@@ -28,6 +28,17 @@
  *    message (per host thread).  Invalid arguments are detected before
  *    anything is launched.  Non-finite DATA is never an error: it is reported
  *    through the non-finite count (MPX §2.1: overflow makes the step skip).
+ *  - The calls that write parameter gradients (mpx_linear_bwd's dW and db,
+ *    mpx_layernorm_bwd's and mpx_classifier_head's dgamma and dbeta,
+ *    mpx_embed_assemble_bwd's dcls and dpos) take a nullable int32 device
+ *    counter d_nonfinite: when set, the number of those half results whose
+ *    exponent bits are all ones (+-inf or NaN) is ADDED to it atomically.
+ *    That is the finite check of MPX §3.4 done where the gradients are
+ *    written: a step that zeroes the counter (mpx_zero), passes it to every
+ *    gradient-writing call and then hands it to mpx_adamw_masked and
+ *    mpx_scale_update gets the same count as mpx_unscale_check over the
+ *    gradient list, without reading the gradients again.  Activation
+ *    cotangents (dX) are never counted.
  *  - The library keeps no state between calls except tensor-list objects
  *    (and their small device tables), which the caller creates and destroys.
  */
@@ -158,10 +169,12 @@ int mpx_linear_fwd(const void* X, const void* W, const void* b, const void* R, v
  * `workspace` (device, ws_bytes) holds split-K partial sums and column
  * partials; its required size is mpx_linear_bwd_workspace(M, N, K) when dW
  * or db is requested (a dX-only call needs none).  Concurrent calls need
- * separate workspaces. */
+ * separate workspaces.  d_nonfinite (nullable) counts non-finite dW and db
+ * elements (MPX §3.4's check, fused into the kernels that write them). */
 int mpx_linear_bwd(const void* X, const void* W, const void* dY, const void* Xpre,
                    int32_t x_act, void* dX, void* dW, void* db, int64_t M, int64_t N,
-                   int64_t K, mpx_dtype dt, void* workspace, size_t ws_bytes, void* stream);
+                   int64_t K, mpx_dtype dt, void* workspace, size_t ws_bytes,
+                   int32_t* d_nonfinite, void* stream);
 size_t mpx_linear_bwd_workspace(int64_t M, int64_t N, int64_t K);
 
 /* Batched half GEMM with float32 accumulation (attention QK^T, PV and their
@@ -236,11 +249,12 @@ int mpx_layernorm_fwd(const void* X, int64_t ldx, const void* gamma, const void*
  * half(column sums); their partial sums use `workspace` (float32,
  * mpx_layernorm_bwd_workspace bytes).  dX (NULL: skipped) and the pair
  * dgamma / dbeta (both NULL: skipped, no workspace needed) may be requested
- * in separate calls, e.g. on two streams; at least one must be given. */
+ * in separate calls, e.g. on two streams; at least one must be given.
+ * d_nonfinite (nullable) counts non-finite dgamma / dbeta elements. */
 int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, const void* dY,
                       const void* Rgrad, void* dX, int64_t ldo, void* dgamma, void* dbeta,
                       int64_t rows, int64_t d, mpx_dtype dt, void* workspace,
-                      size_t ws_bytes, void* stream);
+                      size_t ws_bytes, int32_t* d_nonfinite, void* stream);
 size_t mpx_layernorm_bwd_workspace(int64_t rows, int64_t d);
 
 /* Row softmax of scale * S (float32 math): P = half(softmax(scale * S)).
@@ -292,14 +306,16 @@ size_t mpx_classifier_head_workspace(int64_t B, int64_t d);
  * 1 <= d <= 2048, C * d <= 16384 (W is staged in on-chip memory), B <= 2048.  Every result is the same bits as the separate
  * calls give (same arithmetic, summation orders and roundings).  The weight
  * and bias gradients of the linear layer are left to mpx_linear_bwd (from Z
- * and dlogits).  A label outside [0, C) makes the loss NaN.  Errors:
+ * and dlogits).  d_nonfinite (nullable) counts non-finite dgamma / dbeta
+ * elements.  A label outside [0, C) makes the loss NaN.  Errors:
  * MPX_ERR_INVALID (NULL, sizes, C outside [1, 32], C * d > 16384, B > 2048),
  * MPX_ERR_WORKSPACE. */
 int mpx_classifier_head(const void* X, int64_t ldx, const void* gamma, const void* beta,
                         const void* W, const void* b, const int32_t* labels, int64_t B, int64_t d,
                         int64_t C, const mpx_scale_state* d_state, void* Z, float* d_loss,
                         void* dlogits, void* dX, int64_t ldo, void* dgamma, void* dbeta,
-                        mpx_dtype dt, void* workspace, size_t ws_bytes, void* stream);
+                        mpx_dtype dt, void* workspace, size_t ws_bytes, int32_t* d_nonfinite,
+                        void* stream);
 
 /* Mean squared error over n elements and its scaled cotangent:
  *   *d_loss = mean((y - t)^2);  dY = half(scale * 2 (y - t) / n). */
@@ -319,9 +335,11 @@ int mpx_embed_assemble(const void* E, const void* cls, const void* pos, void* X,
                        int64_t T, int64_t d, mpx_dtype dt, void* stream);
 
 /* Backward of mpx_embed_assemble: dE[b*G+g,:] = dX[b,1+g,:];
- * dcls = half(sum_b dX[b,0,:]); dpos[t,:] = half(sum_b dX[b,t,:]). */
+ * dcls = half(sum_b dX[b,0,:]); dpos[t,:] = half(sum_b dX[b,t,:]).
+ * d_nonfinite (nullable) counts non-finite dcls and dpos elements. */
 int mpx_embed_assemble_bwd(const void* dX, void* dE, void* dcls, void* dpos, int64_t B,
-                           int64_t T, int64_t d, mpx_dtype dt, void* stream);
+                           int64_t T, int64_t d, mpx_dtype dt, int32_t* d_nonfinite,
+                           void* stream);
 
 /* Row gather: dst[r, :] = src[r*stride_rows, :] for r < rows (d columns). */
 int mpx_gather_rows(const void* src, int64_t stride_rows, void* dst, int64_t rows, int64_t d,

@@ -58,7 +58,7 @@ _SIGS = {
     "mpx_scale_update": (C.c_int, [P, P, P]),
     "mpx_adamw_masked": (C.c_int, [P, P, P, P, I32, C.POINTER(AdamWHP), P, P, P, P, I32, P]),
     "mpx_linear_fwd": (C.c_int, [P, P, P, P, P, P, I64, I64, I64, I32, I32, P]),
-    "mpx_linear_bwd": (C.c_int, [P, P, P, P, I32, P, P, P, I64, I64, I64, I32, P, SZ, P]),
+    "mpx_linear_bwd": (C.c_int, [P, P, P, P, I32, P, P, P, I64, I64, I64, I32, P, SZ, P, P]),
     "mpx_linear_bwd_workspace": (SZ, [I64, I64, I64]),
     "mpx_gemm_batched": (C.c_int, [I32, I32, I64, I64, I64, I64, I64, P, I64, I64, I64, P, I64,
                                    I64, I64, P, I64, I64, I64, I32, P]),
@@ -67,7 +67,7 @@ _SIGS = {
     "mpx_attention_bwd": (C.c_int, [P, P, P, P, I64, I64, I64, I64, I32, P, SZ, P]),
     "mpx_attention_bwd_workspace": (SZ, [I64, I64, I64, I64]),
     "mpx_layernorm_fwd": (C.c_int, [P, I64, P, P, P, P, I64, I64, I32, P]),
-    "mpx_layernorm_bwd": (C.c_int, [P, I64, P, P, P, P, I64, P, P, I64, I64, I32, P, SZ, P]),
+    "mpx_layernorm_bwd": (C.c_int, [P, I64, P, P, P, P, I64, P, P, I64, I64, I32, P, SZ, P, P]),
     "mpx_layernorm_bwd_workspace": (SZ, [I64, I64]),
     "mpx_softmax_fwd": (C.c_int, [P, P, I64, I64, I64, F, I32, P]),
     "mpx_softmax_bwd": (C.c_int, [P, P, P, I64, I64, I64, F, I32, P]),
@@ -76,10 +76,10 @@ _SIGS = {
     "mpx_mse": (C.c_int, [P, P, I64, P, P, P, I32, P, SZ, P]),
     "mpx_classifier_head_workspace": (SZ, [I64, I64]),
     "mpx_classifier_head": (C.c_int, [P, I64, P, P, P, P, P, I64, I64, I64, P, P, P, P, P, I64, P, P,
-                                      I32, P, SZ, P]),
+                                      I32, P, SZ, P, P]),
     "mpx_patchify_cast": (C.c_int, [P, P, I64, I64, I64, I64, I64, I32, P]),
     "mpx_embed_assemble": (C.c_int, [P, P, P, P, I64, I64, I64, I32, P]),
-    "mpx_embed_assemble_bwd": (C.c_int, [P, P, P, P, I64, I64, I64, I32, P]),
+    "mpx_embed_assemble_bwd": (C.c_int, [P, P, P, P, I64, I64, I64, I32, P, P]),
     "mpx_gather_rows": (C.c_int, [P, I64, P, I64, I64, I32, P]),
     "mpx_zero": (C.c_int, [P, SZ, P]),
     "mpx_last_error": (C.c_char_p, []),

@@ -61,10 +61,12 @@ __global__ __launch_bounds__(256) void colsum_partial_kernel(const uint16_t* __r
 
 // Phase 2: out[col] = half(sum_s part[s][col]) over nparts slices, in slice
 // order within each of 4 interleaved lanes, lanes combined in lane order.
+// Non-finite results are added to *nonfinite when it is set.
 template <int DT>
 __global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restrict__ part, int nparts,
                                                            int64_t cols, uint16_t* __restrict__ out0,
-                                                           uint16_t* __restrict__ out1, int64_t split) {
+                                                           uint16_t* __restrict__ out1, int64_t split,
+                                                           int32_t* __restrict__ nonfinite) {
   // 32 columns per workgroup, 8 lanes per column: lane group q sums partials
   // q, q + 8, ... in order, then the 8 group sums are added pairwise in a
   // fixed tree
@@ -82,8 +84,10 @@ __global__ __launch_bounds__(256) void colsum_final_kernel(const float* __restri
     const float t = ((red[0][c] + red[1][c]) + (red[2][c] + red[3][c])) +
                     ((red[4][c] + red[5][c]) + (red[6][c] + red[7][c]));
     // columns [0, split) go to out0, [split, cols) to out1 (two results of one pass)
-    if (col < split) out0[col] = f2h<DT>(t);
-    else out1[col - split] = f2h<DT>(t);
+    const uint16_t h = f2h<DT>(t);
+    if (col < split) out0[col] = h;
+    else out1[col - split] = h;
+    if (nonfinite) add_nonfinite(nonfinite, h_nonfinite<DT>(h) ? 1 : 0);
   }
 }
 
@@ -100,10 +104,11 @@ inline size_t colsum_workspace(int64_t rows, int64_t cols) {
   return (size_t)colsum_slices(rows, cols) * cols * sizeof(float);
 }
 
-// out[col] = half(sum_r X[r, col]) for a dense half matrix.
+// out[col] = half(sum_r X[r, col]) for a dense half matrix; non-finite
+// results are added to *nonfinite when it is set.
 template <int DT>
 inline hipError_t colsum_run(const uint16_t* X, int64_t rows, int64_t cols, float* ws, uint16_t* out,
-                             hipStream_t s) {
+                             int32_t* nonfinite, hipStream_t s) {
   const int64_t sl = colsum_slices(rows, cols);
   const int64_t per = (rows + sl - 1) / sl;
   dim3 g1((unsigned)((cols + 255) / 256), (unsigned)sl);
@@ -113,7 +118,7 @@ inline hipError_t colsum_run(const uint16_t* X, int64_t rows, int64_t cols, floa
   else
     colsum_partial_kernel<DT, false><<<g1, 256, 0, s>>>(X, rows, cols, per, ws);
   colsum_final_kernel<DT><<<colsum_final_blocks(cols), 256, 0, s>>>(ws, (int)sl, cols, out, nullptr,
-                                                                       cols);
+                                                                       cols, nonfinite);
   return hipGetLastError();
 }
 

@@ -69,6 +69,24 @@ template <> __device__ __forceinline__ bool h_nonfinite<MPX_BF16>(uint16_t h) {
   return (h & 0x7F80u) == 0x7F80u;
 }
 
+// Number of +-inf / NaN values among the two halves packed in w, without
+// branches: a half whose exponent field is all ones, plus one unit of that
+// field, is exactly 0x8000 (bit 15 of its 16 bits); any other exponent stays
+// below it, and neither sum carries into the next half.
+template <int DT> __device__ __forceinline__ int nonfinite2(uint32_t w) {
+  constexpr uint32_t EXP = DT == MPX_F16 ? 0x7C007C00u : 0x7F807F80u;
+  constexpr uint32_t ONE = DT == MPX_F16 ? 0x04000400u : 0x00800080u;
+  return __builtin_popcount(((w & EXP) + ONE) & 0x80008000u);
+}
+
+// Adds a lane's count of non-finite results to the device counter *cnt (the
+// finite check fused into the kernels that write parameter gradients).  Only
+// lanes with something to add issue the (vector) atomic, so a pass whose
+// results are all finite leaves the counter untouched.
+__device__ __forceinline__ void add_nonfinite(int32_t* cnt, int n) {
+  if (n) atomicAdd(cnt, n);
+}
+
 // GELU, tanh form, and its derivative, in float32.  With
 // sigma = (1 + tanh(u)) / 2 = 1 / (1 + exp(-2u)), u = c (x + a x^3):
 //   gelu(x) = x sigma,  gelu'(x) = sigma + 2 x sigma (1 - sigma) c (1 + 3 a x^2).

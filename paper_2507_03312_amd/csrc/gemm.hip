@@ -73,7 +73,8 @@ extern "C" size_t mpx_linear_bwd_workspace(int64_t M, int64_t N, int64_t K) {
 
 extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, const void* Xpre,
                               int32_t x_act, void* dX, void* dW, void* db, int64_t M, int64_t N,
-                              int64_t K, mpx_dtype dt, void* workspace, size_t ws_bytes, void* stream) {
+                              int64_t K, mpx_dtype dt, void* workspace, size_t ws_bytes,
+                              int32_t* d_nonfinite, void* stream) {
   clear_error();
   MPX_REQUIRE(dY, "NULL dY");
   MPX_REQUIRE(dX || dW || db, "nothing to compute: dX, dW and db are all NULL");
@@ -110,6 +111,7 @@ extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, cons
     g.C = (uint16_t*)dW;
     g.M = N; g.N = K; g.K = M;
     g.lda = N; g.ldb = K; g.ldc = K;
+    g.nonfinite = d_nonfinite;
     const int sp = choose_splits(N, K, M);
     if (sp > 1) {
       g.splits = sp;
@@ -119,9 +121,11 @@ extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, cons
       MPX_HIP(gemm_dispatch(dt, g, false, false, 1, s));
       const int64_t MN = N * K;
       if (dt == MPX_F16)
-        splitk_reduce_kernel<MPX_F16><<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(g.ws, g.splits, MN, (uint16_t*)dW);
+        splitk_reduce_kernel<MPX_F16><<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(g.ws, g.splits, MN, (uint16_t*)dW,
+                                                                            d_nonfinite);
       else
-        splitk_reduce_kernel<MPX_BF16><<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(g.ws, g.splits, MN, (uint16_t*)dW);
+        splitk_reduce_kernel<MPX_BF16><<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(g.ws, g.splits, MN, (uint16_t*)dW,
+                                                                             d_nonfinite);
       MPX_LAUNCHED();
     } else {
       MPX_HIP(gemm_dispatch(dt, g, false, false, 1, s));
@@ -129,9 +133,11 @@ extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, cons
   }
   if (db) {
     if (dt == MPX_F16)
-      MPX_HIP(colsum_run<MPX_F16>((const uint16_t*)dY, M, N, (float*)workspace, (uint16_t*)db, s));
+      MPX_HIP(colsum_run<MPX_F16>((const uint16_t*)dY, M, N, (float*)workspace, (uint16_t*)db,
+                                           d_nonfinite, s));
     else
-      MPX_HIP(colsum_run<MPX_BF16>((const uint16_t*)dY, M, N, (float*)workspace, (uint16_t*)db, s));
+      MPX_HIP(colsum_run<MPX_BF16>((const uint16_t*)dY, M, N, (float*)workspace, (uint16_t*)db,
+                                            d_nonfinite, s));
   }
   return MPX_OK;
 }

@@ -50,6 +50,11 @@ struct GemmArgs {
   const uint16_t* dact;
   int32_t act;
   int32_t full_epi;  // set by the dispatcher: whole tiles may use gemm_epilogue_lds
+  // if set, the number of non-finite half outputs C is added to *nonfinite
+  // (split-K partials are counted by the reduction that rounds them
+  // instead); such calls take the generic epilogue or the whole-tile one
+  // compiled with EPI_COUNT
+  int32_t* nonfinite;
 };
 
 // Loader of one operand tile (ROWS output rows x BK reduction values) into
@@ -237,7 +242,10 @@ __device__ __forceinline__ void tile_origin(int64_t M, int64_t N, int64_t& m0, i
 // 8-byte aligned: no per-element masks, no runtime flag tests, one 64-bit
 // base per wave and 32-bit lane offsets.  The arithmetic is the generic
 // epilogue's, step for step, so both give identical bits.
-enum : int { EPI_BIAS = 1, EPI_GELU = 2, EPI_DACT = 4, EPI_RESID = 8, EPI_GENERIC = -1 };
+// EPI_COUNT: add the number of non-finite outputs to g.nonfinite (weight
+// gradients, which have no other epilogue operation)
+enum : int { EPI_BIAS = 1, EPI_GELU = 2, EPI_DACT = 4, EPI_RESID = 8, EPI_COUNT = 16,
+             EPI_GENERIC = -1 };
 
 // Whole-tile epilogue through LDS, for the transposed accumulator layout and
 // 32 x 64 or 64 x 64 wave tiles.  Step 1 (accumulator layout: lane = one row, runs of 4
@@ -292,6 +300,7 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, const f32x1
     return u32x4{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16),
                  h[4] | ((uint32_t)h[5] << 16), h[6] | ((uint32_t)h[7] << 16)};
   };
+  int bad = 0;
 #pragma unroll
   for (int t = 0; t < 4 * TM; ++t) {
     const int row = (lane >> 3) + 8 * t;
@@ -317,8 +326,13 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, const f32x1
 #pragma unroll
       for (int c = 0; c < 8; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) + h2f<DT>(rv[c]));
     }
-    *reinterpret_cast<u32x4*>(C + off) = p8(h);
+    const u32x4 o = p8(h);
+    if constexpr ((E & EPI_COUNT) != 0)  // no branch inside the store loop
+      bad += nonfinite2<DT>(o[0]) + nonfinite2<DT>(o[1]) + nonfinite2<DT>(o[2]) +
+             nonfinite2<DT>(o[3]);
+    *reinterpret_cast<u32x4*>(C + off) = o;
   }
+  if constexpr ((E & EPI_COUNT) != 0) add_nonfinite(g.nonfinite, bad);
 }
 
 // Generic epilogue shared by the GEMM kernels: any tile, any operand
@@ -397,6 +411,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const f32x16 (&
         if (c < nv) p[c] = d[c];
     }
   };
+  int bad = 0;
   static_for<TM>([&](auto i) {
     static_for<TN>([&](auto j) {
 #pragma unroll
@@ -422,10 +437,13 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& g, const f32x16 (&
           if (g.resid) o = f2h<DT>(h2f<DT>(o) + h2f<DT>(res[c]));
           h[c] = o;
         }
+#pragma unroll
+        for (int c = 0; c < 4; ++c) bad += (c < nv && h_nonfinite<DT>(h[c])) ? 1 : 0;
         st4(C + m * g.ldc + n, vec, nv, h);
       }
     });
   });
+  if (g.nonfinite) add_nonfinite(g.nonfinite, bad);
 }
 
 // OCC: waves per SIMD the register budget is sized for.
@@ -866,15 +884,19 @@ void gemm_dma_persistent_kernel(GemmArgs g) {
   }
 }
 
-// Sum of split-K partials in split order, one rounding: C = half(sum_s W[s]).
+// Sum of split-K partials in split order, one rounding: C = half(sum_s W[s]);
+// non-finite results are added to *nonfinite when it is set.
 template <int DT>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ ws, int splits,
-                                                            int64_t MN, uint16_t* __restrict__ C) {
+                                                            int64_t MN, uint16_t* __restrict__ C,
+                                                            int32_t* __restrict__ nonfinite) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= MN) return;
   float s = ws[i];
   for (int k = 1; k < splits; ++k) s += ws[(int64_t)k * MN + i];
-  C[i] = f2h<DT>(s);
+  const uint16_t h = f2h<DT>(s);
+  C[i] = h;
+  if (nonfinite) add_nonfinite(nonfinite, h_nonfinite<DT>(h) ? 1 : 0);
 }
 
 // ------------------------------------------------------------ dispatch --
@@ -939,7 +961,10 @@ static hipError_t launch_dma(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipSt
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   dim3 grid((unsigned)tiles, (unsigned)(g.splits > 1 ? g.splits : nbatch));
   g.full_epi = full_epilogue_ok(g, BM) ? 1 : 0;
-  const int e = g.full_epi ? epilogue_mask(g) : EPI_GENERIC;
+  // a call that counts non-finite outputs (weight gradients: both operands
+  // mn-major, no epilogue operation) has a whole-tile variant of its own;
+  // any other counting call takes the generic epilogue
+  const int e = g.full_epi ? epilogue_mask(g) | (g.nonfinite ? EPI_COUNT : 0) : EPI_GENERIC;
 #define MPX_D(AKv, BKv, Ev) gemm_dma_kernel<DT, BM, BN, WM, WN, S, OCC, AKv, BKv, Ev><<<grid, NT, 0, s>>>(g)
   if constexpr (BM == 64) {
     // 64 x 128 tiles (outputs too small to fill the CUs with 128 x 128): the
@@ -982,6 +1007,7 @@ static hipError_t launch_dma(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipSt
       else MPX_D(false, true, EPI_GENERIC);
     } else {
       if (e == 0) MPX_D(false, false, 0);
+      else if (e == EPI_COUNT) MPX_D(false, false, EPI_COUNT);
       else MPX_D(false, false, EPI_GENERIC);
     }
   } else {
@@ -1000,7 +1026,8 @@ static hipError_t launch_persistent(GemmArgs g, bool ak, bool bk, hipStream_t s)
   const int64_t tiles = ((g.M + BM - 1) / BM) * ((g.N + BN - 1) / BN);
   const unsigned grid = (unsigned)std::min<int64_t>(tiles, 256 * OCC);
   g.full_epi = full_epilogue_ok(g, BM) ? 1 : 0;
-  const int e = g.full_epi ? epilogue_mask(g) : EPI_GENERIC;
+  // a call that counts non-finite outputs takes the generic epilogue
+  const int e = g.full_epi && !g.nonfinite ? epilogue_mask(g) : EPI_GENERIC;
   if (!ak) return hipErrorInvalidValue;
 #define MPX_P(BKv, Ev) gemm_dma_persistent_kernel<DT, BM, BN, WM, WN, OCC, true, BKv, Ev><<<grid, NT, 0, s>>>(g)
   if (bk) {
@@ -1125,6 +1152,7 @@ __global__ __launch_bounds__(256) void gemm_small_kernel(GemmArgs g, bool ak, bo
   uint16_t h = f2h<DT>(acc + bias);
   if (g.resid) h = f2h<DT>(h2f<DT>(h) + h2f<DT>(g.resid[m * g.ldr + n]));
   g.C[m * g.ldc + n] = h;
+  if (g.nonfinite) add_nonfinite(g.nonfinite, h_nonfinite<DT>(h) ? 1 : 0);
 }
 
 static bool small_ok(const GemmArgs& g, int64_t nbatch) {

@@ -648,7 +648,8 @@ __global__ __launch_bounds__(256) void embed_assemble_bwd_kernel(const uint16_t*
                                                                  uint16_t* __restrict__ dE,
                                                                  uint16_t* __restrict__ dcls,
                                                                  uint16_t* __restrict__ dpos,
-                                                                 int64_t B, int64_t T, int64_t d) {
+                                                                 int64_t B, int64_t T, int64_t d,
+                                                                 int32_t* __restrict__ nonfinite) {
   const int64_t total = T * d;
   for (int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x; o < total; o += (int64_t)gridDim.x * 256) {
     const int64_t t = o / d, c = o % d;
@@ -661,6 +662,8 @@ __global__ __launch_bounds__(256) void embed_assemble_bwd_kernel(const uint16_t*
     const uint16_t h = f2h<DT>(s);
     dpos[o] = h;
     if (t == 0) dcls[c] = h;
+    // dpos and, for the CLS position, dcls: one or two parameter elements
+    if (nonfinite) add_nonfinite(nonfinite, h_nonfinite<DT>(h) ? (t == 0 ? 2 : 1) : 0);
   }
 }
 
@@ -749,7 +752,7 @@ extern "C" size_t mpx_layernorm_bwd_workspace(int64_t rows, int64_t d) {
 extern "C" int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, const void* dY,
                                  const void* Rgrad, void* dX, int64_t ldo, void* dgamma, void* dbeta,
                                  int64_t rows, int64_t d, mpx_dtype dt, void* workspace,
-                                 size_t ws_bytes, void* stream) {
+                                 size_t ws_bytes, int32_t* d_nonfinite, void* stream) {
   clear_error();
   MPX_REQUIRE(X && gamma && dY, "NULL X, gamma or dY");
   MPX_REQUIRE((dgamma == nullptr) == (dbeta == nullptr), "dgamma and dbeta go together");
@@ -772,12 +775,14 @@ extern "C" int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, 
     ln_bwd_launch<MPX_F16>(vpl_for(d), (unsigned)nb, s, (const uint16_t*)X, ldx, (const uint16_t*)gamma,
                            (const uint16_t*)dY, (const uint16_t*)Rgrad, (uint16_t*)dX, ldo, rows, d, part);
     if (part)
-      colsum_final_kernel<MPX_F16><<<fin, 256, 0, s>>>(part, nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d);
+      colsum_final_kernel<MPX_F16><<<fin, 256, 0, s>>>(part, nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d,
+                                                       d_nonfinite);
   } else {
     ln_bwd_launch<MPX_BF16>(vpl_for(d), (unsigned)nb, s, (const uint16_t*)X, ldx, (const uint16_t*)gamma,
                             (const uint16_t*)dY, (const uint16_t*)Rgrad, (uint16_t*)dX, ldo, rows, d, part);
     if (part)
-      colsum_final_kernel<MPX_BF16><<<fin, 256, 0, s>>>(part, nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d);
+      colsum_final_kernel<MPX_BF16><<<fin, 256, 0, s>>>(part, nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d,
+                                                        d_nonfinite);
   }
   MPX_LAUNCHED();
   return MPX_OK;
@@ -872,7 +877,7 @@ extern "C" int mpx_classifier_head(const void* X, int64_t ldx, const void* gamma
                                    int64_t d, int64_t C, const mpx_scale_state* d_state, void* Z,
                                    float* d_loss, void* dlogits, void* dX, int64_t ldo, void* dgamma,
                                    void* dbeta, mpx_dtype dt, void* workspace, size_t ws_bytes,
-                                   void* stream) {
+                                   int32_t* d_nonfinite, void* stream) {
   clear_error();
   MPX_REQUIRE(X && gamma && beta && W && b && labels && d_state && Z && d_loss && dlogits && dX &&
                   dgamma && dbeta,
@@ -902,12 +907,14 @@ extern "C" int mpx_classifier_head(const void* X, int64_t ldx, const void* gamma
     if (vpl == 1) MPX_HEAD(MPX_F16, 1);
     else if (vpl == 2) MPX_HEAD(MPX_F16, 2);
     else MPX_HEAD(MPX_F16, 4);
-    colsum_final_kernel<MPX_F16><<<fin, 256, 0, s>>>(part, (int)nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d);
+    colsum_final_kernel<MPX_F16><<<fin, 256, 0, s>>>(part, (int)nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d,
+                                                     d_nonfinite);
   } else {
     if (vpl == 1) MPX_HEAD(MPX_BF16, 1);
     else if (vpl == 2) MPX_HEAD(MPX_BF16, 2);
     else MPX_HEAD(MPX_BF16, 4);
-    colsum_final_kernel<MPX_BF16><<<fin, 256, 0, s>>>(part, (int)nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d);
+    colsum_final_kernel<MPX_BF16><<<fin, 256, 0, s>>>(part, (int)nb, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta, d,
+                                                      d_nonfinite);
   }
 #undef MPX_HEAD
   mean_kernel<<<1, 256, 0, s>>>(rowloss, B, d_loss);
@@ -958,13 +965,14 @@ extern "C" int mpx_embed_assemble(const void* E, const void* cls, const void* po
 }
 
 extern "C" int mpx_embed_assemble_bwd(const void* dX, void* dE, void* dcls, void* dpos, int64_t B,
-                                      int64_t T, int64_t d, mpx_dtype dt, void* stream) {
+                                      int64_t T, int64_t d, mpx_dtype dt, int32_t* d_nonfinite,
+                                      void* stream) {
   clear_error();
   MPX_REQUIRE(dX && dE && dcls && dpos, "NULL argument");
   MPX_REQUIRE(B >= 1 && T >= 2 && d >= 1, "bad sizes");
   MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
   MPX_DT_DISPATCH(dt, embed_assemble_bwd_kernel, grid_for(T * d), 256, stream, (const uint16_t*)dX,
-                  (uint16_t*)dE, (uint16_t*)dcls, (uint16_t*)dpos, B, T, d);
+                  (uint16_t*)dE, (uint16_t*)dcls, (uint16_t*)dpos, B, T, d, d_nonfinite);
   return MPX_OK;
 }
 

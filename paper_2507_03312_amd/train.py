@@ -129,6 +129,11 @@ class TrainStep:
         self.d_loss = torch.zeros(1, dtype=torch.float32, device=self.device)
         self.hp = mx.AdamWHP(cfg.lr, cfg.beta1, cfg.beta2, cfg.eps, cfg.weight_decay)
         self.half_copy_fresh = False
+        # MPX §3.4's finite check fused into the kernels that write the
+        # parameter gradients (they add their non-finite count to d_nonfinite,
+        # zeroed at the start of the step); False: a separate unscale/check
+        # pass over the whole gradient list after the backward
+        self.fused_check = True
         self.arena.load_masters(workloads.init_params(cfg))
 
     # ---- state access (harness only; each of these synchronises) ----
@@ -159,11 +164,18 @@ class TrainStep:
             self.cast_params()
         self._forward_backward(_stream())
 
+    def _nf(self):
+        """Counter argument of the gradient-writing calls."""
+        return _ptr(self.d_nonfinite) if self.fused_check else None
+
     def finish(self):
-        """Unscale + finite check, masked AdamW (+ half copy), scale update."""
+        """Finite check (unless fused into the backward), masked AdamW (+ half
+        copy), scale update."""
         s = _stream()
         a = self.arena
-        mx.mpx_unscale_check(a.L_g, self.dt, _ptr(self.d_state), _ptr(self.d_nonfinite), None, s)
+        if not self.fused_check:
+            mx.mpx_unscale_check(a.L_g, self.dt, _ptr(self.d_state), _ptr(self.d_nonfinite), None,
+                                 s)
         mx.mpx_adamw_masked(a.L_p, a.L_m, a.L_v, a.L_g, self.dt, self.hp, _ptr(self.d_step),
                             _ptr(self.d_state), _ptr(self.d_nonfinite), a.L_h, self.dt, s)
         mx.mpx_scale_update(_ptr(self.d_state), _ptr(self.d_nonfinite), s)
@@ -226,10 +238,18 @@ class TrainStep:
 
     def inject(self, tensor: int, element: int, value: float):
         """Harness fault injection: overwrite one gradient element (after the
-        backward pass, before the finite check)."""
+        backward pass, before the finite check).  With the fused check the
+        element is written after the kernels that count, so the count is
+        adjusted here as they would have: +1 when a finite element becomes
+        inf / NaN, -1 the other way round."""
         name = self.arena.names[tensor]
         flat = self.arena.gr(name).reshape(-1)
-        flat[element % flat.numel()] = value
+        i = element % flat.numel()
+        was = bool(torch.isfinite(flat[i]).item())
+        flat[i] = value
+        now = bool(torch.isfinite(flat[i]).item())
+        if self.fused_check and was != now:
+            self.d_nonfinite += 1 if was else -1
 
 
 def _linear_gelu_bytes(M: int, N: int, K: int) -> int:
@@ -283,6 +303,9 @@ class MLPStep(TrainStep):
     def _forward_backward(self, s):
         c, a, dt = self.cfg, self.arena, self.dt
         B, D, Dh = c.batch, c.d_in, c.d_hidden
+        nf = self._nf()
+        if nf:
+            mx.mpx_zero(nf, 4, s)
         mx.mpx_cast_to_half(self.L_in, self.L_in16, dt, s)
         self._dominant_call(s)
         mx.mpx_linear_fwd(_ptr(self.hid), _ptr(a.w("fc2.w")), _ptr(a.w("fc2.b")), None,
@@ -292,10 +315,10 @@ class MLPStep(TrainStep):
         wsb = self.ws.numel()
         mx.mpx_linear_bwd(_ptr(self.hid), _ptr(a.w("fc2.w")), _ptr(self.dy), _ptr(self.h_pre),
                           mx.MPX_ACT_GELU_TANH, _ptr(self.dh_pre), _ptr(a.gr("fc2.w")),
-                          _ptr(a.gr("fc2.b")), B, D, Dh, dt, _ptr(self.ws), wsb, s)
+                          _ptr(a.gr("fc2.b")), B, D, Dh, dt, _ptr(self.ws), wsb, nf, s)
         mx.mpx_linear_bwd(_ptr(self.x16), _ptr(a.w("fc1.w")), _ptr(self.dh_pre), None,
                           mx.MPX_ACT_NONE, None, _ptr(a.gr("fc1.w")), _ptr(a.gr("fc1.b")),
-                          B, Dh, D, dt, _ptr(self.ws), wsb, s)
+                          B, Dh, D, dt, _ptr(self.ws), wsb, nf, s)
 
 
 class ViTStep(TrainStep):
@@ -386,10 +409,10 @@ class ViTStep(TrainStep):
             if dX is not None:
                 sites.append((name + ".dX", Mr, N, K, lambda s: mx.mpx_linear_bwd(
                     None, _ptr(w), _ptr(dY), _ptr(Xpre), x_act, _ptr(dX), None, None, Mr, N, K, dt,
-                    None, 0, s)))
+                    None, 0, None, s)))
             sites.append((name + ".dW", Mr, N, K, lambda s: mx.mpx_linear_bwd(
                 _ptr(X), None, _ptr(dY), None, NONE, None, _ptr(gw), _ptr(gb), Mr, N, K, dt,
-                ws2p, ws2b, s)))
+                ws2p, ws2b, None, s)))
 
         dx, du_pre, dx1, dqkv = self.dx[0], self.du_pre[0], self.dx1[0], self.dqkv[0]
         if c.image:
@@ -487,6 +510,16 @@ class ViTStep(TrainStep):
         W, G = a.w, a.gr
         wsp, wsb = _ptr(self.ws), self.ws.numel()
         GELU, NONE = mx.MPX_ACT_GELU_TANH, mx.MPX_ACT_NONE
+        main = torch.cuda.current_stream()
+        side, sh = self.side, self.side.cuda_stream
+        nf = self._nf()
+        if nf:
+            # zeroed first on the step's stream: every gradient-writing call
+            # below is ordered after it (zeroed on the second stream beside
+            # the forward instead, the one-block step measured 1% slower than
+            # with the separate check pass: the cross-stream wait cost more
+            # than this launch)
+            mx.mpx_zero(nf, 4, s)
         # ---- inputs (MPX §3.4: cast inputs to half) and embedding ----
         if c.image:
             mx.mpx_patchify_cast(_ptr(self.img), _ptr(self.patches), B, c.image, c.image,
@@ -526,7 +559,7 @@ class ViTStep(TrainStep):
                                    _ptr(W("head.w")), _ptr(W("head.b")), _ptr(self.labels), B, d, Cn,
                                    _ptr(self.d_state), _ptr(self.zf), _ptr(self.d_loss),
                                    _ptr(self.dlogits), _ptr(self.dxf), T * d, _ptr(G("lnf.g")),
-                                   _ptr(G("lnf.b")), dt, wsp, wsb, s)
+                                   _ptr(G("lnf.b")), dt, wsp, wsb, nf, s)
         else:
             mx.mpx_layernorm_fwd(_ptr(x), T * d, _ptr(W("lnf.g")), _ptr(W("lnf.b")), _ptr(self.zf),
                                  None, B, d, dt, s)
@@ -540,14 +573,12 @@ class ViTStep(TrainStep):
         # backward) runs on the step's stream; the weight and bias gradients
         # of each linear layer, which nothing later in the backward reads, run
         # on a second stream forked at the point their cotangent is ready.
-        main = torch.cuda.current_stream()
-        side, sh = self.side, self.side.cuda_stream
         ws2p, ws2b = _ptr(self.ws2), self.ws2.numel()
 
         def wgrad(X, dY, dW, db, Mr, N, K):
             side.wait_stream(main)
             mx.mpx_linear_bwd(_ptr(X), None, _ptr(dY), None, NONE, None, _ptr(dW), _ptr(db),
-                              Mr, N, K, dt, ws2p, ws2b, sh)
+                              Mr, N, K, dt, ws2p, ws2b, nf, sh)
 
         # LayerNorm backward: with more than one block, dX alone on the step's
         # stream and gamma / beta (re-reading X and dY) on the second stream,
@@ -559,17 +590,17 @@ class ViTStep(TrainStep):
         def ln_bwd(X, ldx, g, dY, R, dX, ldo, gg, gb, rows, fused=False):
             if fused or not side_ln:
                 mx.mpx_layernorm_bwd(_ptr(X), ldx, _ptr(g), _ptr(dY), _ptr(R), _ptr(dX), ldo,
-                                     _ptr(gg), _ptr(gb), rows, d, dt, wsp, wsb, s)
+                                     _ptr(gg), _ptr(gb), rows, d, dt, wsp, wsb, nf, s)
                 return
             mx.mpx_layernorm_bwd(_ptr(X), ldx, _ptr(g), _ptr(dY), _ptr(R), _ptr(dX), ldo, None, None,
-                                 rows, d, dt, None, 0, s)
+                                 rows, d, dt, None, 0, None, s)
             side.wait_stream(main)
             mx.mpx_layernorm_bwd(_ptr(X), ldx, _ptr(g), _ptr(dY), None, None, d, _ptr(gg), _ptr(gb),
-                                 rows, d, dt, ws2p, ws2b, sh)
+                                 rows, d, dt, ws2p, ws2b, nf, sh)
 
         def dgrad(W_, dY, Xpre, act, dX, Mr, N, K):
             mx.mpx_linear_bwd(None, _ptr(W_), _ptr(dY), None if Xpre is None else _ptr(Xpre), act,
-                              _ptr(dX), None, None, Mr, N, K, dt, None, 0, s)
+                              _ptr(dX), None, None, Mr, N, K, dt, None, 0, None, s)
 
         wgrad(self.zf, self.dlogits, G("head.w"), G("head.b"), B, Cn, d)
         if not fused_head:
@@ -606,7 +637,7 @@ class ViTStep(TrainStep):
             dx = dx_out
         if c.image:
             mx.mpx_embed_assemble_bwd(_ptr(dx), _ptr(self.dE), _ptr(G("cls")), _ptr(G("pos")),
-                                      B, T, d, dt, s)
+                                      B, T, d, dt, nf, s)
             wgrad(self.patches, self.dE, G("patch.w"), G("patch.b"), B * c.n_patches, d,
                   c.patch_dim)
         main.wait_stream(side)  # join: the optimizer reads every gradient

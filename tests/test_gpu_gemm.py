@@ -101,7 +101,7 @@ def test_linear_bwd(fmt, mnk):
     dt = mx.DTYPES[fmt]
     mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), None, mx.MPX_ACT_NONE,
                       gdx.data_ptr(), gdw.data_ptr(), gdb.data_ptr(), M, N, K, dt,
-                      ws.data_ptr(), ws_n, _s())
+                      ws.data_ptr(), ws_n, None, _s())
     rdx, rdw, rdb = ops.linear_bwd(pol, x, w, dy)
     assert_within(to_host(gdx), rdx, gemm_bound(dy, w, rdx, fmt, N), "dX")
     assert_within(to_host(gdw), rdw, gemm_bound(dy.T, x, rdw, fmt, M), "dW")
@@ -110,7 +110,7 @@ def test_linear_bwd(fmt, mnk):
     # dX through GELU': half(half(dY W) * gelu'(Xpre))
     mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), txp.data_ptr(),
                       mx.MPX_ACT_GELU_TANH, gdx.data_ptr(), gdw.data_ptr(), None, M, N, K, dt,
-                      ws.data_ptr(), ws_n, _s())
+                      ws.data_ptr(), ws_n, None, _s())
     got = to_host(gdx)
     ref = ops.gelu_bwd(pol, xpre, rdx)
     # GPU's own dX may differ from rdx by the GEMM bound, scaled by |gelu'| <= 1.13
@@ -118,12 +118,48 @@ def test_linear_bwd(fmt, mnk):
     assert_within(got, ref, bound, "dX through gelu'")
 
 
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("mnk", [(4096, 384, 384), (256, 256, 256), (70, 100, 72), (128, 10, 384),
+                                 (2500, 96, 40), (33, 17, 50)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_linear_bwd_counts_nonfinite(fmt, mnk):
+    """MPX §3.4's finite check fused into the kernels that write dW and db
+    (split-K reduction, both GEMM epilogues, the skinny-product kernel, the
+    column sum): the count they add equals the separate check's count over
+    [dW, db], dX is never counted, and a second call adds to the counter."""
+    M, N, K = mnk
+    x = _rand((M, K), fmt, 21)
+    w = _rand((N, K), fmt, 22, 0.05)
+    dy = _rand((M, N), fmt, 23)
+    big = 60000.0 if fmt == "f16" else 3.0e38  # finite, but dW and db overflow in places
+    dy[0, ::2] = big
+    dy[min(1, M - 1), :] = big / 2
+    dy = round_to(dy, fmt)
+    tx, tw, tdy = (to_dev_half(a, fmt) for a in (x, w, dy))
+    gdx, gdw, gdb = _empty((M, K), fmt), _empty((N, K), fmt), _empty((N,), fmt)
+    ws_n = mx.mpx_linear_bwd_workspace(M, N, K)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    dt = mx.DTYPES[fmt]
+    nf = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ref = torch.zeros(1, dtype=torch.int32, device="cuda")
+    mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), None, mx.MPX_ACT_NONE,
+                      gdx.data_ptr(), gdw.data_ptr(), gdb.data_ptr(), M, N, K, dt,
+                      ws.data_ptr(), ws_n, nf.data_ptr(), _s())
+    mx.mpx_unscale_check(mx.TensorList([gdw, gdb]), dt, 0, ref.data_ptr(), None, _s())
+    count, want = int(nf.item()), int(ref.item())
+    assert count == want and 0 < want < N * K + N, (count, want)
+    mx.mpx_linear_bwd(tx.data_ptr(), None, tdy.data_ptr(), None, mx.MPX_ACT_NONE, None,
+                      gdw.data_ptr(), gdb.data_ptr(), M, N, K, dt, ws.data_ptr(), ws_n,
+                      nf.data_ptr(), _s())
+    assert int(nf.item()) == 2 * want
+
+
 def test_linear_bwd_workspace_is_checked():
     M, N, K = 256, 256, 256
     t = _empty((M, K), "f16")
     with pytest.raises(mx.MPXError, match="workspace"):
         mx.mpx_linear_bwd(t.data_ptr(), t.data_ptr(), t.data_ptr(), None, 0, t.data_ptr(),
-                          t.data_ptr(), None, M, N, K, mx.MPX_F16, None, 0, _s())
+                          t.data_ptr(), None, M, N, K, mx.MPX_F16, None, 0, None, _s())
 
 
 def test_invalid_arguments_raise_before_launch():
@@ -207,7 +243,7 @@ def test_full_size_linear_sampled(fmt, mnk):
     ws_n = mx.mpx_linear_bwd_workspace(M, N, K)
     ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
     mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), None, 0, gdx.data_ptr(),
-                      gdw.data_ptr(), gdb.data_ptr(), M, N, K, dt, ws.data_ptr(), ws_n, _s())
+                      gdw.data_ptr(), gdb.data_ptr(), M, N, K, dt, ws.data_ptr(), ws_n, None, _s())
     rows = np.unique(rng.integers(0, M, 48))
     cols = np.unique(rng.integers(0, N, 48))
     ref = pol.gemm(x[rows], w[cols].T)
@@ -259,7 +295,7 @@ def test_every_tile_config(gemm_config, fmt):
     ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
     mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), txp.data_ptr(),
                       mx.MPX_ACT_GELU_TANH, gdx.data_ptr(), gdw.data_ptr(), None, M, N, K, dt,
-                      ws.data_ptr(), ws_n, _s())
+                      ws.data_ptr(), ws_n, None, _s())
     rdx, rdw, _ = ops.linear_bwd(pol, x, w, dy)
     assert_within(to_host(gdw), rdw, gemm_bound(dy.T, x, rdw, fmt, M), "dW")
     ref = ops.gelu_bwd(pol, xpre, rdx)
@@ -313,7 +349,7 @@ def test_persistent_configs_walk_many_tiles(fmt, persistent, plain):
                               pre.data_ptr(), M, N, K, dt, mx.MPX_ACT_GELU_TANH, _s())
             mx.mpx_linear_bwd(None, tw.data_ptr(), tdy.data_ptr(), txp.data_ptr(),
                               mx.MPX_ACT_GELU_TANH, gdx.data_ptr(), None, None, M, N, K, dt,
-                              None, 0, _s())
+                              None, 0, None, _s())
             torch.cuda.synchronize()
             out[cfg] = (y, pre, gdx)
     finally:
@@ -352,7 +388,7 @@ def test_skinny_path_forced(fmt):
             ws_n = mx.mpx_linear_bwd_workspace(M, N, K)
             ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
             mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), None, mx.MPX_ACT_NONE,
-                              gdx.data_ptr(), gdw.data_ptr(), None, M, N, K, dt, ws.data_ptr(), ws_n,
+                              gdx.data_ptr(), gdw.data_ptr(), None, M, N, K, dt, ws.data_ptr(), ws_n, None,
                               _s())
             rdx, rdw, _ = ops.linear_bwd(pol, x, w, dy)
             assert_within(to_host(gdx), rdx, gemm_bound(dy, w, rdx, fmt, N), f"dX {M}x{N}x{K}")
@@ -376,16 +412,16 @@ def test_linear_bwd_subsets_match_full_call(fmt):
     ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
     mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), txp.data_ptr(),
                       mx.MPX_ACT_GELU_TANH, *(t.data_ptr() for t in full), M, N, K, dt,
-                      ws.data_ptr(), ws_n, _s())
+                      ws.data_ptr(), ws_n, None, _s())
     mx.mpx_linear_bwd(None, tw.data_ptr(), tdy.data_ptr(), txp.data_ptr(), mx.MPX_ACT_GELU_TANH,
-                      part[0].data_ptr(), None, None, M, N, K, dt, None, 0, _s())
+                      part[0].data_ptr(), None, None, M, N, K, dt, None, 0, None, _s())
     mx.mpx_linear_bwd(tx.data_ptr(), None, tdy.data_ptr(), None, mx.MPX_ACT_NONE, None,
-                      part[1].data_ptr(), part[2].data_ptr(), M, N, K, dt, ws.data_ptr(), ws_n, _s())
+                      part[1].data_ptr(), part[2].data_ptr(), M, N, K, dt, ws.data_ptr(), ws_n, None, _s())
     for f, q, what in zip(full, part, ("dX", "dW", "db")):
         assert torch.equal(f, q), what
     with pytest.raises(mx.MPXError, match="nothing to compute"):
         mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), None, 0, None, None, None,
-                          M, N, K, dt, ws.data_ptr(), ws_n, _s())
+                          M, N, K, dt, ws.data_ptr(), ws_n, None, _s())
     with pytest.raises(mx.MPXError, match="workspace"):
         mx.mpx_linear_bwd(tx.data_ptr(), None, tdy.data_ptr(), None, 0, None, part[1].data_ptr(),
-                          None, M, N, K, dt, None, 0, _s())
+                          None, M, N, K, dt, None, 0, None, _s())

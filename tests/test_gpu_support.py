@@ -66,7 +66,7 @@ def test_layernorm_fwd_bwd(fmt, rows, d):
     ws = torch.zeros(wsn, dtype=torch.uint8, device="cuda")
     mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), trg.data_ptr(),
                          dx.data_ptr(), d, dg.data_ptr(), db.data_ptr(), rows, d, dt,
-                         ws.data_ptr(), wsn, _s())
+                         ws.data_ptr(), wsn, None, _s())
     rdx, rdg, rdb = ops.layernorm_bwd(pol, x, g, dy)
     rtot = ops.add(pol, rg, rdx)
     assert_within(to_host(dx), rtot, 2 * ulp(rtot, fmt) + ulp(rdx, fmt) + 1e-4 * np.abs(rdx), "LN dX")
@@ -91,19 +91,19 @@ def test_layernorm_bwd_subsets_match_full_call(fmt):
     ws = torch.zeros(wsn, dtype=torch.uint8, device="cuda")
     mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), trg.data_ptr(),
                          full[0].data_ptr(), d, full[1].data_ptr(), full[2].data_ptr(), rows, d, dt,
-                         ws.data_ptr(), wsn, _s())
+                         ws.data_ptr(), wsn, None, _s())
     mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), trg.data_ptr(),
-                         part[0].data_ptr(), d, None, None, rows, d, dt, None, 0, _s())
+                         part[0].data_ptr(), d, None, None, rows, d, dt, None, 0, None, _s())
     mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), None, None, d,
-                         part[1].data_ptr(), part[2].data_ptr(), rows, d, dt, ws.data_ptr(), wsn, _s())
+                         part[1].data_ptr(), part[2].data_ptr(), rows, d, dt, ws.data_ptr(), wsn, None, _s())
     for f, q, what in zip(full, part, ("dX", "dgamma", "dbeta")):
         assert torch.equal(f, q), what
     with pytest.raises(mx.MPXError, match="nothing to compute"):
         mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), None, None, d, None,
-                             None, rows, d, dt, None, 0, _s())
+                             None, rows, d, dt, None, 0, None, _s())
     with pytest.raises(mx.MPXError, match="together"):
         mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), None, None, d,
-                             part[1].data_ptr(), None, rows, d, dt, ws.data_ptr(), wsn, _s())
+                             part[1].data_ptr(), None, rows, d, dt, ws.data_ptr(), wsn, None, _s())
 
 
 def test_layernorm_strided_rows_cls_pooling():
@@ -126,7 +126,7 @@ def test_layernorm_strided_rows_cls_pooling():
     wsn = mx.mpx_layernorm_bwd_workspace(B, d)
     ws = torch.zeros(wsn, dtype=torch.uint8, device="cuda")
     mx.mpx_layernorm_bwd(tx.data_ptr(), T * d, tg.data_ptr(), tdz.data_ptr(), None, dx.data_ptr(),
-                         T * d, dg.data_ptr(), db.data_ptr(), B, d, mx.MPX_BF16, ws.data_ptr(), wsn, _s())
+                         T * d, dg.data_ptr(), db.data_ptr(), B, d, mx.MPX_BF16, ws.data_ptr(), wsn, None, _s())
     got = to_host(dx).reshape(B, T, d)
     rdx, _, _ = ops.layernorm_bwd(pol, x[:, 0, :], g, dz)
     assert_within(got[:, 0, :], rdx, ulp(rdx, fmt) + 1e-4 * np.abs(rdx), "LN dX CLS rows")
@@ -230,7 +230,7 @@ def test_patchify_embed_assemble_and_backward(fmt):
     tdX = to_dev_half(dX, fmt)
     dE, dcls, dpos = _empty((B * G, d), fmt), _empty((d,), fmt), _empty((T, d), fmt)
     mx.mpx_embed_assemble_bwd(tdX.data_ptr(), dE.data_ptr(), dcls.data_ptr(), dpos.data_ptr(), B,
-                              T, d, mx.DTYPES[fmt], _s())
+                              T, d, mx.DTYPES[fmt], None, _s())
     d3 = dX.reshape(B, T, d)
     assert_same_values(to_host(dE), d3[:, 1:].reshape(B * G, d), "dE")
     rpos = pol.R(d3.astype(np.float64).sum(axis=0))
@@ -267,7 +267,7 @@ def test_classifier_head_matches_separate_calls(fmt, B, T, d, C):
     mx.mpx_classifier_head(tx.data_ptr(), ld, tg.data_ptr(), tb.data_ptr(), tw.data_ptr(),
                            tbias.data_ptr(), ty.data_ptr(), B, d, C, st.data_ptr(), z1.data_ptr(),
                            loss1.data_ptr(), dl1.data_ptr(), dx1.data_ptr(), ld, dg1.data_ptr(),
-                           db1.data_ptr(), dt, ws.data_ptr(), wsn, _s())
+                           db1.data_ptr(), dt, ws.data_ptr(), wsn, None, _s())
 
     (z2, dl2, dx2, dg2, db2), loss2 = outs()
     logits, dz = _empty((B, C), fmt), _empty((B, d), fmt)
@@ -280,9 +280,9 @@ def test_classifier_head_matches_separate_calls(fmt, B, T, d, C):
     mx.mpx_cross_entropy(logits.data_ptr(), C, ty.data_ptr(), B, C, st.data_ptr(), loss2.data_ptr(),
                          dl2.data_ptr(), dt, ws2.data_ptr(), ws2n, _s())
     mx.mpx_linear_bwd(None, tw.data_ptr(), dl2.data_ptr(), None, mx.MPX_ACT_NONE, dz.data_ptr(),
-                      None, None, B, C, d, dt, None, 0, _s())
+                      None, None, B, C, d, dt, None, 0, None, _s())
     mx.mpx_layernorm_bwd(tx.data_ptr(), ld, tg.data_ptr(), dz.data_ptr(), None, dx2.data_ptr(), ld,
-                         dg2.data_ptr(), db2.data_ptr(), B, d, dt, ws2.data_ptr(), ws2n, _s())
+                         dg2.data_ptr(), db2.data_ptr(), B, d, dt, ws2.data_ptr(), ws2n, None, _s())
     torch.cuda.synchronize()
     for a, b_, what in ((z1, z2, "Z"), (dl1, dl2, "dlogits"), (dx1, dx2, "dX"), (dg1, dg2, "dgamma"),
                         (db1, db2, "dbeta"), (loss1, loss2, "loss")):
@@ -294,7 +294,7 @@ def test_classifier_head_limits():
     p = t.data_ptr()
     with pytest.raises(mx.MPXError, match="C must be"):
         mx.mpx_classifier_head(p, 64, p, p, p, p, p, 4, 64, 33, p, p, p, p, p, 64, p, p, mx.MPX_BF16,
-                               p, 1 << 20, _s())
+                               p, 1 << 20, None, _s())
     with pytest.raises(mx.MPXError, match="workspace"):
         mx.mpx_classifier_head(p, 64, p, p, p, p, p, 4, 64, 10, p, p, p, p, p, 64, p, p, mx.MPX_BF16,
-                               p, 16, _s())
+                               p, 16, None, _s())

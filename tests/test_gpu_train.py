@@ -158,3 +158,42 @@ def test_graph_replay_matches_eager(name):
             assert np.array_equal(a, b)
         for a, b in zip(eager.grads(), graphed.grads()):
             assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("name,scale,overflows", [("mlp", 2.0 ** 30, True),
+                                                  ("mlp", 2.0 ** 27, False),
+                                                  ("vit_s", 2.0 ** 26, True),
+                                                  ("vit_block", 2.0 ** 127, False)])
+def test_fused_check_matches_separate_pass(name, scale, overflows):
+    """MPX §3.4's finite check done by the kernels that write the parameter
+    gradients gives the same count as the separate pass over the gradient
+    list, and so the same steps: the loss scale is set high enough that the
+    scaled backward overflows in half precision (inf and NaN in many or in a
+    few gradient elements) or is close to it, then halves after each
+    overflow.  Both sides' gradients, masters and scale states stay equal."""
+    import dataclasses
+    cfg = workloads.get(name)
+    if cfg.kind == "vit":
+        cfg = workloads.scaled_down(cfg, batch=4, depth=2) if name == "vit_s" else \
+            workloads.scaled_down(cfg, batch=8)
+    cfg = dataclasses.replace(cfg, scale_init=scale)
+    batch = workloads.make_batch(cfg)
+    fused, sep = make_step(cfg), make_step(cfg)
+    sep.fused_check = False
+    fused.set_batch(batch)
+    sep.set_batch(batch)
+    counts = []
+    for s in range(6):
+        fused.forward_backward()
+        sep.forward_backward()
+        fused.finish()
+        sep.finish()
+        counts.append(sep.nonfinite())
+        assert fused.nonfinite() == sep.nonfinite(), (s, fused.nonfinite(), sep.nonfinite())
+        assert fused.scale_state() == sep.scale_state()
+        for a, b in zip(fused.grads(), sep.grads()):
+            assert np.array_equal(a, b, equal_nan=True)
+        for a, b in zip(fused.masters(), sep.masters()):
+            assert np.array_equal(a, b)
+    if overflows:  # fp16 with these scales: the first step overflows for certain
+        assert counts[0] > 0
