@@ -152,7 +152,11 @@ enum { MPX_ACT_NONE = 0, MPX_ACT_GELU_TANH = 1 };
  *   act == MPX_ACT_NONE:      out = pre
  *   act == MPX_ACT_GELU_TANH: Ypre = pre (required), out = half(gelu(pre))
  *   Y = R ? half(out + R) : out
- * M, N, K >= 1.  Rows are dense (leading dimension = row length). */
+ * M, N, K >= 1.  Rows are dense (leading dimension = row length).
+ * dt == MPX_F32 is full-precision training (MPX's use_mixed_precision
+ * switched off, the baseline of §4): every operand and result is float32,
+ * the products run on the float32 matrix cores and half() above is the
+ * identity. */
 int mpx_linear_fwd(const void* X, const void* W, const void* b, const void* R, void* Y,
                    void* Ypre, int64_t M, int64_t N, int64_t K, mpx_dtype dt, int32_t act,
                    void* stream);
@@ -170,7 +174,9 @@ int mpx_linear_fwd(const void* X, const void* W, const void* b, const void* R, v
  * partials; its required size is mpx_linear_bwd_workspace(M, N, K) when dW
  * or db is requested (a dX-only call needs none).  Concurrent calls need
  * separate workspaces.  d_nonfinite (nullable) counts non-finite dW and db
- * elements (MPX §3.4's check, fused into the kernels that write them). */
+ * elements (MPX §3.4's check, fused into the kernels that write them).
+ * dt == MPX_F32: the same products in float32 (full precision, see
+ * mpx_linear_fwd; the workspace size is the same); d_nonfinite must be NULL. */
 int mpx_linear_bwd(const void* X, const void* W, const void* dY, const void* Xpre,
                    int32_t x_act, void* dX, void* dW, void* db, int64_t M, int64_t N,
                    int64_t K, mpx_dtype dt, void* workspace, size_t ws_bytes,
@@ -318,7 +324,9 @@ int mpx_classifier_head(const void* X, int64_t ldx, const void* gamma, const voi
                         void* stream);
 
 /* Mean squared error over n elements and its scaled cotangent:
- *   *d_loss = mean((y - t)^2);  dY = half(scale * 2 (y - t) / n). */
+ *   *d_loss = mean((y - t)^2);  dY = half(scale * 2 (y - t) / n).
+ * dt == MPX_F32: Y, T and dY are float32 (full precision; half() is the
+ * identity; a state with scale 1 gives the unscaled cotangent). */
 int mpx_mse(const void* Y, const void* T, int64_t n, const mpx_scale_state* d_state,
             float* d_loss, void* dY, mpx_dtype dt, void* workspace, size_t ws_bytes,
             void* stream);

@@ -18,6 +18,11 @@ The reading taken here (one rounding per layer-level op):
 
 ``Policy("f64")`` switches every rounding off and computes GEMMs in float64:
 the plain real-arithmetic model used for finite-difference checks.
+
+``Policy("f32")`` is full-precision training (MPX's ``use_mixed_precision``
+switched off, §3.4: nothing is cast to half): every op's output is rounded to
+float32, GEMMs accumulate in float32 (a library float32 matmul) and the
+full-precision islands are computed in float64 and rounded once to float32.
 """
 from __future__ import annotations
 
@@ -28,7 +33,7 @@ from .numfmt import round_to
 
 class Policy:
     def __init__(self, fmt: str):
-        if fmt not in ("f16", "bf16", "f64"):
+        if fmt not in ("f16", "bf16", "f32", "f64"):
             raise ValueError(fmt)
         self.fmt = fmt
         self.exact = fmt == "f64"

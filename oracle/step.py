@@ -112,6 +112,21 @@ def train_step(cfg, state: TrainState, batch, step: int, pol: Optional[Policy] =
     return new_state, StepResult(loss, nonfinite, nonfinite == 0, scale_used, grads)
 
 
+def full_precision_step(cfg, state: TrainState, batch) -> tuple:
+    """One training step with mixed precision switched off (MPX's
+    ``use_mixed_precision=False``, §3.4): inputs and weights stay float32, the
+    loss is not scaled, every op rounds to float32 (``Policy("f32")``), and
+    AdamW is applied unconditionally to the float32 gradients.  The loss
+    scale state is left as it is.  Returns (new_state, loss, gradients)."""
+    pol = Policy("f32")
+    P = {n: pol.R(w) for n, w in zip(state.names, state.masters)}
+    loss, dout, cache = models.forward_loss(pol, cfg, P, cast_batch(pol, batch), 1.0)
+    G = models.backward(pol, cfg, P, cache, dout)
+    grads = [np.array(G[n], dtype=np.float32) for n in state.names]
+    p, m, v, t = adamw_masked(state.masters, state.m, state.v, grads, state.t, hp_of(cfg), True)
+    return replace(state, masters=p, m=m, v=v, t=t), loss, grads
+
+
 def run(cfg, steps: Optional[int] = None, state: Optional[TrainState] = None):
     """Free-running: ``steps`` training steps on the fixed synthetic batch."""
     state = state or init_state(cfg)

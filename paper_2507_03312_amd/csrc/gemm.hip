@@ -1,7 +1,9 @@
 // C ABI of the half GEMMs (linear forward / backward, batched attention
 // products): argument checks, split-K planning and dispatch to the kernels
 // of gemm_kernels.h, which are compiled once per half type in gemm_f16.hip
-// and gemm_bf16.hip.
+// and gemm_bf16.hip; float32 calls (full-precision training) go to the
+// kernels of gemm_f32.hip.
+#include "gemm_f32.h"
 #include "gemm_kernels.h"
 
 namespace mpx {
@@ -36,6 +38,21 @@ static int choose_splits(int64_t M, int64_t N, int64_t K) {
   return (int)std::max<int64_t>(s, 1);
 }
 
+// split-K plan of a reduction of length Mr over an N x K weight gradient:
+// sp splits of k_split rows each (a multiple of 64), every split non-empty
+static void split_plan(int64_t N, int64_t K, int64_t Mr, int& sp, int64_t& k_split) {
+  sp = choose_splits(N, K, Mr);
+  k_split = ((Mr + sp - 1) / sp + 63) / 64 * 64;
+  sp = (int)((Mr + k_split - 1) / k_split);
+}
+
+static GemmF32Args f32_args() {
+  GemmF32Args g{};
+  g.splits = 1;
+  g.k_split = INT64_MAX / 4;
+  return g;
+}
+
 }  // namespace mpx
 
 using namespace mpx;
@@ -46,9 +63,23 @@ extern "C" int mpx_linear_fwd(const void* X, const void* W, const void* b, const
   clear_error();
   MPX_REQUIRE(X && W && Y, "NULL operand");
   MPX_REQUIRE(M >= 1 && N >= 1 && K >= 1, "M, N, K must be >= 1");
-  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
   MPX_REQUIRE(act == MPX_ACT_NONE || act == MPX_ACT_GELU_TANH, "unknown activation");
   MPX_REQUIRE(act == MPX_ACT_NONE || Ypre, "Ypre is required with an activation");
+  if (dt == MPX_F32) {  // full precision: every operand float32
+    GemmF32Args g = f32_args();
+    g.A = (const float*)X;
+    g.B = (const float*)W;
+    g.C = (float*)Y;
+    g.M = M; g.N = N; g.K = K;
+    g.lda = K; g.ldb = K; g.ldc = N;
+    g.bias = (const float*)b;
+    g.resid = (const float*)R;
+    g.pre = act ? (float*)Ypre : nullptr;
+    g.act = act;
+    MPX_HIP(launch_gemm_f32(g, true, true, (hipStream_t)stream));
+    return MPX_OK;
+  }
   GemmArgs g = base_args();
   g.A = (const uint16_t*)X;
   g.B = (const uint16_t*)W;
@@ -81,9 +112,10 @@ extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, cons
   MPX_REQUIRE(!dX || W, "W is required for dX");
   MPX_REQUIRE(!dW || X, "X is required for dW");
   MPX_REQUIRE(M >= 1 && N >= 1 && K >= 1, "M, N, K must be >= 1");
-  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
   MPX_REQUIRE(x_act == MPX_ACT_NONE || x_act == MPX_ACT_GELU_TANH, "unknown activation");
   MPX_REQUIRE(x_act == MPX_ACT_NONE || !dX || Xpre, "Xpre is required with x_act");
+  MPX_REQUIRE(dt != MPX_F32 || !d_nonfinite, "d_nonfinite is counted for half gradients only");
   if (dW || db) {  // only the weight and bias gradients use the workspace
     const size_t need = mpx_linear_bwd_workspace(M, N, K);
     if (ws_bytes < need || !workspace) {
@@ -92,6 +124,40 @@ extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, cons
     }
   }
   hipStream_t s = (hipStream_t)stream;
+  if (dt == MPX_F32) {  // full precision: the same three products in float32
+    if (dX) {
+      GemmF32Args g = f32_args();
+      g.A = (const float*)dY;
+      g.B = (const float*)W;
+      g.C = (float*)dX;
+      g.M = M; g.N = K; g.K = N;
+      g.lda = N; g.ldb = K; g.ldc = K;
+      g.dact = x_act ? (const float*)Xpre : nullptr;
+      MPX_HIP(launch_gemm_f32(g, true, false, s));
+    }
+    if (dW) {
+      GemmF32Args g = f32_args();
+      g.A = (const float*)dY;
+      g.B = (const float*)X;
+      g.C = (float*)dW;
+      g.M = N; g.N = K; g.K = M;
+      g.lda = N; g.ldb = K; g.ldc = K;
+      int sp;
+      int64_t ks;
+      split_plan(N, K, M, sp, ks);
+      if (sp > 1) {
+        g.splits = sp;
+        g.k_split = ks;
+        g.ws = (float*)workspace;
+        MPX_HIP(launch_gemm_f32(g, false, false, s));
+        MPX_HIP(launch_splitk_reduce_f32(g.ws, sp, N * K, (float*)dW, s));
+      } else {
+        MPX_HIP(launch_gemm_f32(g, false, false, s));
+      }
+    }
+    if (db) MPX_HIP(launch_colsum_f32((const float*)dY, M, N, (float*)workspace, (float*)db, s));
+    return MPX_OK;
+  }
   // dX[M,K] = dY[M,N] W[N,K]: A = dY (k-major over N), B(n=k', k=n) = W[n*K + k'] (mn-major)
   if (dX) {
     GemmArgs g = base_args();
@@ -112,11 +178,12 @@ extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, cons
     g.M = N; g.N = K; g.K = M;
     g.lda = N; g.ldb = K; g.ldc = K;
     g.nonfinite = d_nonfinite;
-    const int sp = choose_splits(N, K, M);
+    int sp;
+    int64_t ks;
+    split_plan(N, K, M, sp, ks);
     if (sp > 1) {
       g.splits = sp;
-      g.k_split = ((M + sp - 1) / sp + 63) / 64 * 64;
-      g.splits = (int)((M + g.k_split - 1) / g.k_split);
+      g.k_split = ks;
       g.ws = (float*)workspace;
       MPX_HIP(gemm_dispatch(dt, g, false, false, 1, s));
       const int64_t MN = N * K;

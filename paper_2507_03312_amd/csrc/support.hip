@@ -596,6 +596,29 @@ __global__ __launch_bounds__(256) void mse_kernel(const uint16_t* __restrict__ Y
   if (threadIdx.x == 0) part[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
 }
 
+// Float32 form of mse_kernel (full-precision training): same blocks and sums.
+__global__ __launch_bounds__(256) void mse_f32_kernel(const float* __restrict__ Y, const float* __restrict__ T,
+                                                      int64_t n, const mpx_scale_state* __restrict__ st,
+                                                      float* __restrict__ part, float* __restrict__ dY) {
+  const float k = 2.0f * st->scale / (float)n;
+  float acc = 0.0f;
+  const int64_t base = (int64_t)blockIdx.x * kMseBlock;
+#pragma unroll
+  for (int u = 0; u < kMseBlock / 256; ++u) {
+    const int64_t i = base + u * 256 + threadIdx.x;
+    if (i < n) {
+      const float df = Y[i] - T[i];
+      acc += df * df;
+      dY[i] = k * df;
+    }
+  }
+  __shared__ float red[4];
+  acc = wave_sum(acc);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) part[blockIdx.x] = ((red[0] + red[1]) + red[2]) + red[3];
+}
+
 // sum of squared errors over blocks, divided by n
 __global__ __launch_bounds__(256) void mse_final_kernel(const float* __restrict__ part, int64_t nb,
                                                         int64_t n, float* __restrict__ loss) {
@@ -928,12 +951,19 @@ extern "C" int mpx_mse(const void* Y, const void* T, int64_t n, const mpx_scale_
   clear_error();
   MPX_REQUIRE(Y && T && d_state && d_loss && dY, "NULL argument");
   MPX_REQUIRE(n >= 1, "n must be >= 1");
-  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
   if (!workspace || ws_bytes < mpx_loss_workspace(n)) {
     set_error("mpx_mse: workspace of " + std::to_string(mpx_loss_workspace(n)) + " bytes required");
     return MPX_ERR_WORKSPACE;
   }
   const int64_t nb = (n + kMseBlock - 1) / kMseBlock;
+  if (dt == MPX_F32) {
+    mse_f32_kernel<<<(unsigned)nb, 256, 0, (hipStream_t)stream>>>((const float*)Y, (const float*)T, n,
+                                                                  d_state, (float*)workspace, (float*)dY);
+    mse_final_kernel<<<1, 256, 0, (hipStream_t)stream>>>((const float*)workspace, nb, n, d_loss);
+    MPX_LAUNCHED();
+    return MPX_OK;
+  }
   MPX_DT_DISPATCH(dt, mse_kernel, (unsigned)nb, 256, stream, (const uint16_t*)Y, (const uint16_t*)T, n,
                   d_state, (float*)workspace, (uint16_t*)dY);
   mse_final_kernel<<<1, 256, 0, (hipStream_t)stream>>>((const float*)workspace, nb, n, d_loss);

@@ -61,9 +61,11 @@ def unpack_scale_state(words: np.ndarray):
 
 
 class Arena:
-    """Flat arenas for masters (f32), m, v (f32), half copy and half grads."""
+    """Flat arenas for masters (f32), m, v (f32), half copy and half grads.
+    With ``full=True`` (full-precision training) there is no half copy (the
+    layers read the masters) and the gradients are float32."""
 
-    def __init__(self, specs, half: str, device):
+    def __init__(self, specs, half: str, device, full: bool = False):
         self.names = [n for n, _, _ in specs]
         self.shapes = {n: tuple(s) for n, s, _ in specs}
         self.offsets: Dict[str, int] = {}
@@ -72,16 +74,16 @@ class Arena:
             self.offsets[n] = off
             off += -(-int(np.prod(s)) // ALIGN) * ALIGN
         self.total = off
-        hdt = TORCH_HALF[half]
+        hdt = torch.float32 if full else TORCH_HALF[half]
         self.p32 = torch.zeros(off, dtype=torch.float32, device=device)
         self.m32 = torch.zeros_like(self.p32)
         self.v32 = torch.zeros_like(self.p32)
-        self.h = torch.zeros(off, dtype=hdt, device=device)
+        self.h = self.p32 if full else torch.zeros(off, dtype=hdt, device=device)
         self.g = torch.zeros(off, dtype=hdt, device=device)
         self.L_p = mx.TensorList([self.p32])
         self.L_m = mx.TensorList([self.m32])
         self.L_v = mx.TensorList([self.v32])
-        self.L_h = mx.TensorList([self.h])
+        self.L_h = None if full else mx.TensorList([self.h])
         self.L_g = mx.TensorList([self.g])
 
     def view(self, arena: torch.Tensor, name: str) -> torch.Tensor:
@@ -114,26 +116,31 @@ class Arena:
 class TrainStep:
     """Device state and the call sequence common to both model families."""
 
-    def __init__(self, cfg, device="cuda"):
+    def __init__(self, cfg, device="cuda", full_precision: bool = False):
         self.cfg = cfg
         self.device = torch.device(device)
+        # full precision: MPX's use_mixed_precision switched off (the
+        # baseline of the paper's comparison): float32 layers, no loss
+        # scaling, AdamW on every step
+        self.full = full_precision
         self.half = cfg.half
-        self.dt = mx.DTYPES[cfg.half]
-        self.hdt = TORCH_HALF[cfg.half]
-        self.arena = Arena(workloads.param_specs(cfg), cfg.half, self.device)
+        self.dt = mx.MPX_F32 if self.full else mx.DTYPES[cfg.half]
+        self.hdt = torch.float32 if self.full else TORCH_HALF[cfg.half]
+        self.arena = Arena(workloads.param_specs(cfg), cfg.half, self.device, self.full)
+        scale0 = 1.0 if self.full else cfg.scale_init
         self.d_state = torch.from_numpy(
-            pack_scale_state(cfg.scale_init, 0, cfg.period, cfg.factor, cfg.min_scale,
+            pack_scale_state(scale0, 0, cfg.period, cfg.factor, cfg.min_scale,
                              cfg.max_scale)).to(self.device)
         self.d_nonfinite = torch.zeros(1, dtype=torch.int32, device=self.device)
         self.d_step = torch.zeros(1, dtype=torch.int32, device=self.device)
         self.d_loss = torch.zeros(1, dtype=torch.float32, device=self.device)
         self.hp = mx.AdamWHP(cfg.lr, cfg.beta1, cfg.beta2, cfg.eps, cfg.weight_decay)
-        self.half_copy_fresh = False
+        self.half_copy_fresh = self.full  # full precision reads the masters directly
         # MPX §3.4's finite check fused into the kernels that write the
         # parameter gradients (they add their non-finite count to d_nonfinite,
         # zeroed at the start of the step); False: a separate unscale/check
         # pass over the whole gradient list after the backward
-        self.fused_check = True
+        self.fused_check = not self.full
         self.arena.load_masters(workloads.init_params(cfg))
 
     # ---- state access (harness only; each of these synchronises) ----
@@ -166,13 +173,18 @@ class TrainStep:
 
     def _nf(self):
         """Counter argument of the gradient-writing calls."""
-        return _ptr(self.d_nonfinite) if self.fused_check else None
+        return _ptr(self.d_nonfinite) if self.fused_check and not self.full else None
 
     def finish(self):
         """Finite check (unless fused into the backward), masked AdamW (+ half
         copy), scale update."""
         s = _stream()
         a = self.arena
+        if self.full:  # no scaling, no check: AdamW on the float32 gradients
+            mx.mpx_adamw_masked(a.L_p, a.L_m, a.L_v, a.L_g, mx.MPX_F32, self.hp,
+                                _ptr(self.d_step), _ptr(self.d_state), _ptr(self.d_nonfinite),
+                                None, self.dt, s)
+            return
         if not self.fused_check:
             mx.mpx_unscale_check(a.L_g, self.dt, _ptr(self.d_state), _ptr(self.d_nonfinite), None,
                                  s)
@@ -259,18 +271,21 @@ def _linear_gelu_bytes(M: int, N: int, K: int) -> int:
 
 
 class MLPStep(TrainStep):
-    """2-layer MLP with GELU and an MSE loss."""
+    """2-layer MLP with GELU and an MSE loss (mixed or full precision)."""
 
-    def __init__(self, cfg, device="cuda"):
-        super().__init__(cfg, device)
+    def __init__(self, cfg, device="cuda", full_precision: bool = False):
+        super().__init__(cfg, device, full_precision)
         B, D, Dh = cfg.batch, cfg.d_in, cfg.d_hidden
         dev, h = self.device, self.hdt
         self.x32 = torch.zeros(B, D, dtype=torch.float32, device=dev)
         self.t32 = torch.zeros(B, D, dtype=torch.float32, device=dev)
-        self.x16 = torch.zeros(B, D, dtype=h, device=dev)
-        self.t16 = torch.zeros(B, D, dtype=h, device=dev)
-        self.L_in = mx.TensorList([self.x32, self.t32])
-        self.L_in16 = mx.TensorList([self.x16, self.t16])
+        if self.full:  # the float32 inputs are used as they are
+            self.x16, self.t16 = self.x32, self.t32
+        else:
+            self.x16 = torch.zeros(B, D, dtype=h, device=dev)
+            self.t16 = torch.zeros(B, D, dtype=h, device=dev)
+            self.L_in = mx.TensorList([self.x32, self.t32])
+            self.L_in16 = mx.TensorList([self.x16, self.t16])
         self.h_pre = torch.zeros(B, Dh, dtype=h, device=dev)
         self.hid = torch.zeros(B, Dh, dtype=h, device=dev)
         self.y = torch.zeros(B, D, dtype=h, device=dev)
@@ -294,7 +309,8 @@ class MLPStep(TrainStep):
 
     def describe(self):
         c = self.cfg
-        return f"MLP {c.d_in}->{c.d_hidden}->{c.d_in} GELU, MSE, batch {c.batch}, {c.half}"
+        prec = "f32 (full precision)" if self.full else c.half
+        return f"MLP {c.d_in}->{c.d_hidden}->{c.d_in} GELU, MSE, batch {c.batch}, {prec}"
 
     def set_batch(self, batch):
         self.x32.copy_(torch.from_numpy(batch["x"]))
@@ -306,7 +322,8 @@ class MLPStep(TrainStep):
         nf = self._nf()
         if nf:
             mx.mpx_zero(nf, 4, s)
-        mx.mpx_cast_to_half(self.L_in, self.L_in16, dt, s)
+        if not self.full:
+            mx.mpx_cast_to_half(self.L_in, self.L_in16, dt, s)
         self._dominant_call(s)
         mx.mpx_linear_fwd(_ptr(self.hid), _ptr(a.w("fc2.w")), _ptr(a.w("fc2.b")), None,
                           _ptr(self.y), None, B, D, Dh, dt, mx.MPX_ACT_NONE, s)
@@ -643,5 +660,9 @@ class ViTStep(TrainStep):
         main.wait_stream(side)  # join: the optimizer reads every gradient
 
 
-def make_step(cfg, device="cuda") -> TrainStep:
-    return MLPStep(cfg, device) if cfg.kind == "mlp" else ViTStep(cfg, device)
+def make_step(cfg, device="cuda", full_precision: bool = False) -> TrainStep:
+    if cfg.kind == "mlp":
+        return MLPStep(cfg, device, full_precision)
+    if full_precision:
+        raise NotImplementedError("full-precision steps are built for the MLP only")
+    return ViTStep(cfg, device)

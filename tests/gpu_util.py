@@ -16,7 +16,7 @@ needs_gpu = pytest.mark.skipif(not HAVE_GPU, reason="no GPU")
 TORCH_HALF = {"f16": None, "bf16": None}
 if torch is not None:
     TORCH_HALF = {"f16": torch.float16, "bf16": torch.bfloat16}
-FMT_BITS = {"f16": (11, -14), "bf16": (8, -126)}
+FMT_BITS = {"f16": (11, -14), "bf16": (8, -126), "f32": (24, -126)}
 
 
 def to_dev_half(a: np.ndarray, fmt: str):
@@ -30,7 +30,8 @@ def to_host(t) -> np.ndarray:
 
 
 def ulp(x: np.ndarray, fmt: str) -> np.ndarray:
-    """Spacing of the half format at |x| (subnormal spacing below the normal range)."""
+    """Spacing of the format (half, or float32) at |x| (subnormal spacing below
+    the normal range)."""
     p, emin = FMT_BITS[fmt]
     x = np.abs(np.asarray(x, np.float64))
     _, e = np.frexp(np.where(np.isfinite(x), x, 1.0))

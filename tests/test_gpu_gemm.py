@@ -425,3 +425,75 @@ def test_linear_bwd_subsets_match_full_call(fmt):
     with pytest.raises(mx.MPXError, match="workspace"):
         mx.mpx_linear_bwd(tx.data_ptr(), None, tdy.data_ptr(), None, 0, None, part[1].data_ptr(),
                           None, M, N, K, dt, None, 0, None, _s())
+
+
+# ------------------------------------------- full precision (MPX_F32) --
+
+def _dev32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+
+def _rand32(shape, seed, std=1.0):
+    return np.random.default_rng(seed).normal(0, std, size=shape).astype(np.float32)
+
+
+def _zeros32(*shape):
+    return torch.zeros(*shape, dtype=torch.float32, device="cuda")
+
+
+# hardware exp2 / reciprocal inside GELU and GELU': a few float32 ulps
+GELU_F32_REL = 4e-6
+
+
+@pytest.mark.parametrize("mnk", [(64, 1024, 512), (70, 100, 72), (33, 17, 50), (300, 200, 1000),
+                                 (4096, 384, 384), (129, 130, 131), (1, 8, 8)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_linear_f32_matches_full_precision_oracle(mnk):
+    """Full-precision training (mixed precision switched off): the float32
+    products, their epilogues and the bias sums against the oracle's float32
+    policy, within the bound of two float32 summation orders."""
+    M, N, K = mnk
+    pol = Policy("f32")
+    F32 = mx.MPX_F32
+    x, w, b, r = _rand32((M, K), 1), _rand32((N, K), 2, 0.05), _rand32((N,), 3, 0.5), _rand32((M, N), 4)
+    tx, tw, tb, tr = (_dev32(a) for a in (x, w, b, r))
+    y, pre = _zeros32(M, N), _zeros32(M, N)
+    ref = ops.linear_fwd(pol, x, w, b)
+    bnd = gemm_bound(x, w.T, ref, "f32", K) + ulp(ref, "f32")
+    mx.mpx_linear_fwd(tx.data_ptr(), tw.data_ptr(), tb.data_ptr(), None, y.data_ptr(), None, M, N, K,
+                      F32, mx.MPX_ACT_NONE, _s())
+    assert_within(to_host(y), ref, bnd, "Y")
+    mx.mpx_linear_fwd(tx.data_ptr(), tw.data_ptr(), tb.data_ptr(), None, y.data_ptr(), pre.data_ptr(),
+                      M, N, K, F32, mx.MPX_ACT_GELU_TANH, _s())
+    gpre = to_host(pre)
+    assert_within(gpre, ref, bnd, "pre-activation")
+    gref = ops.gelu_fwd(pol, gpre)
+    assert_within(to_host(y), gref, GELU_F32_REL * np.abs(gref) + ulp(gref, "f32"), "GELU")
+    mx.mpx_linear_fwd(tx.data_ptr(), tw.data_ptr(), tb.data_ptr(), tr.data_ptr(), y.data_ptr(), None,
+                      M, N, K, F32, mx.MPX_ACT_NONE, _s())
+    rref = ops.add(pol, ref, r)
+    assert_within(to_host(y), rref, bnd + ulp(rref, "f32"), "Y + R")
+    # backward
+    dy, xp = _rand32((M, N), 13), _rand32((M, K), 14)
+    tdy, txp = _dev32(dy), _dev32(xp)
+    gdx, gdw, gdb = _zeros32(M, K), _zeros32(N, K), _zeros32(N)
+    ws_n = mx.mpx_linear_bwd_workspace(M, N, K)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), None, mx.MPX_ACT_NONE,
+                      gdx.data_ptr(), gdw.data_ptr(), gdb.data_ptr(), M, N, K, F32, ws.data_ptr(), ws_n,
+                      None, _s())
+    rdx, rdw, rdb = ops.linear_bwd(pol, x, w, dy)
+    assert_within(to_host(gdx), rdx, gemm_bound(dy, w, rdx, "f32", N), "dX")
+    assert_within(to_host(gdw), rdw, gemm_bound(dy.T, x, rdw, "f32", M), "dW")
+    colb = ulp(rdb, "f32") + 2.0 * M * 2.0 ** -24 * np.abs(dy.astype(np.float64)).sum(axis=0)
+    assert_within(to_host(gdb), rdb, colb, "db")
+    mx.mpx_linear_bwd(tx.data_ptr(), tw.data_ptr(), tdy.data_ptr(), txp.data_ptr(),
+                      mx.MPX_ACT_GELU_TANH, gdx.data_ptr(), None, None, M, N, K, F32, ws.data_ptr(),
+                      ws_n, None, _s())
+    gref = ops.gelu_bwd(pol, xp, rdx)
+    bound = 1.13 * gemm_bound(dy, w, rdx, "f32", N) + GELU_F32_REL * np.abs(gref) + ulp(gref, "f32")
+    assert_within(to_host(gdx), gref, bound, "dX through gelu'")
+    with pytest.raises(mx.MPXError, match="half gradients only"):
+        nf = torch.zeros(1, dtype=torch.int32, device="cuda")
+        mx.mpx_linear_bwd(tx.data_ptr(), None, tdy.data_ptr(), None, 0, None, gdw.data_ptr(), None,
+                          M, N, K, F32, ws.data_ptr(), ws_n, nf.data_ptr(), _s())

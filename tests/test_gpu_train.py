@@ -197,3 +197,49 @@ def test_fused_check_matches_separate_pass(name, scale, overflows):
             assert np.array_equal(a, b)
     if overflows:  # fp16 with these scales: the first step overflows for certain
         assert counts[0] > 0
+
+
+def test_mlp_full_precision_lockstep():
+    """Full precision (mixed precision switched off, the baseline of the
+    paper's comparison) against the oracle's float32 step: from the same
+    start-of-step masters the GPU's float32 gradients match within 1e-5
+    normwise per tensor, the loss within 1e-6, and the oracle's AdamW on the
+    GPU's own gradients matches the GPU's update (masters within 1e-5); no
+    loss scaling, so every step applies."""
+    from oracle.adamw import adamw_masked
+    cfg = workloads.get("mlp")
+    gpu = make_step(cfg, full_precision=True)
+    batch = workloads.make_batch(cfg)
+    gpu.set_batch(batch)
+    ost = ostep.init_state(cfg)
+    for s in range(3):
+        start = ostep.TrainState(ost.names, gpu.masters(), ost.m, ost.v, ost.t, ost.scale)
+        _, loss_ref, g_ref = ostep.full_precision_step(cfg, start, batch)
+        gpu.forward_backward()
+        g_gpu = gpu.grads()
+        assert abs(gpu.loss() - loss_ref) <= 1e-6 * abs(loss_ref)
+        for name, a, b in zip(ost.names, g_gpu, g_ref):
+            assert rel_norm_err(a, b) <= 1e-5, (s, name, rel_norm_err(a, b))
+        gpu.finish()
+        p, m, v, t = adamw_masked(start.masters, start.m, start.v, g_gpu, start.t,
+                                  ostep.hp_of(cfg), True)
+        for name, a, b in zip(ost.names, gpu.masters(), p):
+            assert np.all(np.abs(a - b) <= 1e-5 * np.maximum(np.abs(b), cfg.lr)), (s, name)
+        ost = ostep.TrainState(ost.names, p, m, v, t, ost.scale)
+    assert gpu.nonfinite() == 0 and int(gpu.d_step.item()) == 3
+    assert gpu.scale_state()["scale"] == 1.0
+
+
+def test_mlp_full_precision_graph_replay_matches_eager():
+    cfg = workloads.get("mlp")
+    batch = workloads.make_batch(cfg)
+    eager, graphed = make_step(cfg, full_precision=True), make_step(cfg, full_precision=True)
+    eager.set_batch(batch)
+    graphed.set_batch(batch)
+    graphed.capture()
+    for _ in range(3):
+        eager.step()
+        graphed.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(eager.masters(), graphed.masters()):
+            assert np.array_equal(a, b)

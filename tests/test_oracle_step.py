@@ -43,3 +43,30 @@ def test_mlp_gradients_are_half_and_scaled():
         assert np.array_equal(g.astype(np.float16).astype(np.float32), g)
     # scaled by 2^15: the gradients are far from the f16 subnormal range
     assert max(float(np.max(np.abs(g))) for g in grads) > 1.0
+
+
+def test_full_precision_step_matches_float64_gradients():
+    """Full precision (mixed precision switched off): with every op rounded
+    to float32 the MLP workload's gradients agree with the float64 policy's
+    (the exact-arithmetic model pinned by finite differences) to float32
+    accuracy, the loss is unscaled, the scale state is untouched, and the
+    step applies AdamW (step count advances)."""
+    cfg = workloads.get("mlp")
+    st = step.init_state(cfg)
+    batch = workloads.make_batch(cfg)
+    new, loss, grads = step.full_precision_step(cfg, st, batch)
+    pol = step.Policy("f64")
+    P = {n: np.asarray(w, np.float64) for n, w in zip(st.names, st.masters)}
+    fb = {k: np.asarray(v, np.float64) for k, v in batch.items()}
+    loss64, dout, cache = step.models.forward_loss(pol, cfg, P, fb, 1.0)
+    G = step.models.backward(pol, cfg, P, cache, dout)
+    assert abs(loss - loss64) <= 1e-6 * abs(loss64)
+    for n, g in zip(st.names, grads):
+        assert g.dtype == np.float32
+        ref = np.asarray(G[n], np.float64)
+        err = np.linalg.norm(g - ref) / np.linalg.norm(ref)
+        assert err <= 1e-5, (n, err)
+        # a float32 result, not a half one: some values are not half-representable
+        assert not np.array_equal(g.astype(np.float16).astype(np.float32), g)
+    assert new.t == st.t + 1 and new.scale == st.scale
+    assert any(not np.array_equal(a, b) for a, b in zip(new.masters, st.masters))
