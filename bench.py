@@ -33,6 +33,7 @@ import workloads
 
 PEAK_MFMA_TFLOPS = {"f16": 2500.0, "bf16": 2500.0}   # dense, MI355X
 PEAK_HBM_GBS = 8000.0
+PEAK_F32_TFLOPS = 157.3                               # dense float32 MFMA, MI355X
 DEFAULT_CONFIG = "vit_block"
 
 # HBM bytes per launch of the dominant kernels from two rocprofv3 --pmc runs
@@ -84,6 +85,9 @@ def parse():
     ap.add_argument("--config", default=DEFAULT_CONFIG, choices=workloads.CONFIG_ORDER)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--compare-precision", action="store_true",
+                    help="MLP workload: step time and peak device memory of full precision "
+                         "(mixed precision switched off) against mixed precision, over batch sizes")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB "
                          "(reference dispatch for hardware byte counters)")
@@ -179,6 +183,69 @@ def gemm_table(st, peak):
             "block_aggregate_frac": round(agg / peak, 4)}
 
 
+def compare_precision(args, dev):
+    """Full precision vs mixed precision on the MLP workload (512 -> 1024 ->
+    512, GELU, MSE, fp16) over batch sizes: graph-replayed step time and the
+    peak device memory the step allocates (parameters, optimizer state,
+    activations, workspaces), the shape of the paper's comparison (§4)."""
+    import torch
+    from paper_2507_03312_amd.train import make_step
+    base_cfg = workloads.get("mlp")
+    rows = []
+    gemm = {}
+    batches = [64, 1024, 8192, 32768, 131072]
+    for B in batches:
+        cfg = workloads.scaled_down(base_cfg, batch=B)
+        batch = workloads.make_batch(cfg)
+        row = {"batch": B}
+        for full in (True, False):
+            key = "full" if full else "mixed"
+            torch.cuda.synchronize()
+            torch.cuda.empty_cache()
+            torch.cuda.reset_peak_memory_stats(dev)
+            base = torch.cuda.memory_allocated(dev)
+            st = make_step(cfg, dev, full_precision=full)
+            st.set_batch(batch)
+            st.step()
+            st.capture()
+            steps = max(10, min(2000, 2_000_000 // B))
+            for _ in range(3):
+                st.replay()
+            torch.cuda.synchronize()
+            t0 = torch.cuda.Event(enable_timing=True)
+            t1 = torch.cuda.Event(enable_timing=True)
+            t0.record()
+            for _ in range(steps):
+                st.replay()
+            t1.record()
+            torch.cuda.synchronize()
+            row[key + "_ms"] = round(t0.elapsed_time(t1) / steps, 4)
+            row[key + "_mib"] = round((torch.cuda.max_memory_allocated(dev) - base) / 2 ** 20, 1)
+            if B == batches[-1]:
+                site = st.dominant_site()
+                k_ms = st.time_dominant()
+                tf = site["flops"] / (k_ms * 1e-3) / 1e12
+                peak = PEAK_F32_TFLOPS if full else PEAK_MFMA_TFLOPS[cfg.half]
+                gemm[key] = {"kernel": site["desc"], "us": round(k_ms * 1e3, 2),
+                             "tflops": round(tf, 1), "peak": peak, "frac": round(tf / peak, 4)}
+            del st
+        row["speedup"] = round(row["full_ms"] / row["mixed_ms"], 3)
+        row["memory_ratio"] = round(row["full_mib"] / row["mixed_mib"], 3)
+        rows.append(row)
+        print(json.dumps(row), file=sys.stderr, flush=True)
+    last = rows[-1]
+    line = {"metric": "full-precision / mixed-precision step time", "value": last["speedup"],
+            "unit": "x", "n_gpus": 1, "steps": None, "warmup": 3,
+            "ms_per_step": last["mixed_ms"], "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "f32 vs " + base_cfg.half, "data": "synthetic",
+            "config": {"workload": "MLP 512->1024->512 GELU, MSE; full precision (f32 layers, no "
+                                   "loss scaling) vs mixed precision (fp16 layers, dynamic loss "
+                                   "scaling), batch sizes " + ",".join(map(str, batches)),
+                       "parallelism": "none"},
+            "comparison": rows, "gemm_at_largest_batch": gemm}
+    print(json.dumps(line))
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -192,6 +259,9 @@ def main():
     cfg = workloads.get(args.config)
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
+    if args.compare_precision:
+        compare_precision(args, dev)
+        return
 
     if args.config == "sweep":
         steps = args.steps or 50

@@ -304,8 +304,10 @@ class MLPStep(TrainStep):
     def dominant_site(self):
         c = self.cfg
         M, N, K = c.batch, c.d_hidden, c.d_in
-        return {"name": "fc1.fwd", "flops": 2.0 * M * N * K, "bytes": _linear_gelu_bytes(M, N, K),
-                "desc": f"linear_fwd+GELU M={M} N={N} K={K} ({c.half})"}
+        width = 2 if self.full else 1  # float32 operands: twice the bytes
+        return {"name": "fc1.fwd", "flops": 2.0 * M * N * K,
+                "bytes": width * _linear_gelu_bytes(M, N, K),
+                "desc": f"linear_fwd+GELU M={M} N={N} K={K} ({'f32' if self.full else c.half})"}
 
     def describe(self):
         c = self.cfg
