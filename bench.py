@@ -44,20 +44,20 @@ DEFAULT_CONFIG = "vit_block"
 # they no longer match, the figure is stale and reported as null.
 TRAFFIC = {
     "blk0.up.fwd": {
-        "fetch_kib": 13975.4, "write_kib": 49920.0,
-        "fetch_factor": 262144.0 / 131088.4, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 13962.7, "write_kib": 49920.0,
+        "fetch_factor": 262144.0 / 131088.8, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/gemm_kernels.h": "3fba3ac8fb77021bb068716256f7178b1c1a926420d0b42f2a2d29c1712fa920",
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "b366ba284d399186b2b6f06b2b68e0b01c0fa9e1426ce688bbe91db7f0e42c3f",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
-            "paper_2507_03312_amd/csrc/common.h": "730b9a02e1fa63f557d2c496e7263b42acecd1543d8f7cb787b1a2929e4bbeee",
+            "paper_2507_03312_amd/csrc/common.h": "8c0e81134196be66ac491faba83bf6615b277c811a71a1777f05facdde4e0e23",
         },
     },
     "sweep": {
-        "fetch_kib": 686822.2, "write_kib": 1367202.4,
-        "fetch_factor": 262144.0 / 131089.1, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 686822.2, "write_kib": 1367205.2,
+        "fetch_factor": 262144.0 / 131088.9, "write_factor": 262144.0 / 262144.0,
         "sources": {
             "paper_2507_03312_amd/csrc/sweep.hip": "c602435f1b696d1b01bd40828d85fbd12bbbce651354540e554f5fb723602496",
-            "paper_2507_03312_amd/csrc/common.h": "730b9a02e1fa63f557d2c496e7263b42acecd1543d8f7cb787b1a2929e4bbeee",
+            "paper_2507_03312_amd/csrc/common.h": "8c0e81134196be66ac491faba83bf6615b277c811a71a1777f05facdde4e0e23",
         },
     },
 }
