@@ -86,8 +86,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--compare-precision", action="store_true",
-                    help="MLP workload: step time and peak device memory of full precision "
-                         "(mixed precision switched off) against mixed precision, over batch sizes")
+                    help="step time and peak device memory of full precision (mixed precision "
+                         "switched off) against mixed precision over batch sizes, for the "
+                         "workload of --config (mlp when the default is left)")
     ap.add_argument("--copy-calibration-mib", type=int, default=0,
                     help="after the timed region, run one plain device copy of this many MiB "
                          "(reference dispatch for hardware byte counters)")
@@ -184,16 +185,23 @@ def gemm_table(st, peak):
 
 
 def compare_precision(args, dev):
-    """Full precision vs mixed precision on the MLP workload (512 -> 1024 ->
-    512, GELU, MSE, fp16) over batch sizes: graph-replayed step time and the
-    peak device memory the step allocates (parameters, optimizer state,
-    activations, workspaces), the shape of the paper's comparison (§4)."""
+    """Full precision vs mixed precision over batch sizes: graph-replayed step
+    time and the peak device memory the step allocates (parameters, optimizer
+    state, inputs, activations, workspaces), the shape of the paper's
+    comparison (§4).  MLP workload: batches 64 .. 131072; a ViT workload: half
+    to four times its batch (ViT-S: 128 .. 1024, the paper's range)."""
     import torch
     from paper_2507_03312_amd.train import make_step
-    base_cfg = workloads.get("mlp")
+    name = "mlp" if args.config == DEFAULT_CONFIG else args.config
+    if name == "sweep":
+        raise SystemExit("--compare-precision needs a training workload")
+    base_cfg = workloads.get(name)
     rows = []
     gemm = {}
-    batches = [64, 1024, 8192, 32768, 131072]
+    if name == "mlp":
+        batches = [64, 1024, 8192, 32768, 131072]
+    else:
+        batches = [base_cfg.batch // 2, base_cfg.batch, 2 * base_cfg.batch, 4 * base_cfg.batch]
     for B in batches:
         cfg = workloads.scaled_down(base_cfg, batch=B)
         batch = workloads.make_batch(cfg)
@@ -208,10 +216,16 @@ def compare_precision(args, dev):
             st.set_batch(batch)
             st.step()
             st.capture()
-            steps = max(10, min(2000, 2_000_000 // B))
-            for _ in range(3):
+            for _ in range(2):
                 st.replay()
             torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            st.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            # about half a second of replays per point
+            steps = int(max(3, min(2000, 500.0 / max(e0.elapsed_time(e1), 1e-3))))
             t0 = torch.cuda.Event(enable_timing=True)
             t1 = torch.cuda.Event(enable_timing=True)
             t0.record()
@@ -234,13 +248,16 @@ def compare_precision(args, dev):
         rows.append(row)
         print(json.dumps(row), file=sys.stderr, flush=True)
     last = rows[-1]
+    st = make_step(workloads.scaled_down(base_cfg, batch=1), dev)
+    desc = st.describe().split(", batch")[0]
+    del st
     line = {"metric": "full-precision / mixed-precision step time", "value": last["speedup"],
             "unit": "x", "n_gpus": 1, "steps": None, "warmup": 3,
             "ms_per_step": last["mixed_ms"], "higher_is_better": True, "scaling": "weak",
             "vs_baseline": None, "dtype": "f32 vs " + base_cfg.half, "data": "synthetic",
-            "config": {"workload": "MLP 512->1024->512 GELU, MSE; full precision (f32 layers, no "
-                                   "loss scaling) vs mixed precision (fp16 layers, dynamic loss "
-                                   "scaling), batch sizes " + ",".join(map(str, batches)),
+            "config": {"workload": desc + "; full precision (f32 layers, no loss scaling) vs "
+                                          "mixed precision (" + base_cfg.half + " layers, dynamic "
+                                          "loss scaling), batch sizes " + ",".join(map(str, batches)),
                        "parallelism": "none"},
             "comparison": rows, "gemm_at_largest_batch": gemm}
     print(json.dumps(line))

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libmpx.so")
 BUILD_DIR = os.path.join(PKG, "_build")
 SOURCES = ["sweep.hip", "gemm.hip", "gemm_f16.hip", "gemm_bf16.hip", "gemm_f32.hip", "support.hip",
-           "attention.hip"]
+           "support_f32.hip", "attention.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

@@ -48,6 +48,7 @@ static void split_plan(int64_t N, int64_t K, int64_t Mr, int& sp, int64_t& k_spl
 
 static GemmF32Args f32_args() {
   GemmF32Args g{};
+  g.nb1 = 1;
   g.splits = 1;
   g.k_split = INT64_MAX / 4;
   return g;
@@ -77,7 +78,7 @@ extern "C" int mpx_linear_fwd(const void* X, const void* W, const void* b, const
     g.resid = (const float*)R;
     g.pre = act ? (float*)Ypre : nullptr;
     g.act = act;
-    MPX_HIP(launch_gemm_f32(g, true, true, (hipStream_t)stream));
+    MPX_HIP(launch_gemm_f32(g, true, true, 1, (hipStream_t)stream));
     return MPX_OK;
   }
   GemmArgs g = base_args();
@@ -133,7 +134,7 @@ extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, cons
       g.M = M; g.N = K; g.K = N;
       g.lda = N; g.ldb = K; g.ldc = K;
       g.dact = x_act ? (const float*)Xpre : nullptr;
-      MPX_HIP(launch_gemm_f32(g, true, false, s));
+      MPX_HIP(launch_gemm_f32(g, true, false, 1, s));
     }
     if (dW) {
       GemmF32Args g = f32_args();
@@ -149,10 +150,10 @@ extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, cons
         g.splits = sp;
         g.k_split = ks;
         g.ws = (float*)workspace;
-        MPX_HIP(launch_gemm_f32(g, false, false, s));
+        MPX_HIP(launch_gemm_f32(g, false, false, 1, s));
         MPX_HIP(launch_splitk_reduce_f32(g.ws, sp, N * K, (float*)dW, s));
       } else {
-        MPX_HIP(launch_gemm_f32(g, false, false, s));
+        MPX_HIP(launch_gemm_f32(g, false, false, 1, s));
       }
     }
     if (db) MPX_HIP(launch_colsum_f32((const float*)dY, M, N, (float*)workspace, (float*)db, s));
@@ -217,10 +218,22 @@ extern "C" int mpx_gemm_batched(int32_t trans_a, int32_t trans_b, int64_t M, int
   clear_error();
   MPX_REQUIRE(A && B && C, "NULL operand");
   MPX_REQUIRE(M >= 1 && N >= 1 && K >= 1 && nb0 >= 1 && nb1 >= 1, "sizes must be >= 1");
-  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
   MPX_REQUIRE(nb0 * nb1 <= 65535, "at most 65535 batch entries");
   MPX_REQUIRE(ldc >= N && (trans_a ? lda >= M : lda >= K) && (trans_b ? ldb >= K : ldb >= N),
               "leading dimension too small");
+  if (dt == MPX_F32) {  // full precision
+    GemmF32Args g = f32_args();
+    g.A = (const float*)A;
+    g.B = (const float*)B;
+    g.C = (float*)C;
+    g.M = M; g.N = N; g.K = K;
+    g.lda = lda; g.ldb = ldb; g.ldc = ldc;
+    g.sA0 = sA0; g.sA1 = sA1; g.sB0 = sB0; g.sB1 = sB1; g.sC0 = sC0; g.sC1 = sC1;
+    g.nb1 = nb1;
+    MPX_HIP(launch_gemm_f32(g, trans_a == 0, trans_b != 0, nb0 * nb1, (hipStream_t)stream));
+    return MPX_OK;
+  }
   GemmArgs g = base_args();
   g.A = (const uint16_t*)A;
   g.B = (const uint16_t*)B;

@@ -15,7 +15,8 @@ namespace mpx {
 // opA(m,k) = A[m*lda + k] when ak (k-major), else A[k*lda + m];
 // opB(k,n) = B[n*ldb + k] when bk (k-major), else B[k*ldb + n].
 // splits > 1: split s sums k in [s*k_split, (s+1)*k_split) into ws[s][M][N]
-// (no epilogue); reduce_f32 then adds the splits in order.
+// (no epilogue); reduce_f32 then adds the splits in order.  Batched (splits
+// == 1): entry z = i0 * nb1 + i1 of nbatch offsets A, B, C by i0*s?0 + i1*s?1.
 struct GemmF32Args {
   const float* A;
   const float* B;
@@ -29,9 +30,10 @@ struct GemmF32Args {
   float* pre;
   const float* dact;
   int32_t act;
+  int64_t sA0, sA1, sB0, sB1, sC0, sC1, nb1;
 };
 
-hipError_t launch_gemm_f32(const GemmF32Args& g, bool ak, bool bk, hipStream_t s);
+hipError_t launch_gemm_f32(const GemmF32Args& g, bool ak, bool bk, int64_t nbatch, hipStream_t s);
 // C[i] = sum over s < splits of ws[s*MN + i], in split order
 hipError_t launch_splitk_reduce_f32(const float* ws, int splits, int64_t MN, float* C, hipStream_t s);
 // out[col] = sum over rows of X[r, col] (dense float32 X), float32 partials

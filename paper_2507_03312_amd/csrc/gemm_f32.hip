@@ -77,12 +77,23 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF32Args g) {
   const int64_t tiles_n = (g.N + kBN - 1) / kBN;
   const int64_t m0 = (int64_t)(blockIdx.x / tiles_n) * kBM;
   const int64_t n0 = (int64_t)(blockIdx.x % tiles_n) * kBN;
-  const int split = (int)blockIdx.y;
+  int split = 0;
+  const float* Ap = g.A;
+  const float* Bp = g.B;
+  int64_t offC = 0;
+  if (g.splits > 1) {
+    split = (int)blockIdx.y;
+  } else {  // batch entry
+    const int64_t i0 = blockIdx.y / g.nb1, i1 = blockIdx.y % g.nb1;
+    Ap += i0 * g.sA0 + i1 * g.sA1;
+    Bp += i0 * g.sB0 + i1 * g.sB1;
+    offC = i0 * g.sC0 + i1 * g.sC1;
+  }
   const int64_t kbeg = (int64_t)split * g.k_split;
   const int64_t kend = min(g.K, kbeg + g.k_split);
   const int nk = (int)((kend - kbeg + kBK - 1) / kBK);
-  const bool va = (reinterpret_cast<uintptr_t>(g.A) & 15u) == 0 && g.lda % 4 == 0;
-  const bool vb = (reinterpret_cast<uintptr_t>(g.B) & 15u) == 0 && g.ldb % 4 == 0;
+  const bool va = (reinterpret_cast<uintptr_t>(Ap) & 15u) == 0 && g.lda % 4 == 0;
+  const bool vb = (reinterpret_cast<uintptr_t>(Bp) & 15u) == 0 && g.ldb % 4 == 0;
 
   f32x16 acc[2][2];
 #pragma unroll
@@ -95,8 +106,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF32Args g) {
   TileF32<AK> ta;
   TileF32<BKM> tb;
   if (nk > 0) {
-    ta.load(g.A, g.lda, m0, g.M, kbeg, kend, va, tid);
-    tb.load(g.B, g.ldb, n0, g.N, kbeg, kend, vb, tid);
+    ta.load(Ap, g.lda, m0, g.M, kbeg, kend, va, tid);
+    tb.load(Bp, g.ldb, n0, g.N, kbeg, kend, vb, tid);
     ta.store(sA[0], tid);
     tb.store(sB[0], tid);
   }
@@ -106,8 +117,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF32Args g) {
     const int buf = kt & 1;
     const bool more = kt + 1 < nk;
     if (more) {  // next k tile into registers while this one is multiplied
-      ta.load(g.A, g.lda, m0, g.M, kbeg + (int64_t)(kt + 1) * kBK, kend, va, tid);
-      tb.load(g.B, g.ldb, n0, g.N, kbeg + (int64_t)(kt + 1) * kBK, kend, vb, tid);
+      ta.load(Ap, g.lda, m0, g.M, kbeg + (int64_t)(kt + 1) * kBK, kend, va, tid);
+      tb.load(Bp, g.ldb, n0, g.N, kbeg + (int64_t)(kt + 1) * kBK, kend, vb, tid);
     }
 #pragma unroll
     for (int kk = 0; kk < kBK; kk += 2) {
@@ -143,7 +154,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmF32Args g) {
           g.ws[((int64_t)split * g.M + m) * g.N + n] = v;
           continue;
         }
-        const int64_t o = m * g.ldc + n;
+        const int64_t o = offC + m * g.ldc + n;
         if (g.bias) v += g.bias[n];
         if (g.pre) g.pre[o] = v;
         if (g.act == MPX_ACT_GELU_TANH) v = gelu_tanh(v);
@@ -188,10 +199,13 @@ __global__ __launch_bounds__(256) void colsum_f32_final_kernel(const float* __re
 
 }  // namespace
 
-hipError_t launch_gemm_f32(const GemmF32Args& g, bool ak, bool bk, hipStream_t s) {
+hipError_t launch_gemm_f32(const GemmF32Args& g, bool ak, bool bk, int64_t nbatch, hipStream_t s) {
   const int64_t tiles = ((g.M + kBM - 1) / kBM) * ((g.N + kBN - 1) / kBN);
-  if (tiles > 0x7FFFFFFF || g.splits < 1 || g.splits > 65535) return hipErrorInvalidValue;
-  const dim3 grid((unsigned)tiles, (unsigned)g.splits);
+  const int64_t gy = g.splits > 1 ? g.splits : nbatch;
+  if (tiles > 0x7FFFFFFF || g.splits < 1 || gy < 1 || gy > 65535 || g.nb1 < 1 ||
+      (g.splits > 1 && nbatch != 1))
+    return hipErrorInvalidValue;
+  const dim3 grid((unsigned)tiles, (unsigned)gy);
   if (ak && bk) gemm_f32_kernel<true, true><<<grid, 256, 0, s>>>(g);
   else if (ak) gemm_f32_kernel<true, false><<<grid, 256, 0, s>>>(g);
   else if (bk) gemm_f32_kernel<false, true><<<grid, 256, 0, s>>>(g);

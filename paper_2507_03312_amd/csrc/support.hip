@@ -10,6 +10,7 @@
 #include "colsum.h"
 #include "common.h"
 #include "mfma.h"
+#include "support_f32.h"
 
 namespace mpx {
 
@@ -754,7 +755,12 @@ extern "C" int mpx_layernorm_fwd(const void* X, int64_t ldx, const void* gamma, 
   clear_error();
   MPX_REQUIRE(X && gamma && beta && Y, "NULL argument");
   MPX_REQUIRE(rows >= 1 && d >= 1 && d <= 2048 && ldx >= d, "bad sizes (1 <= d <= 2048, ldx >= d)");
-  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
+  if (dt == MPX_F32) {
+    MPX_HIP(launch_layernorm_fwd_f32((const float*)X, ldx, (const float*)gamma, (const float*)beta,
+                                     (float*)Y, mean_rstd, rows, d, (hipStream_t)stream));
+    return MPX_OK;
+  }
   const unsigned grid = (unsigned)((rows + 4 * kLnRows - 1) / (4 * kLnRows));
   hipStream_t s = (hipStream_t)stream;
   if (dt == MPX_F16)
@@ -781,7 +787,9 @@ extern "C" int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, 
   MPX_REQUIRE((dgamma == nullptr) == (dbeta == nullptr), "dgamma and dbeta go together");
   MPX_REQUIRE(dX || dgamma, "nothing to compute: dX, dgamma and dbeta are all NULL");
   MPX_REQUIRE(rows >= 1 && d >= 1 && d <= 2048 && ldx >= d && ldo >= d, "bad sizes");
-  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
+  MPX_REQUIRE(dt != MPX_F32 || d <= kLnF32MaxD, "MPX_F32 LayerNorm backward needs d <= 1024");
+  MPX_REQUIRE(dt != MPX_F32 || !d_nonfinite, "d_nonfinite is counted for half gradients only");
   float* part = nullptr;
   if (dgamma) {  // only the gamma / beta gradients use the workspace
     const size_t need = mpx_layernorm_bwd_workspace(rows, d);
@@ -790,6 +798,12 @@ extern "C" int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, 
       return MPX_ERR_WORKSPACE;
     }
     part = (float*)workspace;
+  }
+  if (dt == MPX_F32) {  // its block count equals ln_bwd_blocks: the same workspace
+    MPX_HIP(launch_layernorm_bwd_f32((const float*)X, ldx, (const float*)gamma, (const float*)dY,
+                                     (const float*)Rgrad, (float*)dX, ldo, (float*)dgamma,
+                                     (float*)dbeta, rows, d, part, (hipStream_t)stream));
+    return MPX_OK;
   }
   const int nb = ln_bwd_blocks(rows);
   hipStream_t s = (hipStream_t)stream;
@@ -835,7 +849,12 @@ extern "C" int mpx_softmax_fwd(const void* S, void* P, int64_t rows, int64_t n, 
   clear_error();
   MPX_REQUIRE(S && P, "NULL argument");
   MPX_REQUIRE(rows >= 1 && n >= 1 && n <= 1024 && ld >= n, "bad sizes (1 <= n <= 1024, ld >= n)");
-  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
+  if (dt == MPX_F32) {
+    MPX_HIP(launch_softmax_f32(false, (const float*)S, nullptr, (float*)P, rows, n, ld, scale,
+                               (hipStream_t)stream));
+    return MPX_OK;
+  }
   const unsigned grid = (unsigned)((rows + 4 * kSmRows - 1) / (4 * kSmRows));
   if (dt == MPX_F16)
     softmax_launch<MPX_F16>(false, sm_vpl(n), grid, (hipStream_t)stream, (const uint16_t*)S, nullptr,
@@ -852,7 +871,12 @@ extern "C" int mpx_softmax_bwd(const void* P, const void* dP, void* dS, int64_t 
   clear_error();
   MPX_REQUIRE(P && dP && dS, "NULL argument");
   MPX_REQUIRE(rows >= 1 && n >= 1 && n <= 1024 && ld >= n, "bad sizes (1 <= n <= 1024, ld >= n)");
-  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
+  if (dt == MPX_F32) {
+    MPX_HIP(launch_softmax_f32(true, (const float*)P, (const float*)dP, (float*)dS, rows, n, ld, scale,
+                               (hipStream_t)stream));
+    return MPX_OK;
+  }
   const unsigned grid = (unsigned)((rows + 4 * kSmRows - 1) / (4 * kSmRows));
   if (dt == MPX_F16)
     softmax_launch<MPX_F16>(true, sm_vpl(n), grid, (hipStream_t)stream, (const uint16_t*)P,
@@ -875,10 +899,17 @@ extern "C" int mpx_cross_entropy(const void* Z, int64_t ldz, const int32_t* labe
   clear_error();
   MPX_REQUIRE(Z && labels && d_state && d_loss && dZ, "NULL argument");
   MPX_REQUIRE(B >= 1 && C >= 1 && ldz >= C, "bad sizes");
-  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
   if (!workspace || ws_bytes < mpx_loss_workspace(B)) {
     set_error("mpx_cross_entropy: workspace of " + std::to_string(mpx_loss_workspace(B)) + " bytes required");
     return MPX_ERR_WORKSPACE;
+  }
+  if (dt == MPX_F32) {
+    MPX_HIP(launch_cross_entropy_f32((const float*)Z, ldz, labels, B, C, d_state, (float*)workspace,
+                                     (float*)dZ, (hipStream_t)stream));
+    mean_kernel<<<1, 256, 0, (hipStream_t)stream>>>((const float*)workspace, B, d_loss);
+    MPX_LAUNCHED();
+    return MPX_OK;
   }
   MPX_DT_DISPATCH(dt, cross_entropy_kernel, (unsigned)((B + 3) / 4), 256, stream, (const uint16_t*)Z, ldz,
                   labels, B, C, d_state, (float*)workspace, (uint16_t*)dZ);
@@ -977,7 +1008,11 @@ extern "C" int mpx_patchify_cast(const float* images, void* patches, int64_t B, 
   MPX_REQUIRE(images && patches, "NULL argument");
   MPX_REQUIRE(B >= 1 && C >= 1 && p >= 1 && H >= p && W >= p && H % p == 0 && W % p == 0,
               "bad sizes (H and W must be multiples of p)");
-  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
+  if (dt == MPX_F32) {
+    MPX_HIP(launch_patchify_f32(images, (float*)patches, B, H, W, C, p, (hipStream_t)stream));
+    return MPX_OK;
+  }
   MPX_DT_DISPATCH(dt, patchify_cast_kernel, grid_for(B * H * W * C), 256, stream, images,
                   (uint16_t*)patches, B, H, W, C, p);
   return MPX_OK;
@@ -988,7 +1023,12 @@ extern "C" int mpx_embed_assemble(const void* E, const void* cls, const void* po
   clear_error();
   MPX_REQUIRE(E && cls && pos && X, "NULL argument");
   MPX_REQUIRE(B >= 1 && T >= 2 && d >= 1, "bad sizes");
-  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
+  if (dt == MPX_F32) {
+    MPX_HIP(launch_embed_assemble_f32((const float*)E, (const float*)cls, (const float*)pos, (float*)X,
+                                      B, T, d, (hipStream_t)stream));
+    return MPX_OK;
+  }
   MPX_DT_DISPATCH(dt, embed_assemble_kernel, grid_for(B * T * d), 256, stream, (const uint16_t*)E,
                   (const uint16_t*)cls, (const uint16_t*)pos, (uint16_t*)X, B, T, d);
   return MPX_OK;
@@ -1000,7 +1040,13 @@ extern "C" int mpx_embed_assemble_bwd(const void* dX, void* dE, void* dcls, void
   clear_error();
   MPX_REQUIRE(dX && dE && dcls && dpos, "NULL argument");
   MPX_REQUIRE(B >= 1 && T >= 2 && d >= 1, "bad sizes");
-  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
+  if (dt == MPX_F32) {
+    MPX_REQUIRE(!d_nonfinite, "d_nonfinite is counted for half gradients only");
+    MPX_HIP(launch_embed_assemble_bwd_f32((const float*)dX, (float*)dE, (float*)dcls, (float*)dpos, B,
+                                          T, d, (hipStream_t)stream));
+    return MPX_OK;
+  }
   MPX_DT_DISPATCH(dt, embed_assemble_bwd_kernel, grid_for(T * d), 256, stream, (const uint16_t*)dX,
                   (uint16_t*)dE, (uint16_t*)dcls, (uint16_t*)dpos, B, T, d, d_nonfinite);
   return MPX_OK;

@@ -341,10 +341,11 @@ class MLPStep(TrainStep):
 
 
 class ViTStep(TrainStep):
-    """Pre-LayerNorm ViT (token or image input), CLS pooling, CE loss."""
+    """Pre-LayerNorm ViT (token or image input), CLS pooling, CE loss (mixed
+    or full precision; full precision takes the unfused attention and head)."""
 
-    def __init__(self, cfg, device="cuda"):
-        super().__init__(cfg, device)
+    def __init__(self, cfg, device="cuda", full_precision: bool = False):
+        super().__init__(cfg, device, full_precision)
         B, T, d, H, F, Cn = cfg.batch, cfg.tokens, cfg.d_model, cfg.heads, cfg.d_mlp, cfg.classes
         self.ldT = -(-T // 8) * 8
         M = B * T
@@ -360,8 +361,11 @@ class ViTStep(TrainStep):
         else:
             self.tok32 = torch.zeros(M, d, dtype=torch.float32, device=dev)
             self.L_tok32 = mx.TensorList([self.tok32])
-        self.x0 = z(M, d)
-        self.L_x0 = mx.TensorList([self.x0])
+        if self.full and not cfg.image:  # the float32 tokens are the input as they are
+            self.x0 = self.tok32
+        else:
+            self.x0 = z(M, d)
+            self.L_x0 = mx.TensorList([self.x0])
         self.blocks = []
         for _ in range(cfg.depth):
             self.blocks.append({
@@ -451,9 +455,11 @@ class ViTStep(TrainStep):
     def dominant_site(self):
         c = self.cfg
         M = c.batch * c.tokens
+        width = 2 if self.full else 1  # float32 operands: twice the bytes
+        prec = "f32" if self.full else c.half
         return {"name": "blk0.up.fwd", "flops": 2.0 * M * c.d_mlp * c.d_model,
-                "bytes": _linear_gelu_bytes(M, c.d_mlp, c.d_model),
-                "desc": f"linear_fwd+GELU (MLP up-projection) M={M} N={c.d_mlp} K={c.d_model} ({c.half})"}
+                "bytes": width * _linear_gelu_bytes(M, c.d_mlp, c.d_model),
+                "desc": f"linear_fwd+GELU (MLP up-projection) M={M} N={c.d_mlp} K={c.d_model} ({prec})"}
 
     def describe(self):
         c = self.cfg
@@ -476,7 +482,7 @@ class ViTStep(TrainStep):
     # batched GEMMs around the row softmax.
     def _fused_attention(self):
         c = self.cfg
-        return c.tokens <= 256 and c.head_dim == 64
+        return not self.full and c.tokens <= 256 and c.head_dim == 64
 
     def _attn_fwd(self, blk, s):
         c, dt = self.cfg, self.dt
@@ -547,7 +553,7 @@ class ViTStep(TrainStep):
                               _ptr(self.E), None, B * c.n_patches, d, c.patch_dim, dt, NONE, s)
             mx.mpx_embed_assemble(_ptr(self.E), _ptr(W("cls")), _ptr(W("pos")), _ptr(self.x0),
                                   B, T, d, dt, s)
-        else:
+        elif not self.full:
             mx.mpx_cast_to_half(self.L_tok32, self.L_x0, dt, s)
         # ---- blocks ----
         x = self.x0
@@ -572,7 +578,7 @@ class ViTStep(TrainStep):
         # down to the final LayerNorm's input are one pass per row, the same
         # bits as the separate calls (three launches instead of seven on the
         # critical path); its weight gradients follow below.
-        fused_head = Cn <= 32 and Cn * d <= 16384 and B <= 2048
+        fused_head = not self.full and Cn <= 32 and Cn * d <= 16384 and B <= 2048
         if fused_head:
             mx.mpx_classifier_head(_ptr(x), T * d, _ptr(W("lnf.g")), _ptr(W("lnf.b")),
                                    _ptr(W("head.w")), _ptr(W("head.b")), _ptr(self.labels), B, d, Cn,
@@ -663,8 +669,5 @@ class ViTStep(TrainStep):
 
 
 def make_step(cfg, device="cuda", full_precision: bool = False) -> TrainStep:
-    if cfg.kind == "mlp":
-        return MLPStep(cfg, device, full_precision)
-    if full_precision:
-        raise NotImplementedError("full-precision steps are built for the MLP only")
-    return ViTStep(cfg, device)
+    cls = MLPStep if cfg.kind == "mlp" else ViTStep
+    return cls(cfg, device, full_precision)

@@ -497,3 +497,29 @@ def test_linear_f32_matches_full_precision_oracle(mnk):
         nf = torch.zeros(1, dtype=torch.int32, device="cuda")
         mx.mpx_linear_bwd(tx.data_ptr(), None, tdy.data_ptr(), None, 0, None, gdw.data_ptr(), None,
                           M, N, K, F32, ws.data_ptr(), ws_n, nf.data_ptr(), _s())
+
+
+@pytest.mark.parametrize("tr", [(0, 1), (0, 0), (1, 0)])
+def test_gemm_batched_f32(tr):
+    """The attention products of full-precision training (per-head strided
+    operands of a fused QKV activation), against float64 products."""
+    ta, tb = tr
+    B, H, T, hd = 3, 2, 65, 64
+    M, N, K = (T, T, hd) if (ta, tb) == (0, 1) else (T, hd, T)
+    rng = np.random.default_rng(sum(tr))
+    A = rng.normal(size=(B, H, M, K) if not ta else (B, H, K, M)).astype(np.float32)
+    Bm = rng.normal(size=(B, H, N, K) if tb else (B, H, K, N)).astype(np.float32)
+    a, b = A.reshape(B * H, *A.shape[2:]), Bm.reshape(B * H, *Bm.shape[2:])
+    opa = a.transpose(0, 2, 1) if ta else a
+    opb = b.transpose(0, 2, 1) if tb else b
+    ref = np.matmul(opa.astype(np.float64), opb.astype(np.float64))
+    tA, tB = _dev32(A), _dev32(Bm)
+    C = _zeros32(B, H, M, N)
+    lda, ldb = A.shape[-1], Bm.shape[-1]
+    mx.mpx_gemm_batched(ta, tb, M, N, K, B, H, tA.data_ptr(), lda, H * A.shape[2] * lda, A.shape[2] * lda,
+                        tB.data_ptr(), ldb, H * Bm.shape[2] * ldb, Bm.shape[2] * ldb,
+                        C.data_ptr(), N, H * M * N, M * N, mx.MPX_F32, _s())
+    got = to_host(C).reshape(B * H, M, N)
+    bound = ulp(ref, "f32") + 2.0 * K * 2.0 ** -24 * np.matmul(np.abs(opa).astype(np.float64),
+                                                               np.abs(opb).astype(np.float64))
+    assert_within(got, ref, bound, "batched f32")

@@ -298,3 +298,118 @@ def test_classifier_head_limits():
     with pytest.raises(mx.MPXError, match="workspace"):
         mx.mpx_classifier_head(p, 64, p, p, p, p, p, 4, 64, 10, p, p, p, p, p, 64, p, p, mx.MPX_BF16,
                                p, 16, None, _s())
+
+
+# ------------------------------------------- full precision (MPX_F32) --
+# The float32 support ops against the oracle's float32 policy (float64
+# inside, one rounding to float32): the GPU's float32 reductions differ from
+# that by a few float32 ulps of the row's magnitude.
+
+def _f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+
+def _close32(got, ref, scale, rel=2e-6, what=""):
+    """|got - ref| <= rel * (|ref| + scale) elementwise (scale: the row's size)."""
+    got, ref = np.asarray(got, np.float64), np.asarray(ref, np.float64)
+    assert got.shape == ref.shape, what
+    err = np.abs(got - ref)
+    bnd = rel * (np.abs(ref) + scale)
+    assert np.all(err <= bnd), f"{what}: worst {err.max():.3g} (bound {bnd[np.argmax(err - bnd)]:.3g})"
+
+
+@pytest.mark.parametrize("rows,d", [(130, 384), (7, 768), (65, 100)])
+def test_layernorm_f32(rows, d):
+    pol = Policy("f32")
+    rng = np.random.default_rng(rows + d)
+    x = rng.normal(0.5, 2.0, size=(rows, d)).astype(np.float32)
+    g = rng.normal(1.0, 0.1, size=d).astype(np.float32)
+    b = rng.normal(0.0, 0.1, size=d).astype(np.float32)
+    dy = rng.normal(0, 1, size=(rows, d)).astype(np.float32)
+    r = rng.normal(0, 1, size=(rows, d)).astype(np.float32)
+    tx, tg, tb, tdy, tr = (_f32(a) for a in (x, g, b, dy, r))
+    y = torch.zeros(rows, d, device="cuda")
+    F32 = mx.MPX_F32
+    mx.mpx_layernorm_fwd(tx.data_ptr(), d, tg.data_ptr(), tb.data_ptr(), y.data_ptr(), None, rows, d,
+                         F32, _s())
+    _close32(to_host(y), ops.layernorm_fwd(pol, x, g, b), 4.0, 4e-6, "LN fwd")
+    dx = torch.zeros(rows, d, device="cuda")
+    dg, db = torch.zeros(d, device="cuda"), torch.zeros(d, device="cuda")
+    ws_n = mx.mpx_layernorm_bwd_workspace(rows, d)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), tr.data_ptr(), dx.data_ptr(),
+                         d, dg.data_ptr(), db.data_ptr(), rows, d, F32, ws.data_ptr(), ws_n, None, _s())
+    rdx, rdg, rdb = ops.layernorm_bwd(pol, x, g, dy)
+    _close32(to_host(dx), ops.add(pol, rdx, r), 4.0, 4e-6, "LN dX + R")
+    _close32(to_host(dg), rdg, math.sqrt(rows) * 4.0, 4e-6, "dgamma")
+    _close32(to_host(db), rdb, math.sqrt(rows) * 4.0, 4e-6, "dbeta")
+
+
+@pytest.mark.parametrize("rows,n,ld", [(300, 65, 72), (20, 197, 200), (4, 1024, 1024)])
+def test_softmax_f32(rows, n, ld):
+    pol = Policy("f32")
+    rng = np.random.default_rng(n)
+    s = rng.normal(0, 3, size=(rows, ld)).astype(np.float32)
+    dp = rng.normal(0, 1, size=(rows, ld)).astype(np.float32)
+    ts, tdp = _f32(s), _f32(dp)
+    p = torch.full((rows, ld), 7.0, device="cuda")
+    ds = torch.full((rows, ld), 7.0, device="cuda")
+    scale = 0.125
+    mx.mpx_softmax_fwd(ts.data_ptr(), p.data_ptr(), rows, n, ld, scale, mx.MPX_F32, _s())
+    gp = to_host(p)
+    _close32(gp[:, :n], ops.softmax_fwd(pol, s[:, :n], scale), 0.0, 4e-6, "P")
+    assert np.all(gp[:, n:] == 0)
+    mx.mpx_softmax_bwd(p.data_ptr(), tdp.data_ptr(), ds.data_ptr(), rows, n, ld, scale, mx.MPX_F32, _s())
+    gds = to_host(ds)
+    ref = ops.softmax_bwd(pol, gp[:, :n], dp[:, :n], scale)
+    _close32(gds[:, :n], ref, scale * np.abs(gp[:, :n]) * 4.0, 4e-6, "dS")
+    assert np.all(gds[:, n:] == 0)
+
+
+def test_cross_entropy_embed_patchify_f32():
+    pol = Policy("f32")
+    rng = np.random.default_rng(5)
+    B, C = 37, 100
+    z = rng.normal(0, 2, size=(B, C)).astype(np.float32)
+    y = rng.integers(0, C, size=B).astype(np.int32)
+    tz, ty = _f32(z), torch.from_numpy(y).cuda()
+    state = torch.from_numpy(np.frombuffer(np.array([1.0], np.float32).tobytes() + np.zeros(5, np.int32).tobytes(),
+                                           dtype=np.int32).copy()).cuda()
+    loss = torch.zeros(1, device="cuda")
+    dz = torch.zeros(B, C, device="cuda")
+    ws_n = mx.mpx_loss_workspace(B)
+    ws = torch.zeros(ws_n, dtype=torch.uint8, device="cuda")
+    mx.mpx_cross_entropy(tz.data_ptr(), C, ty.data_ptr(), B, C, state.data_ptr(), loss.data_ptr(),
+                         dz.data_ptr(), mx.MPX_F32, ws.data_ptr(), ws_n, _s())
+    rl, rdz = ops.ce_fwd_bwd(pol, z, y, 1.0)
+    assert abs(float(loss.item()) - rl) <= 2e-6 * abs(rl)
+    _close32(to_host(dz), rdz, 1.0 / B, 4e-6, "dZ")
+    # patches and token assembly (and its backward)
+    Bi, H, W, Ch, p, d = 2, 8, 8, 3, 4, 16
+    img = rng.uniform(0, 1, size=(Bi, H, W, Ch)).astype(np.float32)
+    G, T = (H // p) * (W // p), (H // p) * (W // p) + 1
+    pt = torch.zeros(Bi * G, p * p * Ch, device="cuda")
+    timg = _f32(img)  # kept alive: a freed temporary's memory can be reused before the launch
+    mx.mpx_patchify_cast(timg.data_ptr(), pt.data_ptr(), Bi, H, W, Ch, p, mx.MPX_F32, _s())
+    assert np.array_equal(to_host(pt), ops.patchify(img, p))
+    E = rng.normal(size=(Bi * G, d)).astype(np.float32)
+    cls = rng.normal(size=d).astype(np.float32)
+    pos = rng.normal(size=(T, d)).astype(np.float32)
+    X = torch.zeros(Bi * T, d, device="cuda")
+    tE, tcls, tpos = _f32(E), _f32(cls), _f32(pos)
+    mx.mpx_embed_assemble(tE.data_ptr(), tcls.data_ptr(), tpos.data_ptr(), X.data_ptr(),
+                          Bi, T, d, mx.MPX_F32, _s())
+    ref = np.empty((Bi, T, d), np.float32)
+    ref[:, 0] = cls + pos[0]
+    ref[:, 1:] = E.reshape(Bi, G, d) + pos[None, 1:]
+    assert np.array_equal(to_host(X), ref.reshape(Bi * T, d))
+    dX = rng.normal(size=(Bi * T, d)).astype(np.float32)
+    dE, dcls, dpos = (torch.zeros(Bi * G, d, device="cuda"), torch.zeros(d, device="cuda"),
+                      torch.zeros(T, d, device="cuda"))
+    tdX = _f32(dX)
+    mx.mpx_embed_assemble_bwd(tdX.data_ptr(), dE.data_ptr(), dcls.data_ptr(), dpos.data_ptr(), Bi, T,
+                              d, mx.MPX_F32, None, _s())
+    d3 = dX.reshape(Bi, T, d)
+    assert np.array_equal(to_host(dE), d3[:, 1:].reshape(Bi * G, d))
+    _close32(to_host(dpos), d3.astype(np.float64).sum(axis=0), 2.0, 4e-7, "dpos")
+    _close32(to_host(dcls), d3[:, 0].astype(np.float64).sum(axis=0), 2.0, 4e-7, "dcls")

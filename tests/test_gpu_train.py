@@ -243,3 +243,37 @@ def test_mlp_full_precision_graph_replay_matches_eager():
         torch.cuda.synchronize()
         for a, b in zip(eager.masters(), graphed.masters()):
             assert np.array_equal(a, b)
+
+
+@pytest.mark.parametrize("name", ["vit_block", "vit_s"])
+def test_vit_full_precision_lockstep(name):
+    """Full-precision ViT steps (float32 layers, unfused float32 attention and
+    head, no loss scaling) against the oracle's float32 step: gradients within
+    1e-4 normwise per tensor, the loss within 1e-5, masters within 1e-5 after
+    the oracle's AdamW on the GPU's own gradients."""
+    from oracle.adamw import adamw_masked
+    cfg = workloads.get(name)
+    cfg = workloads.scaled_down(cfg, batch=4, depth=2) if name == "vit_s" else \
+        workloads.scaled_down(cfg, batch=8)
+    gpu = make_step(cfg, full_precision=True)
+    batch = workloads.make_batch(cfg)
+    gpu.set_batch(batch)
+    ost = ostep.init_state(cfg)
+    for s in range(2):
+        start = ostep.TrainState(ost.names, gpu.masters(), ost.m, ost.v, ost.t, ost.scale)
+        _, loss_ref, g_ref = ostep.full_precision_step(cfg, start, batch)
+        gpu.forward_backward()
+        g_gpu = gpu.grads()
+        assert abs(gpu.loss() - loss_ref) <= 1e-5 * abs(loss_ref)
+        d = cfg.d_model
+        for nm, a, b in zip(ost.names, g_gpu, g_ref):
+            if nm.endswith("qkv.b"):  # the key bias's exact gradient is zero: rounding noise only
+                a, b = np.concatenate([a[:d], a[2 * d:]]), np.concatenate([b[:d], b[2 * d:]])
+            assert rel_norm_err(a, b) <= 1e-4, (s, nm, rel_norm_err(a, b))
+        gpu.finish()
+        p, m, v, t = adamw_masked(start.masters, start.m, start.v, g_gpu, start.t,
+                                  ostep.hp_of(cfg), True)
+        for nm, a, b in zip(ost.names, gpu.masters(), p):
+            assert np.all(np.abs(a - b) <= 1e-5 * np.maximum(np.abs(b), cfg.lr)), (s, nm)
+        ost = ostep.TrainState(ost.names, p, m, v, t, ost.scale)
+    assert int(gpu.d_step.item()) == 2
