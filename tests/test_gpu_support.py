@@ -413,3 +413,69 @@ def test_cross_entropy_embed_patchify_f32():
     assert np.array_equal(to_host(dE), d3[:, 1:].reshape(Bi * G, d))
     _close32(to_host(dpos), d3.astype(np.float64).sum(axis=0), 2.0, 4e-7, "dpos")
     _close32(to_host(dcls), d3[:, 0].astype(np.float64).sum(axis=0), 2.0, 4e-7, "dcls")
+
+
+@pytest.mark.parametrize("fmt", ["f16", "bf16"])
+def test_nonfinite_counts_of_layernorm_head_and_embedding(fmt):
+    """MPX §3.4's finite check fused into the LayerNorm, classifier-head and
+    token-assembly backward: the count each adds equals the separate check's
+    count over the parameter gradients it writes (dgamma / dbeta; dcls /
+    dpos), with cotangents large enough that some of those sums overflow."""
+    from paper_2507_03312_amd.train import pack_scale_state
+    dt = mx.DTYPES[fmt]
+    big = 30000.0 if fmt == "f16" else 1.0e38
+    rng = np.random.default_rng(3)
+    nf = torch.zeros(1, dtype=torch.int32, device="cuda")
+    ref = torch.zeros(1, dtype=torch.int32, device="cuda")
+
+    def check(grads, add_to):
+        torch.cuda.synchronize()
+        mx.mpx_unscale_check(mx.TensorList(grads), dt, 0, ref.data_ptr(), None, _s())
+        got, want = int(nf.item()), int(ref.item())
+        assert got == add_to + want and want > 0, (got, add_to, want)
+        return got
+
+    # LayerNorm: rows whose cotangent is large in every other column
+    rows, d = 96, 256
+    x = round_to(rng.normal(size=(rows, d)), fmt)
+    g = round_to(1.0 + 0.1 * rng.normal(size=d), fmt)
+    dy = rng.normal(size=(rows, d))
+    dy[:, ::2] = big
+    dy = round_to(dy, fmt)
+    tx, tg, tdy = (to_dev_half(a, fmt) for a in (x, g, dy))
+    dg, db = _empty((d,), fmt), _empty((d,), fmt)
+    wsn = mx.mpx_layernorm_bwd_workspace(rows, d)
+    ws = torch.zeros(wsn, dtype=torch.uint8, device="cuda")
+    mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), None, None, d, dg.data_ptr(),
+                         db.data_ptr(), rows, d, dt, ws.data_ptr(), wsn, nf.data_ptr(), _s())
+    total = check([dg, db], 0)
+    # token assembly backward: large CLS-position cotangents in some columns
+    B, T = 4, 5
+    dX = rng.normal(size=(B * T, d))
+    dX.reshape(B, T, d)[:, 0, :64] = big
+    dX = round_to(dX, fmt)
+    tdX = to_dev_half(dX, fmt)
+    dE, dcls, dpos = _empty((B * (T - 1), d), fmt), _empty((d,), fmt), _empty((T, d), fmt)
+    mx.mpx_embed_assemble_bwd(tdX.data_ptr(), dE.data_ptr(), dcls.data_ptr(), dpos.data_ptr(), B, T, d,
+                              dt, nf.data_ptr(), _s())
+    total = check([dcls, dpos], total)
+    # classifier head: the loss scale (and for bfloat16 a huge W) pushes the
+    # head's cotangents, and so dgamma / dbeta, past the format's range
+    Bh, C = 64, 10
+    xh = round_to(rng.normal(size=(Bh, d)), fmt)
+    w = round_to((0.5 if fmt == "f16" else 1.0e30) * rng.normal(size=(C, d)), fmt)
+    y = rng.integers(0, C, size=Bh).astype(np.int32)
+    scale = 2.0 ** 24 if fmt == "f16" else 2.0 ** 100
+    st = torch.from_numpy(pack_scale_state(scale, 0, 10)).cuda()
+    txh, tw, tb0 = to_dev_half(xh, fmt), to_dev_half(w, fmt), _empty((C,), fmt)
+    ty = torch.from_numpy(y).cuda()
+    z, dl, dxh = _empty((Bh, d), fmt), _empty((Bh, C), fmt), _empty((Bh, d), fmt)
+    dgh, dbh = _empty((d,), fmt), _empty((d,), fmt)
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    wsn = mx.mpx_classifier_head_workspace(Bh, d)
+    wsh = torch.zeros(wsn, dtype=torch.uint8, device="cuda")
+    mx.mpx_classifier_head(txh.data_ptr(), d, tg.data_ptr(), tb0.data_ptr(), tw.data_ptr(), tb0.data_ptr(),
+                           ty.data_ptr(), Bh, d, C, st.data_ptr(), z.data_ptr(), loss.data_ptr(),
+                           dl.data_ptr(), dxh.data_ptr(), d, dgh.data_ptr(), dbh.data_ptr(), dt,
+                           wsh.data_ptr(), wsn, nf.data_ptr(), _s())
+    check([dgh, dbh], total)
