@@ -138,9 +138,14 @@ __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const uint16_t* __re
 // waves that stride over the rows, which also bounds the gamma / beta
 // partials (one pair of float32 rows per workgroup).  Holding four float32
 // rows per wave instead left room for one wave per SIMD at d = 768 and ran
-// 2.4x slower (79 vs 32 us at 12608 x 768).
+// 2.4x slower (79 vs 32 us at 12608 x 768).  A call without gamma / beta
+// writes no partials and takes up to 2048 workgroups: more waves in flight
+// hide the row loads (25.3 -> 21.4 us at 12608 x 768, 22.6 -> 16.4 at
+// 16640 x 384, 11.4 -> 8.8 at 8320 x 384); more partials (1024 or 2048
+// workgroups) made the gamma / beta calls slower.
 constexpr int kLnBwdWaves = 4;
 constexpr int kLnBwdMaxBlocks = 512;
+constexpr int kLnBwdDxMaxBlocks = 2048;
 
 template <int VPL>
 struct RowH {
@@ -267,9 +272,9 @@ __global__ __launch_bounds__(64 * kLnBwdWaves) void layernorm_bwd_kernel(
   }
 }
 
-static int ln_bwd_blocks(int64_t rows) {
+static int ln_bwd_blocks(int64_t rows, bool partials = true) {
   const int64_t nb = (rows + kLnBwdWaves - 1) / kLnBwdWaves;
-  return (int)std::max<int64_t>(1, std::min<int64_t>(nb, kLnBwdMaxBlocks));
+  return (int)std::max<int64_t>(1, std::min<int64_t>(nb, partials ? kLnBwdMaxBlocks : kLnBwdDxMaxBlocks));
 }
 
 // --------------------------------------------------------------- softmax --
@@ -805,7 +810,7 @@ extern "C" int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, 
                                      (float*)dbeta, rows, d, part, (hipStream_t)stream));
     return MPX_OK;
   }
-  const int nb = ln_bwd_blocks(rows);
+  const int nb = ln_bwd_blocks(rows, part != nullptr);
   hipStream_t s = (hipStream_t)stream;
   const unsigned fin = colsum_final_blocks(2 * d);
   if (dt == MPX_F16) {
