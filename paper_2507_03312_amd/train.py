@@ -406,6 +406,8 @@ class ViTStep(TrainStep):
                   mx.mpx_layernorm_bwd_workspace(M, d))
         self.ws2 = torch.zeros(ws2, dtype=torch.uint8, device=dev)
         self.side = torch.cuda.Stream(device=dev)  # default priority
+        self.side_ln = None  # None: LayerNorm gamma / beta on the second stream
+        self.split_last_ln = True
 
     def _dominant_call(self, s):
         c, a, blk = self.cfg, self.arena, self.blocks[0]
@@ -605,14 +607,17 @@ class ViTStep(TrainStep):
             mx.mpx_linear_bwd(_ptr(X), None, _ptr(dY), None, NONE, None, _ptr(dW), _ptr(db),
                               Mr, N, K, dt, ws2p, ws2b, nf, sh)
 
-        # LayerNorm backward: with more than one block, dX alone on the step's
-        # stream and gamma / beta (re-reading X and dY) on the second stream,
-        # which takes their final column reduction off the critical path
-        # (ViT-S +1.3%, ViT-B +1.7%); a one-block model has too little work
-        # to hide it behind and keeps the single call (it measured 0.7% slower)
-        side_ln = c.depth > 1
+        # LayerNorm backward: dX alone on the step's stream and gamma / beta
+        # (re-reading X and dY) on the second stream, which takes their final
+        # column reduction off the critical path (ViT-S +1.3%, ViT-B +1.7%;
+        # the one-block model +6.2% since the dX-only call got its wider grid)
+        side_ln = True if self.side_ln is None else self.side_ln
 
         def ln_bwd(X, ldx, g, dY, R, dX, ldo, gg, gb, rows, fused=False):
+            if dX is None:  # only gamma / beta are needed
+                mx.mpx_layernorm_bwd(_ptr(X), ldx, _ptr(g), _ptr(dY), None, None, d, _ptr(gg),
+                                     _ptr(gb), rows, d, dt, wsp, wsb, nf, s)
+                return
             if fused or not side_ln:
                 mx.mpx_layernorm_bwd(_ptr(X), ldx, _ptr(g), _ptr(dY), _ptr(R), _ptr(dX), ldo,
                                      _ptr(gg), _ptr(gb), rows, d, dt, wsp, wsb, nf, s)
@@ -652,10 +657,13 @@ class ViTStep(TrainStep):
             self._attn_bwd(blk, dqkv, s)
             wgrad(blk["a"], dqkv, G(p + "qkv.w"), G(p + "qkv.b"), M, 3 * d, d)
             dgrad(W(p + "qkv.w"), dqkv, None, NONE, da, M, 3 * d, d)
-            # the backward's last LayerNorm stays one call: nothing is left to
-            # overlap its gamma / beta with
-            ln_bwd(xin, d, W(p + "ln1.g"), da, dx1, dx_out, d, G(p + "ln1.g"), G(p + "ln1.b"), M,
-                   fused=(i == 0))
+            # the backward's last LayerNorm: with token inputs nothing reads the
+            # input cotangent, so only gamma / beta are computed; with images
+            # it is split like the others (gamma / beta beside the embedding
+            # backward), unless split_last_ln is switched off
+            last_dx = None if (i == 0 and not c.image) else dx_out
+            ln_bwd(xin, d, W(p + "ln1.g"), da, dx1, last_dx, d, G(p + "ln1.g"), G(p + "ln1.b"), M,
+                   fused=(i == 0 and not self.split_last_ln))
             ev = torch.cuda.Event()
             ev.record(side)
             done.append(ev)
