@@ -179,7 +179,8 @@ int mpx_linear_fwd(const void* X, const void* W, const void* b, const void* R, v
  * (on the critical path) and dW / db can run on different streams.
  * `workspace` (device, ws_bytes) holds split-K partial sums and column
  * partials; its required size is mpx_linear_bwd_workspace(M, N, K) when dW
- * or db is requested (a dX-only call needs none).  Concurrent calls need
+ * or db is requested (a dX-only call needs none, a db-only call only the
+ * column partials, which that size always covers).  Concurrent calls need
  * separate workspaces.  d_nonfinite (nullable) counts non-finite dW and db
  * elements (MPX §3.4's check, fused into the kernels that write them).
  * dt == MPX_F32: the same products in float32 (full precision, see

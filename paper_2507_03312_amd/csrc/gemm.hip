@@ -118,7 +118,8 @@ extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, cons
   MPX_REQUIRE(x_act == MPX_ACT_NONE || !dX || Xpre, "Xpre is required with x_act");
   MPX_REQUIRE(dt != MPX_F32 || !d_nonfinite, "d_nonfinite is counted for half gradients only");
   if (dW || db) {  // only the weight and bias gradients use the workspace
-    const size_t need = mpx_linear_bwd_workspace(M, N, K);
+    // a bias-only call needs just the column partials
+    const size_t need = dW ? mpx_linear_bwd_workspace(M, N, K) : colsum_workspace(M, N) + 256;
     if (ws_bytes < need || !workspace) {
       set_error("mpx_linear_bwd: workspace of " + std::to_string(need) + " bytes required");
       return MPX_ERR_WORKSPACE;

@@ -94,7 +94,9 @@ __device__ __forceinline__ void row_stats(const RowVec<VPL>& r, int64_t d, int l
   rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + kLnEps);
 }
 
-constexpr int kLnRows = 2;  // rows per wave
+// rows per wave: one row per wave measured faster than two (12608 x 768:
+// 10.6 vs 12.9 us; 8320 x 384: 5.9 vs 6.25) and four (17.0, 7.3)
+constexpr int kLnRows = 1;
 
 template <int DT, int VPL>
 __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const uint16_t* __restrict__ X, int64_t ldx,
