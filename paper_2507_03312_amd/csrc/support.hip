@@ -520,14 +520,23 @@ __global__ __launch_bounds__(64 * kHeadWaves) void classifier_head_kernel(
     for (int v = 0; v < VPL; ++v)
 #pragma unroll
       for (int j = 0; j < 8; ++j) dz[v][j] = 0.0f;
+    const bool wvec = d % 8 == 0;  // W rows 16-byte aligned in LDS: a lane's 8 halves in one read
     for (int c = 0; c < C; ++c) {
       const float dlc = __shfl(dl, c);
       const uint16_t* wr = sW + c * d;
 #pragma unroll
-      for (int v = 0; v < VPL; ++v)
+      for (int v = 0; v < VPL; ++v) {
+        const int64_t c0 = (int64_t)v * 512 + lane * 8;
+        if (wvec && c0 + 8 <= d) {
+          const u32x4 w8 = *reinterpret_cast<const u32x4*>(wr + c0);
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
-          if (col_ok(d, lane, v, j)) dz[v][j] += dlc * h2f<DT>(wr[v * 512 + lane * 8 + j]);
+          for (int j = 0; j < 8; ++j) dz[v][j] += dlc * hx<DT>(w8, j);
+        } else {
+#pragma unroll
+          for (int j = 0; j < 8; ++j)
+            if (col_ok(d, lane, v, j)) dz[v][j] += dlc * h2f<DT>(wr[c0 + j]);
+        }
+      }
     }
     float s1 = 0.0f, s2 = 0.0f;
 #pragma unroll
