@@ -43,7 +43,7 @@ DEFAULT_CONFIG = "vit_block"
 # entry records the SHA-256 of the sources its kernel was built from; when
 # they no longer match, the figure is stale and reported as null.
 TRAFFIC = {
-    "blk0.up.fwd": {
+    "vit_block/blk0.up.fwd": {
         "fetch_kib": 13962.7, "write_kib": 49920.0,
         "fetch_factor": 262144.0 / 131088.8, "write_factor": 262144.0 / 262144.0,
         "sources": {
@@ -52,7 +52,25 @@ TRAFFIC = {
             "paper_2507_03312_amd/csrc/common.h": "8c0e81134196be66ac491faba83bf6615b277c811a71a1777f05facdde4e0e23",
         },
     },
-    "sweep": {
+    "vit_s/blk0.up.fwd": {
+        "fetch_kib": 25743.5, "write_kib": 99840.0,
+        "fetch_factor": 262144.0 / 131094.4, "write_factor": 262144.0 / 262144.0,
+        "sources": {
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "b366ba284d399186b2b6f06b2b68e0b01c0fa9e1426ce688bbe91db7f0e42c3f",
+            "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
+            "paper_2507_03312_amd/csrc/common.h": "8c0e81134196be66ac491faba83bf6615b277c811a71a1777f05facdde4e0e23",
+        },
+    },
+    "vit_b/blk0.up.fwd": {
+        "fetch_kib": 70785.7, "write_kib": 151313.1,
+        "fetch_factor": 262144.0 / 131092.9, "write_factor": 262144.0 / 262144.0,
+        "sources": {
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "b366ba284d399186b2b6f06b2b68e0b01c0fa9e1426ce688bbe91db7f0e42c3f",
+            "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
+            "paper_2507_03312_amd/csrc/common.h": "8c0e81134196be66ac491faba83bf6615b277c811a71a1777f05facdde4e0e23",
+        },
+    },
+    "sweep/adamw": {
         "fetch_kib": 686822.2, "write_kib": 1367205.2,
         "fetch_factor": 262144.0 / 131088.9, "write_factor": 262144.0 / 262144.0,
         "sources": {
@@ -64,6 +82,9 @@ TRAFFIC = {
 
 
 def traffic_bytes(name):
+    """HBM bytes of one launch of a workload's dominant kernel ("workload/site"),
+    from the stored counter readings, or None when none were taken for that
+    workload or a source they depend on has changed since."""
     """Measured HBM bytes per launch of kernel site `name`, or None."""
     import hashlib
     t = TRAFFIC.get(name)
@@ -313,7 +334,7 @@ def main():
                            "elements": sw.numel, "parallelism": "none"},
                 "roofline": {"bound": "hbm", "achieved": round(k_gbs, 1), "peak": PEAK_HBM_GBS,
                              "unit": "GB/s", "frac": round(k_gbs / PEAK_HBM_GBS, 4),
-                             "traffic": traffic_bytes("sweep"),
+                             "traffic": traffic_bytes("sweep/adamw"),
                              "kernel": "masked AdamW + half copy, 28 B/element",
                              "avg_launch_ms": round(k_ms, 4)}}
         if not args.no_cpu_baseline:
@@ -354,7 +375,7 @@ def main():
     else:
         roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(tflops / peak, 4), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
-    roof.update({"traffic": traffic_bytes(site["name"]), "algorithmic_bytes": site["bytes"],
+    roof.update({"traffic": traffic_bytes(args.config + "/" + site["name"]), "algorithmic_bytes": site["bytes"],
                  "flops": site["flops"], "kernel": site["desc"], "avg_launch_ms": round(k_ms, 5)})
     gemm = gemm_table(st, peak)
     line = {"metric": "train steps/s", "value": round(1000.0 / ms, 3), "unit": "steps/s",
