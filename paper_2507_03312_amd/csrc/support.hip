@@ -653,36 +653,48 @@ __global__ __launch_bounds__(256) void mse_final_kernel(const float* __restrict_
 
 // ------------------------------------------------------------ embeddings --
 
+// Patch vectors: workgroups over (patch, 256 elements of its vector); a
+// vector element e = i * (p C) + r is pixel row i of the patch, offset r in
+// that row's p C contiguous floats.  32-bit index math (the host checks the
+// sizes); patches stride over gridDim.y.
 template <int DT>
 __global__ __launch_bounds__(256) void patchify_cast_kernel(const float* __restrict__ img,
-                                                            uint16_t* __restrict__ out, int64_t B,
-                                                            int64_t H, int64_t W, int64_t C, int64_t p) {
-  const int64_t pd = p * p * C;
-  const int64_t gw = W / p, gh = H / p;
-  const int64_t total = B * gh * gw * pd;
-  for (int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x; o < total; o += (int64_t)gridDim.x * 256) {
-    const int64_t row = o / pd, e = o % pd;
-    const int64_t b = row / (gh * gw), g = row % (gh * gw);
-    const int64_t gy = g / gw, gx = g % gw;
-    const int64_t i = e / (p * C), j = (e / C) % p, c = e % C;
-    out[o] = f2h<DT>(img[((b * H + gy * p + i) * W + gx * p + j) * C + c]);
+                                                            uint16_t* __restrict__ out, int B, int H,
+                                                            int W, int C, int p) {
+  const int pc = p * C, pd = p * pc;
+  const int gw = W / p, G = (H / p) * gw;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= pd) return;
+  const int i = e / pc, r = e - i * pc;
+  for (int row = blockIdx.y; row < B * G; row += gridDim.y) {
+    const int b = row / G, g = row - b * G;
+    const int gy = g / gw, gx = g - gy * gw;
+    const int64_t src = (((int64_t)b * H + gy * p + i) * W + (int64_t)gx * p) * C + r;
+    out[(int64_t)row * pd + e] = f2h<DT>(img[src]);
   }
 }
 
+// Token rows: workgroups over (256 columns, row); rows stride over gridDim.y.
 template <int DT>
 __global__ __launch_bounds__(256) void embed_assemble_kernel(const uint16_t* __restrict__ E,
                                                              const uint16_t* __restrict__ cls,
                                                              const uint16_t* __restrict__ pos,
-                                                             uint16_t* __restrict__ X, int64_t B,
-                                                             int64_t T, int64_t d) {
-  const int64_t total = B * T * d;
-  for (int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x; o < total; o += (int64_t)gridDim.x * 256) {
-    const int64_t b = o / (T * d), t = (o / d) % T, c = o % d;
-    const float base = t == 0 ? h2f<DT>(cls[c]) : h2f<DT>(E[(b * (T - 1) + t - 1) * d + c]);
-    X[o] = f2h<DT>(base + h2f<DT>(pos[t * d + c]));
+                                                             uint16_t* __restrict__ X, int B, int T,
+                                                             int64_t d) {
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= d) return;
+  for (int row = blockIdx.y; row < B * T; row += gridDim.y) {
+    const int b = row / T, t = row - b * T;
+    const float base = t == 0 ? h2f<DT>(cls[c]) : h2f<DT>(E[((int64_t)b * (T - 1) + t - 1) * d + c]);
+    X[(int64_t)row * d + c] = f2h<DT>(base + h2f<DT>(pos[(int64_t)t * d + c]));
   }
 }
 
+// Backward: dE rows are copies of the dX rows t > 0; dpos (and dcls, its
+// t = 0 row) are column sums over the batch.  A wave owns 64 consecutive
+// (t, c) outputs and the workgroup's four waves split the batch (b = w mod
+// 4), so every access is 128 contiguous bytes; the four partial sums are
+// added in a fixed order.
 template <int DT>
 __global__ __launch_bounds__(256) void embed_assemble_bwd_kernel(const uint16_t* __restrict__ dX,
                                                                  uint16_t* __restrict__ dE,
@@ -690,20 +702,28 @@ __global__ __launch_bounds__(256) void embed_assemble_bwd_kernel(const uint16_t*
                                                                  uint16_t* __restrict__ dpos,
                                                                  int64_t B, int64_t T, int64_t d,
                                                                  int32_t* __restrict__ nonfinite) {
+  __shared__ float red[4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int64_t total = T * d;
-  for (int64_t o = (int64_t)blockIdx.x * 256 + threadIdx.x; o < total; o += (int64_t)gridDim.x * 256) {
-    const int64_t t = o / d, c = o % d;
-    float s = 0.0f;
-    for (int64_t b = 0; b < B; ++b) {
-      const uint16_t v = dX[b * T * d + o];
+  const int64_t o = (int64_t)blockIdx.x * 64 + lane;
+  float s = 0.0f;
+  if (o < total) {
+    const bool body = o >= d;  // t > 0: a patch token, copied to dE
+#pragma unroll 4
+    for (int64_t b = w; b < B; b += 4) {
+      const uint16_t v = dX[b * total + o];
       s += h2f<DT>(v);
-      if (t > 0) dE[(b * (T - 1) + t - 1) * d + c] = v;
+      if (body) dE[b * (total - d) + (o - d)] = v;
     }
-    const uint16_t h = f2h<DT>(s);
+  }
+  red[w][lane] = s;
+  __syncthreads();
+  if (w == 0 && o < total) {
+    const uint16_t h = f2h<DT>((red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]));
     dpos[o] = h;
-    if (t == 0) dcls[c] = h;
+    if (o < d) dcls[o] = h;
     // dpos and, for the CLS position, dcls: one or two parameter elements
-    if (nonfinite) add_nonfinite(nonfinite, h_nonfinite<DT>(h) ? (t == 0 ? 2 : 1) : 0);
+    if (nonfinite) add_nonfinite(nonfinite, h_nonfinite<DT>(h) ? (o < d ? 2 : 1) : 0);
   }
 }
 
@@ -1029,8 +1049,13 @@ extern "C" int mpx_patchify_cast(const float* images, void* patches, int64_t B, 
     MPX_HIP(launch_patchify_f32(images, (float*)patches, B, H, W, C, p, (hipStream_t)stream));
     return MPX_OK;
   }
-  MPX_DT_DISPATCH(dt, patchify_cast_kernel, grid_for(B * H * W * C), 256, stream, images,
-                  (uint16_t*)patches, B, H, W, C, p);
+  MPX_REQUIRE(B * H * W * C < ((int64_t)1 << 31), "at most 2^31 - 1 image values");
+  {
+    const int64_t pd = p * p * C, rows = B * (H / p) * (W / p);
+    const dim3 grid((unsigned)((pd + 255) / 256), (unsigned)std::min<int64_t>(rows, 65535));
+    MPX_DT_DISPATCH(dt, patchify_cast_kernel, grid, 256, stream, images, (uint16_t*)patches, (int)B,
+                    (int)H, (int)W, (int)C, (int)p);
+  }
   return MPX_OK;
 }
 
@@ -1045,8 +1070,12 @@ extern "C" int mpx_embed_assemble(const void* E, const void* cls, const void* po
                                       B, T, d, (hipStream_t)stream));
     return MPX_OK;
   }
-  MPX_DT_DISPATCH(dt, embed_assemble_kernel, grid_for(B * T * d), 256, stream, (const uint16_t*)E,
-                  (const uint16_t*)cls, (const uint16_t*)pos, (uint16_t*)X, B, T, d);
+  MPX_REQUIRE(B * T < ((int64_t)1 << 31), "at most 2^31 - 1 token rows");
+  {
+    const dim3 grid((unsigned)((d + 255) / 256), (unsigned)std::min<int64_t>(B * T, 65535));
+    MPX_DT_DISPATCH(dt, embed_assemble_kernel, grid, 256, stream, (const uint16_t*)E,
+                    (const uint16_t*)cls, (const uint16_t*)pos, (uint16_t*)X, (int)B, (int)T, d);
+  }
   return MPX_OK;
 }
 
@@ -1063,8 +1092,9 @@ extern "C" int mpx_embed_assemble_bwd(const void* dX, void* dE, void* dcls, void
                                           T, d, (hipStream_t)stream));
     return MPX_OK;
   }
-  MPX_DT_DISPATCH(dt, embed_assemble_bwd_kernel, grid_for(T * d), 256, stream, (const uint16_t*)dX,
-                  (uint16_t*)dE, (uint16_t*)dcls, (uint16_t*)dpos, B, T, d, d_nonfinite);
+  MPX_DT_DISPATCH(dt, embed_assemble_bwd_kernel, (unsigned)((T * d + 63) / 64), 256, stream,
+                  (const uint16_t*)dX, (uint16_t*)dE, (uint16_t*)dcls, (uint16_t*)dpos, B, T, d,
+                  d_nonfinite);
   return MPX_OK;
 }
 

@@ -205,9 +205,10 @@ def test_mse(fmt):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
-def test_patchify_embed_assemble_and_backward(fmt):
+@pytest.mark.parametrize("B,Hh,C,p,d", [(3, 8, 3, 4, 16), (9, 32, 3, 4, 384), (2, 48, 3, 16, 100)],
+                         ids=lambda v: str(v))
+def test_patchify_embed_assemble_and_backward(fmt, B, Hh, C, p, d):
     pol = Policy(fmt)
-    B, Hh, C, p, d = 3, 8, 3, 4, 16
     G = (Hh // p) ** 2
     T = G + 1
     img = np.random.default_rng(1).uniform(0, 1, (B, Hh, Hh, C)).astype(np.float32)
