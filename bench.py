@@ -44,38 +44,38 @@ DEFAULT_CONFIG = "vit_block"
 # they no longer match, the figure is stale and reported as null.
 TRAFFIC = {
     "vit_block/blk0.up.fwd": {
-        "fetch_kib": 13962.7, "write_kib": 49920.0,
-        "fetch_factor": 262144.0 / 131088.8, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 13932.2, "write_kib": 49920.0,
+        "fetch_factor": 262144.0 / 131089.0, "write_factor": 262144.0 / 262144.0,
         "sources": {
             "paper_2507_03312_amd/csrc/gemm_kernels.h": "b366ba284d399186b2b6f06b2b68e0b01c0fa9e1426ce688bbe91db7f0e42c3f",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
-            "paper_2507_03312_amd/csrc/common.h": "8c0e81134196be66ac491faba83bf6615b277c811a71a1777f05facdde4e0e23",
+            "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
     },
     "vit_s/blk0.up.fwd": {
-        "fetch_kib": 25743.5, "write_kib": 99840.0,
-        "fetch_factor": 262144.0 / 131094.4, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 25552.8, "write_kib": 99840.0,
+        "fetch_factor": 262144.0 / 131094.2, "write_factor": 262144.0 / 262144.0,
         "sources": {
             "paper_2507_03312_amd/csrc/gemm_kernels.h": "b366ba284d399186b2b6f06b2b68e0b01c0fa9e1426ce688bbe91db7f0e42c3f",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
-            "paper_2507_03312_amd/csrc/common.h": "8c0e81134196be66ac491faba83bf6615b277c811a71a1777f05facdde4e0e23",
+            "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
     },
     "vit_b/blk0.up.fwd": {
-        "fetch_kib": 70785.7, "write_kib": 151313.1,
-        "fetch_factor": 262144.0 / 131092.9, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 70847.6, "write_kib": 151310.6,
+        "fetch_factor": 262144.0 / 131091.0, "write_factor": 262144.0 / 262144.0,
         "sources": {
             "paper_2507_03312_amd/csrc/gemm_kernels.h": "b366ba284d399186b2b6f06b2b68e0b01c0fa9e1426ce688bbe91db7f0e42c3f",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
-            "paper_2507_03312_amd/csrc/common.h": "8c0e81134196be66ac491faba83bf6615b277c811a71a1777f05facdde4e0e23",
+            "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
     },
     "sweep/adamw": {
-        "fetch_kib": 686822.2, "write_kib": 1367205.2,
-        "fetch_factor": 262144.0 / 131088.9, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 686822.3, "write_kib": 1367203.6,
+        "fetch_factor": 262144.0 / 131089.0, "write_factor": 262144.0 / 262144.0,
         "sources": {
             "paper_2507_03312_amd/csrc/sweep.hip": "c602435f1b696d1b01bd40828d85fbd12bbbce651354540e554f5fb723602496",
-            "paper_2507_03312_amd/csrc/common.h": "8c0e81134196be66ac491faba83bf6615b277c811a71a1777f05facdde4e0e23",
+            "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
     },
 }

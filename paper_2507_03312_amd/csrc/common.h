@@ -100,10 +100,14 @@ __device__ __forceinline__ float gelu_sigma(float x) {
   return __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(x * __builtin_fmaf(k2, x * x, k1)));
 }
 __device__ __forceinline__ float gelu_tanh(float x) { return x * gelu_sigma(x); }
+// gelu'(x) = s + s (1 - s) x (2c + 6ac x^2): four fused operations after sigma
+// (s (1 - s) as s - s^2; the bracket as one fma on x^2).
 __device__ __forceinline__ float gelu_tanh_grad(float x) {
-  const float c = 0.7978845608028654f, a = 0.044715f;
+  const float k2 = 1.5957691216057308f;   // 2c
+  const float k6 = 0.21406444881780073f;  // 6ac
   const float s = gelu_sigma(x);
-  return s + 2.0f * x * s * (1.0f - s) * c * (1.0f + 3.0f * a * x * x);
+  const float u = __builtin_fmaf(-s, s, s);
+  return __builtin_fmaf(u, x * __builtin_fmaf(k6, x * x, k2), s);
 }
 
 // ------------------------------------------------------------ reductions --
