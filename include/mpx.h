@@ -256,6 +256,16 @@ int mpx_layernorm_fwd(const void* X, int64_t ldx, const void* gamma, const void*
                       void* Y, float* mean_rstd, int64_t rows, int64_t d, mpx_dtype dt,
                       void* stream);
 
+/* The input cast of MPX §3.4 fused with a first LayerNorm (a model whose
+ * float32 inputs feed a pre-LayerNorm block): X float32 [rows, d] with row
+ * stride ldx; Xh = half(X) [rows, d] dense (round to nearest even), and Y,
+ * mean_rstd exactly as mpx_layernorm_fwd(Xh, d, gamma, beta, Y, mean_rstd)
+ * gives them: the same bits as mpx_cast_to_half followed by that call, in one
+ * pass.  1 <= d <= 2048; half dtypes only. */
+int mpx_layernorm_fwd_cast(const float* X, int64_t ldx, const void* gamma, const void* beta,
+                           void* Xh, void* Y, float* mean_rstd, int64_t rows, int64_t d,
+                           mpx_dtype dt, void* stream);
+
 /* LayerNorm backward.  dX = half(dLN) or, if Rgrad != NULL, dX = half(Rgrad +
  * half(dLN)) (the residual branch's cotangent added after the LN cotangent is
  * rounded).  X has row stride ldx; dX, dY, Rgrad are dense [rows, d] unless

@@ -67,6 +67,7 @@ _SIGS = {
     "mpx_attention_bwd": (C.c_int, [P, P, P, P, I64, I64, I64, I64, I32, P, SZ, P]),
     "mpx_attention_bwd_workspace": (SZ, [I64, I64, I64, I64]),
     "mpx_layernorm_fwd": (C.c_int, [P, I64, P, P, P, P, I64, I64, I32, P]),
+    "mpx_layernorm_fwd_cast": (C.c_int, [P, I64, P, P, P, P, P, I64, I64, I32, P]),
     "mpx_layernorm_bwd": (C.c_int, [P, I64, P, P, P, P, I64, P, P, I64, I64, I32, P, SZ, P, P]),
     "mpx_layernorm_bwd_workspace": (SZ, [I64, I64]),
     "mpx_softmax_fwd": (C.c_int, [P, P, I64, I64, I64, F, I32, P]),
@@ -169,6 +170,7 @@ mpx_gemm_set_config = _call("mpx_gemm_set_config")
 mpx_attention_fwd = _call("mpx_attention_fwd")
 mpx_attention_bwd = _call("mpx_attention_bwd")
 mpx_layernorm_fwd = _call("mpx_layernorm_fwd")
+mpx_layernorm_fwd_cast = _call("mpx_layernorm_fwd_cast")
 mpx_layernorm_bwd = _call("mpx_layernorm_bwd")
 mpx_softmax_fwd = _call("mpx_softmax_fwd")
 mpx_softmax_bwd = _call("mpx_softmax_bwd")

@@ -73,6 +73,19 @@ __device__ __forceinline__ bool col_ok(int64_t d, int lane, int v, int j) {
   return (int64_t)v * 512 + lane * 8 + j < d;
 }
 
+// LayerNorm output before rounding, (x - mean) rstd gamma + beta, with the
+// last multiply-add fused explicitly and its float32 result kept as such (the
+// empty asm): left alone, the compiler may turn the multiply-add and the
+// rounding to half into one mixed-precision fma that rounds the exact value
+// once, which differs from rounding the float32 value on half-way cases.
+// Every kernel that normalises a row (the forward, its fused input-cast
+// form, the classifier head) so rounds the same float32 value.
+__device__ __forceinline__ float ln_affine(float x, float mean, float rstd, float g, float b) {
+  float y = __builtin_fmaf((x - mean) * rstd, g, b);
+  asm volatile("" : "+v"(y));
+  return y;
+}
+
 // mean and 1/sqrt(var + eps) of one row held by a wave (two-pass)
 template <int VPL>
 __device__ __forceinline__ void row_stats(const RowVec<VPL>& r, int64_t d, int lane, float& mean,
@@ -123,12 +136,67 @@ __global__ __launch_bounds__(256) void layernorm_fwd_kernel(const uint16_t* __re
 #pragma unroll
     for (int v = 0; v < VPL; ++v)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) h[v][j] = f2h<DT>((x[i].x[v][j] - mean) * rstd * g.x[v][j] + b.x[v][j]);
+      for (int j = 0; j < 8; ++j) h[v][j] = f2h<DT>(ln_affine(x[i].x[v][j], mean, rstd, g.x[v][j], b.x[v][j]));
     store_row<DT, VPL>(Y + (r0 + i) * d, d, lane, h);
     if (mr && lane == 0) {
       mr[2 * (r0 + i)] = mean;
       mr[2 * (r0 + i) + 1] = rstd;
     }
+  }
+}
+
+// The input cast (§3.4) fused with the first LayerNorm: each float32 value
+// is rounded to half, the half row is written out (the residual stream needs
+// it) and normalised exactly as layernorm_fwd_kernel normalises that half
+// row, so both outputs are the bits of the cast followed by the LayerNorm.
+template <int DT, int VPL>
+__global__ __launch_bounds__(256) void layernorm_fwd_cast_kernel(
+    const float* __restrict__ X, int64_t ldx, const uint16_t* __restrict__ gamma,
+    const uint16_t* __restrict__ beta, uint16_t* __restrict__ Xh, uint16_t* __restrict__ Y,
+    float* __restrict__ mr, int64_t rows, int64_t d) {
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= rows) return;
+  const float* xr = X + r * ldx;
+  RowVec<VPL> x;
+  uint16_t xh[VPL][8];
+#pragma unroll
+  for (int v = 0; v < VPL; ++v) {
+    const int64_t c = (int64_t)v * 512 + lane * 8;
+    float f[8];
+    if (c + 8 <= d && (reinterpret_cast<uintptr_t>(xr + c) & 15u) == 0) {
+      const f32x4 a = *reinterpret_cast<const f32x4*>(xr + c);
+      const f32x4 b = *reinterpret_cast<const f32x4*>(xr + c + 4);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        f[j] = a[j];
+        f[4 + j] = b[j];
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < 8; ++j) f[j] = c + j < d ? xr[c + j] : 0.0f;
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      xh[v][j] = f2h<DT>(f[j]);
+      x.x[v][j] = col_ok(d, lane, v, j) ? h2f<DT>(xh[v][j]) : 0.0f;
+    }
+  }
+  store_row<DT, VPL>(Xh + r * d, d, lane, xh);
+  RowVec<VPL> g, b;
+  load_row<DT, VPL>(gamma, d, lane, g);
+  load_row<DT, VPL>(beta, d, lane, b);
+  float mean, rstd;
+  row_stats<VPL>(x, d, lane, mean, rstd);
+  uint16_t h[VPL][8];
+#pragma unroll
+  for (int v = 0; v < VPL; ++v)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) h[v][j] = f2h<DT>(ln_affine(x.x[v][j], mean, rstd, g.x[v][j], b.x[v][j]));
+  store_row<DT, VPL>(Y + r * d, d, lane, h);
+  if (mr && lane == 0) {
+    mr[2 * r] = mean;
+    mr[2 * r + 1] = rstd;
   }
 }
 
@@ -476,7 +544,7 @@ __global__ __launch_bounds__(64 * kHeadWaves) void classifier_head_kernel(
 #pragma unroll
     for (int v = 0; v < VPL; ++v)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) zh[v][j] = f2h<DT>((x.x[v][j] - mean) * rstd * g.x[v][j] + be.x[v][j]);
+      for (int j = 0; j < 8; ++j) zh[v][j] = f2h<DT>(ln_affine(x.x[v][j], mean, rstd, g.x[v][j], be.x[v][j]));
     store_row<DT, VPL>(Z + r * d, d, lane, zh);
     uint16_t* zs = zrow[wave];
 #pragma unroll
@@ -805,6 +873,34 @@ extern "C" int mpx_layernorm_fwd(const void* X, int64_t ldx, const void* gamma, 
   else
     ln_fwd_launch<MPX_BF16>(vpl_for(d), grid, s, (const uint16_t*)X, ldx, (const uint16_t*)gamma,
                             (const uint16_t*)beta, (uint16_t*)Y, mean_rstd, rows, d);
+  MPX_LAUNCHED();
+  return MPX_OK;
+}
+
+extern "C" int mpx_layernorm_fwd_cast(const float* X, int64_t ldx, const void* gamma,
+                                      const void* beta, void* Xh, void* Y, float* mean_rstd,
+                                      int64_t rows, int64_t d, mpx_dtype dt, void* stream) {
+  clear_error();
+  MPX_REQUIRE(X && gamma && beta && Xh && Y, "NULL argument");
+  MPX_REQUIRE(rows >= 1 && d >= 1 && d <= 2048 && ldx >= d, "bad sizes (1 <= d <= 2048, ldx >= d)");
+  MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
+  const unsigned grid = (unsigned)((rows + 3) / 4);
+  hipStream_t s = (hipStream_t)stream;
+  const int vpl = vpl_for(d);
+#define MPX_LNC(DTv, V)                                                                          \
+  layernorm_fwd_cast_kernel<DTv, V><<<grid, 256, 0, s>>>(X, ldx, (const uint16_t*)gamma,        \
+                                                         (const uint16_t*)beta, (uint16_t*)Xh,  \
+                                                         (uint16_t*)Y, mean_rstd, rows, d)
+  if (dt == MPX_F16) {
+    if (vpl == 1) MPX_LNC(MPX_F16, 1);
+    else if (vpl == 2) MPX_LNC(MPX_F16, 2);
+    else MPX_LNC(MPX_F16, 4);
+  } else {
+    if (vpl == 1) MPX_LNC(MPX_BF16, 1);
+    else if (vpl == 2) MPX_LNC(MPX_BF16, 2);
+    else MPX_LNC(MPX_BF16, 4);
+  }
+#undef MPX_LNC
   MPX_LAUNCHED();
   return MPX_OK;
 }

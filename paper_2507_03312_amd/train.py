@@ -557,14 +557,20 @@ class ViTStep(TrainStep):
                               _ptr(self.E), None, B * c.n_patches, d, c.patch_dim, dt, NONE, s)
             mx.mpx_embed_assemble(_ptr(self.E), _ptr(W("cls")), _ptr(W("pos")), _ptr(self.x0),
                                   B, T, d, dt, s)
-        elif not self.full:
-            mx.mpx_cast_to_half(self.L_tok32, self.L_x0, dt, s)
+        # token inputs in mixed precision: their cast to half is fused with
+        # the first block's LayerNorm (one pass instead of two)
+        cast_in_ln = not c.image and not self.full
         # ---- blocks ----
         x = self.x0
         for i, blk in enumerate(self.blocks):
             p = f"blk{i}."
-            mx.mpx_layernorm_fwd(_ptr(x), d, _ptr(W(p + "ln1.g")), _ptr(W(p + "ln1.b")),
-                                 _ptr(blk["a"]), None, M, d, dt, s)
+            if i == 0 and cast_in_ln:
+                mx.mpx_layernorm_fwd_cast(_ptr(self.tok32), d, _ptr(W(p + "ln1.g")),
+                                          _ptr(W(p + "ln1.b")), _ptr(self.x0), _ptr(blk["a"]), None,
+                                          M, d, dt, s)
+            else:
+                mx.mpx_layernorm_fwd(_ptr(x), d, _ptr(W(p + "ln1.g")), _ptr(W(p + "ln1.b")),
+                                     _ptr(blk["a"]), None, M, d, dt, s)
             mx.mpx_linear_fwd(_ptr(blk["a"]), _ptr(W(p + "qkv.w")), _ptr(W(p + "qkv.b")), None,
                               _ptr(blk["qkv"]), None, M, 3 * d, d, dt, NONE, s)
             self._attn_fwd(blk, s)

@@ -480,3 +480,30 @@ def test_nonfinite_counts_of_layernorm_head_and_embedding(fmt):
                            dl.data_ptr(), dxh.data_ptr(), d, dgh.data_ptr(), dbh.data_ptr(), dt,
                            wsh.data_ptr(), wsn, nf.data_ptr(), _s())
     check([dgh, dbh], total)
+
+
+@pytest.mark.parametrize("fmt", ["f16", "bf16"])
+@pytest.mark.parametrize("rows,d,ldx", [(8320, 384, 384), (65, 100, 104), (7, 768, 768), (33, 1500, 1501)])
+def test_layernorm_fwd_cast_matches_cast_then_layernorm(fmt, rows, d, ldx):
+    """The input cast fused with the first LayerNorm gives the same bits as
+    the cast followed by the LayerNorm (both outputs and the row stats)."""
+    dt = mx.DTYPES[fmt]
+    rng = np.random.default_rng(rows + d)
+    x = rng.normal(0.3, 1.5, size=(rows, ldx)).astype(np.float32)
+    g = to_dev_half(round_to(1.0 + 0.1 * rng.normal(size=d), fmt), fmt)
+    b = to_dev_half(round_to(0.1 * rng.normal(size=d), fmt), fmt)
+    tx = torch.from_numpy(x).cuda()
+    xh1, y1 = _empty((rows, d), fmt), _empty((rows, d), fmt)
+    mr1 = torch.zeros(rows, 2, device="cuda")
+    mx.mpx_layernorm_fwd_cast(tx.data_ptr(), ldx, g.data_ptr(), b.data_ptr(), xh1.data_ptr(), y1.data_ptr(),
+                              mr1.data_ptr(), rows, d, dt, _s())
+    # reference: the cast (x as dense rows), then the LayerNorm
+    tdense = torch.from_numpy(np.ascontiguousarray(x[:, :d])).cuda()
+    xh2, y2 = _empty((rows, d), fmt), _empty((rows, d), fmt)
+    mr2 = torch.zeros(rows, 2, device="cuda")
+    src, dst = mx.TensorList([tdense]), mx.TensorList([xh2])
+    mx.mpx_cast_to_half(src, dst, dt, _s())
+    mx.mpx_layernorm_fwd(xh2.data_ptr(), d, g.data_ptr(), b.data_ptr(), y2.data_ptr(), mr2.data_ptr(), rows, d,
+                         dt, _s())
+    torch.cuda.synchronize()
+    assert torch.equal(xh1, xh2) and torch.equal(y1, y2) and torch.equal(mr1, mr2)
