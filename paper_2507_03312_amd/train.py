@@ -230,9 +230,11 @@ class TrainStep:
         step, as the step issues it; each does 2 M N K flops."""
         return []
 
-    def time_call(self, call, launches: int = 20, reps: int = 5) -> float:
-        """Mean duration (ms) of ``call(stream)`` from HIP events around a graph
-        of ``launches`` back-to-back calls, replayed ``reps`` times."""
+    def time_call(self, call, launches: int = 20, reps: int = 5, groups: int = 5) -> float:
+        """Duration (ms) of one ``call(stream)``: HIP events around ``reps``
+        replays of a graph of ``launches`` back-to-back calls give one mean per
+        group; the median over ``groups`` such groups is returned (one group
+        alone moved by up to a third from box to box)."""
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
@@ -240,13 +242,16 @@ class TrainStep:
                 call(_stream())
         g.replay()
         torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(reps):
-            g.replay()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / (reps * launches)
+        means = []
+        for _ in range(groups):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                g.replay()
+            e1.record()
+            torch.cuda.synchronize()
+            means.append(e0.elapsed_time(e1) / (reps * launches))
+        return sorted(means)[groups // 2]
 
     def inject(self, tensor: int, element: int, value: float):
         """Harness fault injection: overwrite one gradient element (after the
