@@ -10,9 +10,9 @@ the step runs as one captured HIP graph.
 
 Prints ONE JSON line.  `value` is train steps/s for the model workloads (or
 unscale+AdamW GB/s for the optimizer sweep).  `roofline` covers the dominant
-kernel: its mean launch duration comes from HIP events around a graph of
+kernel: its launch duration comes from HIP events around a graph of
 back-to-back launches with the step's own operands, on the stream they run
-on; `bound` is whichever of the MFMA and HBM ceilings is the binding one for
+on (the median of five groups of replays); `bound` is whichever of the MFMA and HBM ceilings is the binding one for
 its algorithmic flops and bytes (`frac` against that one; the other fraction
 is given too).  `traffic` is the HBM bytes per launch from the FETCH_SIZE /
 WRITE_SIZE counters, scaled by a plain copy's reading, or null when the
