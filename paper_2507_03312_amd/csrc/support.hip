@@ -556,16 +556,31 @@ __global__ __launch_bounds__(64 * kHeadWaves) void classifier_head_kernel(
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
+    // logits two classes at a time (two independent chains, each in the
+    // skinny product kernel's order: k = lane, lane + 64, ..., then the xor
+    // butterfly and lane 0's value)
     float logit = -INFINITY;  // lane c < C: class c
-    for (int c = 0; c < C; ++c) {
-      const uint16_t* wr = sW + c * d;
-      float acc = 0.0f;
-      for (int64_t k = lane; k < d; k += 64) acc += h2f<DT>(zs[k]) * h2f<DT>(wr[k]);
+    for (int c = 0; c < C; c += 2) {
+      const bool two = c + 1 < C;
+      const uint16_t* w0 = sW + c * d;
+      const uint16_t* w1 = sW + (two ? c + 1 : c) * d;
+      float a0 = 0.0f, a1 = 0.0f;
+      for (int k = lane; k < (int)d; k += 64) {
+        const float zk = h2f<DT>(zs[k]);
+        a0 += zk * h2f<DT>(w0[k]);
+        a1 += zk * h2f<DT>(w1[k]);
+      }
 #pragma unroll
-      for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
-      acc = __shfl(acc, 0);
-      const float lg = h2f<DT>(f2h<DT>(acc + h2f<DT>(bias[c])));
-      if (lane == c) logit = lg;
+      for (int o = 32; o >= 1; o >>= 1) {
+        a0 += __shfl_xor(a0, o);
+        a1 += __shfl_xor(a1, o);
+      }
+      const float l0 = h2f<DT>(f2h<DT>(__shfl(a0, 0) + h2f<DT>(bias[c])));
+      if (lane == c) logit = l0;
+      if (two) {
+        const float l1 = h2f<DT>(f2h<DT>(__shfl(a1, 0) + h2f<DT>(bias[c + 1])));
+        if (lane == c + 1) logit = l1;
+      }
     }
     const float scale = st->scale;
     const int32_t y = labels[r];
