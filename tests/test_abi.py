@@ -41,3 +41,22 @@ def test_binding_loads_and_covers_the_header():
     # a pure host call: size queries need no device
     assert binding.mpx_linear_bwd_workspace(64, 512, 1024) > 0
     assert binding.mpx_layernorm_bwd_workspace(100, 384) > 0
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="libmpx.so not built")
+def test_argument_checks_of_the_float32_and_fused_paths():
+    """Host-side argument checks return an error before anything is
+    dereferenced or launched (the pointers here are placeholders)."""
+    from paper_2507_03312_amd import binding as mx
+    p = 256  # never dereferenced: every call below fails its checks first
+    with pytest.raises(mx.MPXError, match="d <= 1024"):
+        mx.mpx_layernorm_bwd(p, 2048, p, p, None, p, 2048, None, None, 4, 2048, mx.MPX_F32, None, 0,
+                             None, 0)
+    with pytest.raises(mx.MPXError, match="half gradients only"):
+        mx.mpx_linear_bwd(p, None, p, None, 0, None, p, None, 8, 8, 8, mx.MPX_F32, p, 1 << 20, p, 0)
+    with pytest.raises(mx.MPXError, match="half gradients only"):
+        mx.mpx_embed_assemble_bwd(p, p, p, p, 2, 3, 8, mx.MPX_F32, p, 0)
+    with pytest.raises(mx.MPXError, match="MPX_F16 or MPX_BF16"):
+        mx.mpx_layernorm_fwd_cast(p, 8, p, p, p, p, None, 4, 8, mx.MPX_F32, 0)
+    with pytest.raises(mx.MPXError, match="MPX_F16, MPX_BF16 or MPX_F32"):
+        mx.mpx_linear_fwd(p, p, None, None, p, None, 8, 8, 8, 7, 0, 0)
