@@ -1,12 +1,15 @@
 """Benchmark of the mixed-precision training step on one MI355X.
 
-python bench.py [--gpus 1] [--steps K] [--warmup W] [--config NAME] [--no-cpu-baseline]
+python bench.py [--gpus 1] [--steps K] [--warmup W] [--config NAME]
+                [--no-cpu-baseline] [--no-sweep] [--step-only]
 
 A step is one pass of the whole hot path over one synthetic batch: cast the
 inputs, half forward, loss with the scale seed, half backward, unscale +
 finite check, masked AdamW with the fused half copy, loss-scale update.
 Inputs and parameters are resident in HBM before the timed region starts;
-the step runs as one captured HIP graph.
+the step runs as one captured HIP graph.  The default workload is the
+ViT-Base-like model (12 blocks, d 768, 197 tokens, batch 64, bf16), the
+largest of the workloads.
 
 Prints ONE JSON line.  `value` is train steps/s for the model workloads (or
 unscale+AdamW GB/s for the optimizer sweep).  `roofline` covers the dominant
@@ -16,8 +19,17 @@ on (the median of five groups of replays); `bound` is whichever of the MFMA and 
 its algorithmic flops and bytes (`frac` against that one; the other fraction
 is given too).  `traffic` is the HBM bytes per launch from the FETCH_SIZE /
 WRITE_SIZE counters, scaled by a plain copy's reading, or null when the
-kernel sources changed since the counters were taken.  `cpu_baseline` times
-the CPU oracle on a bounded sample.
+kernel sources changed since the counters were taken.  `gemm` times every
+linear-layer GEMM call of one block against the dense MFMA peak.  `sweep`
+(model workloads, unless --no-sweep) is the standalone optimizer sweep over
+1e8 fp16 gradient elements in 200 tensors: unscale + check + masked AdamW +
+scale update GB/s on applied steps (28 B per element), and the time of a
+skipped step (a non-finite gradient: check, no AdamW write, scale halved)
+separately.  `cpu_baseline` times the CPU oracle on a bounded sample.
+
+--step-only runs the warmup and the timed steps and nothing else (no
+per-kernel timing graphs, no sweep, no oracle), so that a kernel trace of
+the run holds exactly the step's launches; it prints how many steps ran.
 """
 from __future__ import annotations
 
@@ -34,7 +46,7 @@ import workloads
 PEAK_MFMA_TFLOPS = {"f16": 2500.0, "bf16": 2500.0}   # dense, MI355X
 PEAK_HBM_GBS = 8000.0
 PEAK_F32_TFLOPS = 157.3                               # dense float32 MFMA, MI355X
-DEFAULT_CONFIG = "vit_block"
+DEFAULT_CONFIG = "vit_b"
 
 # HBM bytes per launch of the dominant kernels from two rocprofv3 --pmc runs
 # (FETCH_SIZE, then WRITE_SIZE; KiB per dispatch), each scaled by what the
@@ -103,8 +115,13 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
-    ap.add_argument("--config", default=DEFAULT_CONFIG, choices=workloads.CONFIG_ORDER)
+    ap.add_argument("--config", default=None, choices=workloads.CONFIG_ORDER,
+                    help=f"workload (default {DEFAULT_CONFIG}; mlp for --compare-precision)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="model workloads: leave out the optimizer-sweep sub-object")
+    ap.add_argument("--step-only", action="store_true",
+                    help="warmup and timed steps only (for kernel traces of the step)")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--compare-precision", action="store_true",
                     help="step time and peak device memory of full precision (mixed precision "
@@ -126,8 +143,31 @@ def cpu_threads() -> int:
 
 
 def cpu_baseline_train(cfg, budget_s):
-    """Oracle training steps on the host, as many as fit the time budget (>= 1)."""
+    """Oracle training steps on the host, as many as fit the time budget (>= 1).
+
+    When one step of the full model would take far longer than the budget
+    (ViT-S, ViT-B), the sample is the oracle's gradient computation and
+    update at depths 1 and 2 of the same workload (full batch, width and
+    token count); the per-block cost t2 - t1 and the rest (embedding, head,
+    optimizer) t1 - (t2 - t1) give the full step by a linear model in the
+    depth, which is how the oracle's work grows (blocks are identical)."""
     from oracle import step as ostep
+    if cfg.kind == "vit" and cfg.depth > 2 and cfg.batch * cfg.tokens * cfg.d_model * cfg.depth > 1e8:
+        times = []
+        for depth in (1, 2):
+            c = workloads.scaled_down(cfg, depth=depth)
+            st = ostep.init_state(c)
+            batch = workloads.make_batch(c)
+            t0 = time.perf_counter()
+            ostep.train_step(c, st, batch, 0)
+            times.append(time.perf_counter() - t0)
+        per_block = max(times[1] - times[0], 1e-9)
+        est = times[0] - per_block + cfg.depth * per_block
+        return {"value": 1.0 / est, "unit": "steps/s", "cores": cpu_threads(), "kind": "oracle",
+                "sample": f"one oracle training step of the '{cfg.name}' workload at depth 1 "
+                          f"({times[0]:.1f} s) and at depth 2 ({times[1]:.1f} s), full batch and "
+                          f"width; the {cfg.depth}-block step is extrapolated linearly in the "
+                          f"depth: {est:.1f} s"}
     st = ostep.init_state(cfg)
     batch = workloads.make_batch(cfg)
     t0 = time.perf_counter()
@@ -213,7 +253,7 @@ def compare_precision(args, dev):
     to four times its batch (ViT-S: 128 .. 1024, the paper's range)."""
     import torch
     from paper_2507_03312_amd.train import make_step
-    name = "mlp" if args.config == DEFAULT_CONFIG else args.config
+    name = args.config or "mlp"
     if name == "sweep":
         raise SystemExit("--compare-precision needs a training workload")
     base_cfg = workloads.get(name)
@@ -284,6 +324,74 @@ def compare_precision(args, dev):
     print(json.dumps(line))
 
 
+def measure_sweep(dev, steps, warm, step_only=False):
+    """The optimizer-sweep workload (1e8 fp16 gradient elements in 200
+    tensors): GB/s of whole applied steps (unscale + check, masked AdamW with
+    the half copy, scale update; 28 B per element algorithmic), the time of a
+    skipped step (one +inf in the gradients: the check, AdamW writing
+    nothing, the scale halved), and the AdamW kernel alone (the dominant
+    kernel).  Each step runs as one captured HIP graph."""
+    import torch
+    from paper_2507_03312_amd.sweep import SweepStep
+    cfg = workloads.get("sweep")
+    sw = SweepStep(cfg, device=dev)
+    gf, params = workloads.sweep_tensors(cfg, sw.sizes)
+    sw.load(gf, params)
+    del gf, params
+    torch.cuda.synchronize()
+    for _ in range(warm):
+        sw.step()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        sw.step()
+    torch.cuda.synchronize()
+
+    def timed(n):
+        for _ in range(2):
+            g.replay()
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(n):
+            g.replay()
+        t1.record()
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / n
+
+    applied_ms = timed(steps)
+    if step_only:
+        print(f"step-only: {warm} eager sweep steps, then {steps + 2} graph replays of the step",
+              file=sys.stderr)
+        return {"value": round(sw.numel * 28 / (applied_ms * 1e-3) / 1e9, 1),
+                "ms_per_applied_step": round(applied_ms, 4)}
+    k_ms = sw.time_graph(sw.adamw)   # AdamW alone (applied)
+    saved = sw.inject(workloads.Injection(0, 0, 0, float("inf")))
+    applied_before = int(sw.d_step.item())
+    skipped_ms = timed(max(steps // 2, 5))
+    assert int(sw.d_step.item()) == applied_before, "a skipped step applied AdamW"
+    sw.restore(saved)
+    bytes_per = sw.numel * 28
+    gbs = bytes_per / (applied_ms * 1e-3) / 1e9
+    k_gbs = bytes_per / (k_ms * 1e-3) / 1e9
+    out = {"metric": "unscale+AdamW GB/s", "value": round(gbs, 1), "unit": "GB/s",
+           "frac_of_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "ms_per_applied_step": round(applied_ms, 4),
+           "skipped_step_ms": round(skipped_ms, 4), "elements": sw.numel, "bytes_per_element": 28,
+           "steps": steps, "workload": "200 fp16 gradient tensors, lognormal sizes summing to 1e8 "
+                                       "elements, fp32 masters/m/v, scale 2^16; a step = unscale + "
+                                       "check, masked AdamW + half copy, scale update",
+           "adamw_kernel": {"bound": "hbm", "achieved": round(k_gbs, 1), "peak": PEAK_HBM_GBS,
+                            "unit": "GB/s", "frac": round(k_gbs / PEAK_HBM_GBS, 4),
+                            "traffic": traffic_bytes("sweep/adamw"),
+                            "kernel": "masked AdamW + half copy, 28 B/element",
+                            "avg_launch_ms": round(k_ms, 4)}}
+    del sw, g
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -292,57 +400,38 @@ def main():
         sys.exit(2)
     import torch
     from paper_2507_03312_amd.train import make_step
-    from paper_2507_03312_amd.sweep import SweepStep
 
-    cfg = workloads.get(args.config)
     torch.cuda.set_device(0)
     dev = torch.device("cuda:0")
     if args.compare_precision:
         compare_precision(args, dev)
         return
+    name = args.config or DEFAULT_CONFIG
+    cfg = workloads.get(name)
 
-    if args.config == "sweep":
+    if name == "sweep":
         steps = args.steps or 50
         warm = args.warmup if args.warmup is not None else 5
-        sw = SweepStep(cfg, device=dev)
-        gf, params = workloads.sweep_tensors(cfg, sw.sizes)
-        sw.load(gf, params)
-        del gf, params
-        torch.cuda.synchronize()
-        for _ in range(warm):
-            sw.step()
-        torch.cuda.synchronize()
-        t0 = torch.cuda.Event(enable_timing=True)
-        t1 = torch.cuda.Event(enable_timing=True)
-        t0.record()
-        for _ in range(steps):
-            sw.step()
-        t1.record()
-        torch.cuda.synchronize()
-        ms = t0.elapsed_time(t1) / steps
-        bytes_per = sw.numel * 28            # g 2 + p,m,v 12 read; p,m,v 12 + half copy 2 written
-        gbs = bytes_per / (ms * 1e-3) / 1e9
-        k_ms = sw.time_graph(sw.adamw)       # the dominant kernel: masked AdamW + half copy
+        sw = measure_sweep(dev, steps, warm, args.step_only)
+        if args.step_only:
+            print(json.dumps({"metric": "unscale+AdamW GB/s", "value": sw["value"], "unit": "GB/s",
+                              "ms_per_step": sw["ms_per_applied_step"], "steps": steps,
+                              "warmup": warm, "step_only": True}))
+            return
         calibration_copy(args, dev)
-        k_gbs = bytes_per / (k_ms * 1e-3) / 1e9
-        line = {"metric": "unscale+AdamW GB/s", "value": round(gbs, 1), "unit": "GB/s",
-                "n_gpus": 1, "steps": steps, "warmup": warm, "ms_per_step": round(ms, 4),
+        line = {"metric": "unscale+AdamW GB/s", "value": sw["value"], "unit": "GB/s",
+                "n_gpus": 1, "steps": steps, "warmup": warm, "ms_per_step": sw["ms_per_applied_step"],
                 "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
                 "dtype": "f32 (f16 gradients)", "data": "synthetic",
-                "config": {"workload": "sweep: 200 fp16 gradient tensors, lognormal sizes, "
-                                       "1e8 elements, masked AdamW + half copy",
-                           "elements": sw.numel, "parallelism": "none"},
-                "roofline": {"bound": "hbm", "achieved": round(k_gbs, 1), "peak": PEAK_HBM_GBS,
-                             "unit": "GB/s", "frac": round(k_gbs / PEAK_HBM_GBS, 4),
-                             "traffic": traffic_bytes("sweep/adamw"),
-                             "kernel": "masked AdamW + half copy, 28 B/element",
-                             "avg_launch_ms": round(k_ms, 4)}}
+                "config": {"workload": "sweep: " + sw["workload"], "elements": sw["elements"],
+                           "parallelism": "none"},
+                "roofline": sw["adamw_kernel"], "skipped_step_ms": sw["skipped_step_ms"]}
         if not args.no_cpu_baseline:
             line["cpu_baseline"] = cpu_baseline_sweep(cfg, args.cpu_seconds)
         print(json.dumps(line))
         return
 
-    steps = args.steps or {"mlp": 500, "vit_block": 300, "vit_s": 50, "vit_b": 30}[args.config]
+    steps = args.steps or {"mlp": 500, "vit_block": 300, "vit_s": 50, "vit_b": 30}[name]
     warm = args.warmup if args.warmup is not None else 5
     st = make_step(cfg, dev)
     st.set_batch(workloads.make_batch(cfg))
@@ -362,6 +451,14 @@ def main():
     t1.record()
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps
+    if args.step_only:
+        print(f"step-only: {warm} eager steps, then {warm + steps} graph replays of the step "
+              f"({2 * warm + steps} steps in all; the first eager step also casts the masters)",
+              file=sys.stderr)
+        print(json.dumps({"metric": "train steps/s", "value": round(1000.0 / ms, 3), "unit": "steps/s",
+                          "n_gpus": 1, "steps": steps, "warmup": warm, "ms_per_step": round(ms, 4),
+                          "config": {"workload": st.describe()}, "step_only": True}))
+        return
     k_ms = st.time_dominant()
     calibration_copy(args, dev)
     peak = PEAK_MFMA_TFLOPS[cfg.half]
@@ -375,7 +472,7 @@ def main():
     else:
         roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": peak, "unit": "TFLOP/s",
                 "frac": round(tflops / peak, 4), "hbm_frac": round(gbs / PEAK_HBM_GBS, 4)}
-    roof.update({"traffic": traffic_bytes(args.config + "/" + site["name"]), "algorithmic_bytes": site["bytes"],
+    roof.update({"traffic": traffic_bytes(name + "/" + site["name"]), "algorithmic_bytes": site["bytes"],
                  "flops": site["flops"], "kernel": site["desc"], "avg_launch_ms": round(k_ms, 5)})
     gemm = gemm_table(st, peak)
     line = {"metric": "train steps/s", "value": round(1000.0 / ms, 3), "unit": "steps/s",
@@ -387,8 +484,16 @@ def main():
             "roofline": roof}
     if gemm:
         line["gemm"] = gemm
+    del st
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    if not args.no_sweep:
+        line["sweep"] = measure_sweep(dev, 50, 5)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline_train(cfg, args.cpu_seconds)
+        if not args.no_sweep:
+            line["sweep"]["cpu_baseline"] = cpu_baseline_sweep(workloads.get("sweep"),
+                                                               min(args.cpu_seconds, 8.0))
     print(json.dumps(line))
 
 

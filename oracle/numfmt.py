@@ -64,10 +64,3 @@ def round_to(x, fmt: str) -> np.ndarray:
         for i in range(0, xf.size, CHUNK):
             out[i:i + CHUNK] = _round_block(xf[i:i + CHUNK], p, emin, emax)
         return out.reshape(x.shape)
-
-
-def is_representable(x: np.ndarray, fmt: str) -> bool:
-    """True when every finite value of ``x`` is exactly a ``fmt`` value."""
-    x = np.asarray(x, dtype=np.float64)
-    fin = np.isfinite(x)
-    return bool(np.array_equal(round_to(x[fin], fmt).astype(np.float64), x[fin]))

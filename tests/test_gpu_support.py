@@ -14,7 +14,8 @@ import pytest
 from oracle import ops
 from oracle.numfmt import round_to
 from oracle.policy import Policy
-from tests.gpu_util import HAVE_GPU, assert_same_values, assert_within, to_dev_half, to_host, ulp
+from tests.gpu_util import (HAVE_GPU, assert_same_values, assert_within, gemm_bound, to_dev_half,
+                            to_host, ulp)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not HAVE_GPU, reason="no GPU")]
 
@@ -290,6 +291,82 @@ def test_classifier_head_matches_separate_calls(fmt, B, T, d, C):
         assert torch.equal(a, b_), what
 
 
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("B,T,d,C", [(128, 65, 384, 10), (33, 2, 512, 32)], ids=lambda v: str(v))
+def test_classifier_head_against_oracle(fmt, B, T, d, C):
+    """The fused classifier head against the oracle's ops, per element, stage
+    by stage: each stage the GPU exposes (Z, dlogits, dX, dgamma, dbeta) is
+    compared with the oracle's op on the GPU's own exposed input, and the
+    stages it keeps internal (the logits, dZ) enter through their propagated
+    bounds:
+      Z        = LN(x)                       one half ulp + float32 evaluation
+      logits   = half(Z W^T + b)             within the GEMM bound delta of
+                                             the oracle's logits from the GPU's Z
+      dlogits  = CE cotangent of the logits: a logit error of at most Delta
+                 per row moves every softmax probability by a factor within
+                 exp(+-2 Delta), so |d dlogits| <= scale/B p (exp(2 Delta) - 1)
+                 on top of one ulp and the float32 evaluation term;
+      loss     = mean(logsumexp - logit_y):  within mean(2 Delta) + 1e-5 |loss|
+      dZ       = half(dlogits W)             within the GEMM bound eps of the
+                                             oracle's dZ from the GPU's dlogits
+      dX, dgamma, dbeta = LN backward of dZ: the oracle's values plus the
+                 linear propagation of eps through the LN backward."""
+    from paper_2507_03312_amd.train import pack_scale_state
+    pol = Policy(fmt)
+    dt = mx.DTYPES[fmt]
+    x = _rand((B * T, d), fmt, 31, 2.0, 0.5)
+    g, be = _rand((d,), fmt, 32, 0.2, 1.0), _rand((d,), fmt, 33, 0.2)
+    w, bias = _rand((C, d), fmt, 34, 0.05), _rand((C,), fmt, 35, 0.5)
+    y = np.random.default_rng(36).integers(0, C, B).astype(np.int32)
+    scale = 2.0 ** 15
+    tx, tg, tb, tw, tbias = (to_dev_half(a, fmt) for a in (x, g, be, w, bias))
+    ty = torch.from_numpy(y).cuda()
+    st = torch.from_numpy(pack_scale_state(scale, 0, 10)).cuda()
+    ld = T * d
+    z, dl, dx = _empty((B, d), fmt), _empty((B, C), fmt), _empty((B * T, d), fmt)
+    dg, db = _empty((d,), fmt), _empty((d,), fmt)
+    loss = torch.zeros(1, dtype=torch.float32, device="cuda")
+    wsn = mx.mpx_classifier_head_workspace(B, d)
+    ws = torch.zeros(wsn, dtype=torch.uint8, device="cuda")
+    mx.mpx_classifier_head(tx.data_ptr(), ld, tg.data_ptr(), tb.data_ptr(), tw.data_ptr(),
+                           tbias.data_ptr(), ty.data_ptr(), B, d, C, st.data_ptr(), z.data_ptr(),
+                           loss.data_ptr(), dl.data_ptr(), dx.data_ptr(), ld, dg.data_ptr(),
+                           db.data_ptr(), dt, ws.data_ptr(), wsn, None, _s())
+    torch.cuda.synchronize()
+    xc = x.reshape(B, T, d)[:, 0, :]
+    # Z
+    gz = to_host(z)
+    rz = ops.layernorm_fwd(pol, xc, g, be)
+    xhat = ops.layernorm_fwd(Policy("f64"), xc, np.ones(d), np.zeros(d))
+    f32_err = 2.0 ** -21 * (np.abs(xhat * g.astype(np.float64)) + np.abs(be.astype(np.float64)))
+    assert_within(gz, rz, ulp(rz, fmt) + f32_err, "head Z")
+    # logits (internal) -> dlogits and the loss
+    rl = ops.linear_fwd(pol, gz, w, bias)
+    delta = np.max(gemm_bound(gz, w.T, rl, fmt, d), axis=1, keepdims=True)      # per row
+    rloss, rdl = ops.ce_fwd_bwd(pol, rl, y, scale)
+    l64 = rl.astype(np.float64)
+    p = np.exp(l64 - l64.max(axis=1, keepdims=True))
+    p /= p.sum(axis=1, keepdims=True)
+    sens = scale / B * p * np.expm1(2.0 * delta)
+    gdl = to_host(dl)
+    assert_within(gdl, rdl, ulp(rdl, fmt) + 1e-5 * np.abs(rdl) + sens, "head dlogits")
+    assert abs(float(loss.item()) - rloss) <= float(np.mean(2.0 * delta)) + 1e-5 * abs(rloss)
+    # dZ (internal) -> dX, dgamma, dbeta
+    rdz, _, _ = ops.linear_bwd(pol, gz, w, gdl)
+    eps = gemm_bound(gdl, w, rdz, fmt, C)
+    rdx, rdg, rdb = ops.layernorm_bwd(pol, xc, g, rdz)
+    x64 = xc.astype(np.float64)
+    rstd = 1.0 / np.sqrt(x64.var(axis=1, keepdims=True) + 1e-5)
+    ge = np.abs(g.astype(np.float64)) * eps
+    prop = rstd * (ge + ge.mean(axis=1, keepdims=True)
+                   + np.abs(xhat) * (ge * np.abs(xhat)).mean(axis=1, keepdims=True))
+    gx = to_host(dx).reshape(B, T, d)
+    assert_within(gx[:, 0, :], rdx, 2 * ulp(rdx, fmt) + 1e-4 * np.abs(rdx) + prop, "head dX")
+    assert_within(to_host(dg), rdg, _sum_bound(rdz * np.abs(xhat), fmt, rdg) + 1e-4 * np.abs(rdg)
+                  + (eps * np.abs(xhat)).sum(axis=0), "head dgamma")
+    assert_within(to_host(db), rdb, _sum_bound(rdz, fmt, rdb) + eps.sum(axis=0), "head dbeta")
+
+
 def test_classifier_head_limits():
     t = _empty((64, 64), "bf16")
     p = t.data_ptr()
@@ -507,3 +584,30 @@ def test_layernorm_fwd_cast_matches_cast_then_layernorm(fmt, rows, d, ldx):
                          dt, _s())
     torch.cuda.synchronize()
     assert torch.equal(xh1, xh2) and torch.equal(y1, y2) and torch.equal(mr1, mr2)
+
+
+@pytest.mark.parametrize("fmt", ["f16", "bf16"])
+@pytest.mark.parametrize("rows,d,ldx", [(8320, 384, 384), (33, 1500, 1501)])
+def test_layernorm_fwd_cast_against_oracle(fmt, rows, d, ldx):
+    """The fused input cast + LayerNorm against the oracle directly: the half
+    copy is the oracle's rounding of the float32 inputs, bit for bit, and the
+    normalised output is the oracle's LayerNorm of that copy within one half
+    ulp plus the float32 evaluation term."""
+    pol = Policy(fmt)
+    dt = mx.DTYPES[fmt]
+    rng = np.random.default_rng(rows + 7 * d)
+    x = rng.normal(0.3, 1.5, size=(rows, ldx)).astype(np.float32)
+    g = round_to(1.0 + 0.1 * rng.normal(size=d), fmt)
+    b = round_to(0.1 * rng.normal(size=d), fmt)
+    tg, tb = to_dev_half(g, fmt), to_dev_half(b, fmt)
+    tx = torch.from_numpy(x).cuda()
+    xh, yv = _empty((rows, d), fmt), _empty((rows, d), fmt)
+    mx.mpx_layernorm_fwd_cast(tx.data_ptr(), ldx, tg.data_ptr(), tb.data_ptr(), xh.data_ptr(),
+                              yv.data_ptr(), None, rows, d, dt, _s())
+    torch.cuda.synchronize()
+    rxh = pol.R(x[:, :d])
+    assert_same_values(to_host(xh), rxh, "half copy")
+    ref = ops.layernorm_fwd(pol, rxh, g, b)
+    xhat = ops.layernorm_fwd(Policy("f64"), rxh, np.ones(d), np.zeros(d))
+    f32_err = 2.0 ** -21 * (np.abs(xhat * g.astype(np.float64)) + np.abs(b.astype(np.float64)))
+    assert_within(to_host(yv), ref, ulp(ref, fmt) + f32_err, "LN of the cast")

@@ -183,7 +183,11 @@ def test_adamw_bit_exact_against_oracle_expression():
 def test_full_sweep_workload_sampled():
     """1e8 elements in 200 tensors: scale/skip trajectory over the 200 steps
     bit-exact against the oracle's state machine driven by the oracle's own
-    finite count; AdamW checked on sampled elements after the first steps."""
+    finite count; AdamW (p, m, v and the half copy) checked on up to 64
+    sampled elements of EVERY tensor after the first three steps, on the two
+    skipped steps (nothing written) and on the first applied step after each
+    skip (bias corrections use the count of applied steps), and at the end.
+    AdamW is elementwise, so the oracle follows the sampled elements alone."""
     from paper_2507_03312_amd.sweep import SweepStep
     cfg = workloads.get("sweep")
     sizes = workloads.sweep_sizes(cfg)
@@ -192,16 +196,19 @@ def test_full_sweep_workload_sampled():
     gpu.load(gf, params)
     rng = np.random.default_rng(9)
     samples = [np.unique(rng.integers(0, n, size=min(n, 64))) for n in sizes]
+    idx = [torch.from_numpy(i).cuda() for i in samples]
     g_s = [round_to(g[i], "f16") for g, i in zip(gf, samples)]
     p_s = [p[i].copy() for p, i in zip(params, samples)]
     m_s = [np.zeros_like(x) for x in p_s]
     v_s = [np.zeros_like(x) for x in p_s]
     # N(0, 1e-3) * 2^16 stays far below the float16 maximum: only injections overflow
     assert max(float(np.max(np.abs(g))) for g in gf) < 65504 / 4
-    base_nonfinite = 0
+    skips = [inj.step for inj in cfg.injections]
+    check_at = {0, 1, 2, cfg.steps - 1} | set(skips) | {s + 1 for s in skips}
     st = oscale.make_state(cfg.scale_init, cfg.period)
     hp = oadamw.AdamWHP(cfg.lr, cfg.beta1, cfg.beta2, cfg.eps, cfg.weight_decay)
     t = 0
+    checked = 0
     for s in range(cfg.steps):
         injs = gpu.injections_at(s)
         saved = [gpu.inject(inj) for inj in injs]
@@ -209,14 +216,22 @@ def test_full_sweep_workload_sampled():
         for sv in saved:
             gpu.restore(sv)
         finite = not injs
-        assert int(gpu.d_nonfinite.item()) == base_nonfinite + len(injs)
-        if finite and s < 3:
-            g32 = [oscale.unscale(g, st.scale) for g in g_s]
-            p_s, m_s, v_s, t = oadamw.adamw_masked(p_s, m_s, v_s, g32, t, hp, True)
-            for i in range(0, len(sizes), 17):
-                got = gpu.p[i][torch.from_numpy(samples[i]).cuda()].cpu().numpy()
-                assert np.all(np.abs(got - p_s[i]) <= 1e-5 * np.maximum(np.abs(p_s[i]), cfg.lr))
+        assert int(gpu.d_nonfinite.item()) == len(injs)
+        g32 = [oscale.unscale(g, st.scale) for g in g_s]
+        p_s, m_s, v_s, t = oadamw.adamw_masked(p_s, m_s, v_s, g32, t, hp, finite)
+        if s in check_at:
+            for i in range(len(sizes)):
+                for dev, ref, what in ((gpu.p, p_s, "p"), (gpu.m, m_s, "m"), (gpu.v, v_s, "v")):
+                    got = dev[i][idx[i]].cpu().numpy()
+                    tol = 1e-5 * (np.maximum(np.abs(ref[i]), cfg.lr) if what == "p"
+                                  else max(float(np.max(np.abs(ref[i]))), 1e-30))
+                    assert np.all(np.abs(got - ref[i]) <= tol), (s, i, what)
+                got_p = gpu.p[i][idx[i]].cpu().numpy()
+                assert_same_values(to_host(gpu.h[i][idx[i]]), round_to(got_p, "f16"), "half copy")
+            checked += 1
         st = oscale.adjust(st, finite)
         got = gpu.scale_state()
         assert got["scale"] == float(st.scale) and got["counter"] == st.counter
+        assert int(gpu.d_step.item()) == t
     assert int(gpu.d_step.item()) == cfg.steps - 2
+    assert checked == len(check_at)

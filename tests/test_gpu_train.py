@@ -2,22 +2,47 @@
 §3.5 composed), through the C ABI.
 
 * Lockstep: from the same start-of-step masters, the GPU's scaled half
-  gradients match the oracle's within 2e-2 relative (normwise, per tensor);
-  then the oracle's unscale/check/adjust/AdamW
-  applied to the GPU's own gradients matches the GPU's post-step state: flag,
-  skip, scale and counter bit-exact, masters within 1e-5.
+  gradients match the oracle's per tensor within 2e-2 relative, both
+  normwise (||gpu - ref|| <= 2e-2 ||ref||) and elementwise
+  (|gpu - ref| <= 2e-2 max(max |ref|, S) per element).  S is the magnitude
+  of the summands of that element: a parameter gradient is a sum over
+  tokens (dW = sum_m dY[m]^T X[m], db = sum_m dY[m], dgamma = sum_m
+  dY[m] xhat[m], dbeta = sum_m dY[m]), so S = |dY|^T |X|, sum |dY|,
+  sum |dY xhat|, from the oracle's own operands.  Operands that differ by
+  relative rounding errors r give sums that differ by at most about 2 r S,
+  however much the terms cancel; S = |ref| when they do not cancel, and
+  S exceeds max |ref| only where a few large terms cancel (a batch of two
+  images sends the loss gradient into the last block through two CLS rows,
+  so its MLP weight gradients are sums of two products).  Then the oracle's unscale/check/
+  adjust/AdamW applied to the GPU's own gradients matches the GPU's
+  post-step state: flag, skip, scale and counter bit-exact, masters and both
+  moments within 1e-5.
 * Free-running: the oracle and the GPU each run the steps on their own; the
   flag / skip / scale trajectories are bit-exact and the masters agree within
-  2e-2 normwise over the whole model and for every weight matrix, and within
-  5e-2 for each 1-D tensor (biases, LayerNorm parameters: few elements whose
-  gradients are sums over all tokens, where Adam's normalisation turns small
-  gradient differences into differences of a sizeable fraction of the
-  learning rate).  The key-projection bias
-  is left out of the per-tensor comparison: its exact gradient is zero (a
-  softmax ignores a shift shared by a whole row of scores), so both sides
-  only see rounding noise there, and Adam turns noise of either sign into
-  full-size steps of that sign.
+  2e-2 normwise over the whole model and for every tensor.  Each step
+  reports the overflow margin max|g| / max-finite of both sides; a flag
+  mismatch at a margin within 2e-2 of 1 is reported as a boundary case (a
+  failure that names itself), never passed.  Two exclusions, each with a
+  mathematical reason:
+  - the key-projection bias: its exact gradient is zero (a softmax ignores a
+    shift shared by a whole row of scores), so both sides only see rounding
+    noise there, and Adam turns noise of either sign into full-size steps of
+    that sign;
+  - elements of tensors that start at zero (biases, LayerNorm beta, the CLS
+    token) whose first-step gradients differ in sign between the two sides.
+    Adam's first step is lr * g / (|g| + eps), i.e. lr * sign(g), so such an
+    element takes opposite steps on the two sides; a sign can differ only
+    where |g| lies within the lockstep bound of zero, which the first step's
+    gradients (from identical masters) are checked against.  These elements
+    are bounded by |delta p| <= 2 lr sum_t c_t + 2 lr wd sum_t |p| instead,
+    after the n applied steps t = 1..n: one AdamW step moves an element by
+    lr (|m_hat| / (sqrt(v_hat) + eps) + wd |p|), and Cauchy-Schwarz over the
+    moment sums gives |m_hat| / sqrt(v_hat) <= c_t =
+    (1 - b1) sqrt(1 - b2^t) / ((1 - b1^t) sqrt(1 - b2))
+    * sqrt(sum_{k<t} (b1^2 / b2)^k)  (1 at t = 1, 1.04 at t = 10).
 """
+import sys
+
 import numpy as np
 import pytest
 
@@ -32,6 +57,81 @@ if HAVE_GPU:
     import torch
     from paper_2507_03312_amd.train import make_step
 
+MAX_FINITE = {"f16": 65504.0, "bf16": 3.3895313892515355e38}
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def _check_grads(s, names, g_gpu, g_ref, summands=None):
+    """Per tensor: identical finiteness; for finite nonzero references the
+    normwise 2e-2 bound and the elementwise bound 2e-2 max(max|ref|, S),
+    with S the summand magnitudes (``summands``: name -> array, where known)."""
+    worst = (0.0, "")
+    cancel = []
+    for name, a, b in zip(names, g_gpu, g_ref):
+        fin = np.isfinite(b)
+        assert np.array_equal(np.isfinite(a), fin), (s, name)
+        if fin.all() and np.any(b):
+            a64, b64 = a.astype(np.float64), b.astype(np.float64)
+            rn = rel_norm_err(a, b)
+            mref = float(np.max(np.abs(b64)))
+            err = np.abs(a64 - b64)
+            S = summands.get(name) if summands else None
+            scale = mref if S is None else np.maximum(mref, S.reshape(b.shape))
+            assert rn <= 2e-2, (s, name, "normwise", rn)
+            bad = err > 2e-2 * scale
+            assert not bad.any(), (s, name, "elementwise", float(np.max(err / scale)))
+            el = float(np.max(err)) / mref
+            if el > 2e-2:
+                cancel.append(f"{name} ({int(np.sum(err > 2e-2 * mref))} elements, "
+                              f"{el:.3f} of max|ref|)")
+            worst = max(worst, (max(rn, float(np.max(err / scale))), name))
+    if cancel:
+        _say(f"  step {s}: within the summand bound only: " + ", ".join(cancel))
+    return worst
+
+
+def _oracle_gradients(cfg, masters, names, batch, pol, scale):
+    """The oracle's steps 1-4 (as ``oracle.step.gradients``) and, for every
+    gradient that is a sum over tokens, the magnitude of its summands, taken
+    from the operands of the oracle's own linear and LayerNorm backward calls
+    (recorded by wrapping them; their arithmetic is untouched)."""
+    from oracle import models, ops
+    P = {n: pol.R(w) for n, w in zip(names, masters)}
+    by_id = {id(P[n]): n for n in names}
+    rec = {}
+    lin0, ln0 = ops.linear_bwd, ops.layernorm_bwd
+
+    def lin(pol_, x, w, dy, need_dx=True):
+        n = by_id.get(id(w))
+        if n is not None:
+            ax, ady = np.abs(np.asarray(x, np.float64)), np.abs(np.asarray(dy, np.float64))
+            rec[n] = ady.T @ ax
+            rec[n[:-2] + ".b"] = ady.sum(axis=0)
+        return lin0(pol_, x, w, dy, need_dx)
+
+    def ln(pol_, x, g, dy):
+        n = by_id.get(id(g))
+        if n is not None:
+            z = np.asarray(x, np.float64)
+            mu = z.mean(axis=-1, keepdims=True)
+            xhat = (z - mu) / np.sqrt(((z - mu) ** 2).mean(axis=-1, keepdims=True) + 1e-5)
+            ady = np.abs(np.asarray(dy, np.float64))
+            rec[n] = (ady * np.abs(xhat)).reshape(-1, z.shape[-1]).sum(axis=0)
+            rec[n[:-2] + ".b"] = ady.reshape(-1, z.shape[-1]).sum(axis=0)
+        return ln0(pol_, x, g, dy)
+
+    ops.linear_bwd, ops.layernorm_bwd = lin, ln
+    try:
+        loss, dout, cache = models.forward_loss(pol, cfg, P, ostep.cast_batch(pol, batch), scale)
+        G = models.backward(pol, cfg, P, cache, dout)
+    finally:
+        ops.linear_bwd, ops.layernorm_bwd = lin0, ln0
+    return loss, [np.array(G[n], dtype=np.float32) for n in names], rec
+
 
 def _lockstep(cfg, steps):
     gpu = make_step(cfg)
@@ -42,7 +142,8 @@ def _lockstep(cfg, steps):
     for s in range(steps):
         # oracle gradients from the GPU's current masters (identical start state)
         start = ostep.TrainState(ost.names, gpu.masters(), ost.m, ost.v, ost.t, ost.scale)
-        loss_ref, g_ref = ostep.gradients(cfg, start, batch, pol)
+        loss_ref, g_ref, summ = _oracle_gradients(cfg, start.masters, ost.names, batch, pol,
+                                                  start.scale.scale)
         gpu.forward_backward()
         for inj in cfg.injections:
             if inj.step == s:
@@ -50,11 +151,7 @@ def _lockstep(cfg, steps):
         ostep.apply_injections(cfg, s, g_ref)
         g_gpu = gpu.grads()
         assert abs(gpu.loss() - loss_ref) <= 1e-2 * abs(loss_ref) + 1e-6
-        for name, a, b in zip(ost.names, g_gpu, g_ref):
-            fin = np.isfinite(b)
-            assert np.array_equal(np.isfinite(a), fin), name
-            if fin.all() and np.any(b):
-                assert rel_norm_err(a, b) <= 2e-2, (s, name, rel_norm_err(a, b))
+        worst = _check_grads(s, ost.names, g_gpu, g_ref, summ)
         # oracle's steps 5-8 on the GPU's own gradients vs the GPU's update
         ref_state, nf = ostep.finish_step(cfg, start, g_gpu)
         gpu.finish()
@@ -66,39 +163,103 @@ def _lockstep(cfg, steps):
             assert np.all(np.abs(a - b) <= 1e-5 * np.maximum(np.abs(b), cfg.lr)), (s, name)
         ost = ostep.TrainState(ost.names, ref_state.masters, ref_state.m, ref_state.v,
                                ref_state.t, ref_state.scale)
-        # moments: compare once per step too
-        gm = gpu.arena.read(gpu.arena.m32)
-        for name, a, b in zip(ost.names, gm, ref_state.m):
-            assert np.all(np.abs(a - b) <= 1e-5 * max(float(np.max(np.abs(b))), 1e-30)), (s, name)
+        # both moments: compare once per step too
+        for arena, ref in ((gpu.arena.m32, ref_state.m), (gpu.arena.v32, ref_state.v)):
+            for name, a, b in zip(ost.names, gpu.arena.read(arena), ref):
+                assert np.all(np.abs(a - b) <= 1e-5 * max(float(np.max(np.abs(b))), 1e-30)), (s, name)
+        _say(f"  lockstep {cfg.name} step {s}: loss {loss_ref:.6f}, nonfinite {nf}, "
+             f"worst gradient error {worst[0]:.2e} ({worst[1]})")
 
 
-def _free_running(cfg, steps):
+def _margin(grads, half):
+    """max |finite g| / largest finite half, and whether any value overflowed."""
+    mx = max(float(np.max(np.abs(np.where(np.isfinite(g), g, 0.0)))) for g in grads)
+    return mx / MAX_FINITE[half], any(not np.isfinite(g).all() for g in grads)
+
+
+def _adam_divergence(cfg, n):
+    """Largest difference two AdamW trajectories of one element starting at
+    zero can reach after n applied steps, whatever their gradients: twice the
+    sum over t of lr (c_t + wd |p_t|), with |p_t| <= lr sum_{s<=t} c_s."""
+    b1, b2 = cfg.beta1, cfg.beta2
+    tot, p = 0.0, 0.0
+    for t in range(1, n + 1):
+        c = ((1 - b1) * np.sqrt(1 - b2 ** t) / ((1 - b1 ** t) * np.sqrt(1 - b2))
+             * np.sqrt(sum((b1 * b1 / b2) ** k for k in range(t))))
+        step = cfg.lr * (c + cfg.weight_decay * p)
+        p += step
+        tot += step
+    return 2.0 * tot * (1 + 1e-6)
+
+
+def _free_running(cfg, steps, graph=False):
+    """``graph``: the GPU replays the step captured as one HIP graph (no
+    injections can be made then: the configuration must have none)."""
     gpu = make_step(cfg)
     batch = workloads.make_batch(cfg)
     gpu.set_batch(batch)
     ost, results = ostep.run(cfg, steps=steps)
+    if graph:
+        assert not cfg.injections
+        gpu.capture()
     flags, scales = [], []
+    g0 = None
     for s in range(steps):
         scales.append(gpu.scale_state()["scale"])
-        gpu.forward_backward()
-        for inj in cfg.injections:
-            if inj.step == s:
-                gpu.inject(inj.tensor, inj.element, inj.value)
-        gpu.finish()
+        if graph:
+            gpu.replay()
+        else:
+            gpu.forward_backward()
+            for inj in cfg.injections:
+                if inj.step == s:
+                    gpu.inject(inj.tensor, inj.element, inj.value)
+            gpu.finish()
+        grads = gpu.grads()
+        if s == 0:   # identical start: the lockstep bounds hold
+            g0 = grads
+            _check_grads(s, ost.names, grads, results[0].grads_half)
         flags.append(gpu.nonfinite())
+        mg, og = _margin(grads, cfg.half)
+        mo, oo = _margin(results[s].grads_half, cfg.half)
+        _say(f"  free-running {cfg.name} step {s}: scale {scales[-1]:g}, nonfinite gpu {flags[-1]} "
+             f"oracle {results[s].nonfinite}; overflow margin gpu {mg:.3e}{' (inf)' if og else ''} "
+             f"oracle {mo:.3e}{' (inf)' if oo else ''}")
+        if (flags[-1] > 0) != (results[s].nonfinite > 0):
+            near = abs(max(mg, mo) - 1.0) <= 2e-2 or og != oo
+            pytest.fail(f"step {s}: skip decisions differ (gpu {flags[-1]}, oracle "
+                        f"{results[s].nonfinite}){' -- BOUNDARY CASE: overflow margin within 2e-2 of 1' if near else ''}")
     assert [f > 0 for f in flags] == [r.nonfinite > 0 for r in results]
     assert scales == [r.scale_used for r in results]
     st = gpu.scale_state()
     assert st["scale"] == float(ost.scale.scale) and st["counter"] == ost.scale.counter
+    assert int(gpu.d_step.item()) == ost.t
     ga, oa = gpu.masters(), ost.masters
     assert rel_norm_err(np.concatenate([a.ravel() for a in ga]),
                         np.concatenate([b.ravel() for b in oa])) <= 2e-2
     d = cfg.d_model
-    for name, a, b in zip(ost.names, ga, oa):
-        if name.endswith("qkv.b"):
-            a, b = np.concatenate([a[:d], a[2 * d:]]), np.concatenate([b[:d], b[2 * d:]])
-        tol = 2e-2 if a.ndim >= 2 else 5e-2
-        assert rel_norm_err(a, b) <= tol, (name, rel_norm_err(a, b))
+    init = workloads.init_params(cfg)
+    n = ost.t
+    worst = (0.0, "")
+    flipped_total = 0
+    for i, (name, a, b) in enumerate(zip(ost.names, ga, oa)):
+        a, b = a.astype(np.float64).ravel(), b.astype(np.float64).ravel()
+        keep = np.ones(a.shape, bool)
+        if name.endswith("qkv.b"):          # the key bias: exact gradient zero
+            keep[d:2 * d] = False
+        flipped = 0
+        if not np.any(init[name]) and n > 0:  # zero start: Adam's sign-sensitive first step
+            ga0 = g0[i].ravel().astype(np.float64)
+            gr0 = results[0].grads_half[i].ravel().astype(np.float64)
+            flip = keep & (np.sign(ga0) != np.sign(gr0))
+            flipped = int(flip.sum())
+            flipped_total += flipped
+            assert np.all(np.abs(a[flip] - b[flip]) <= _adam_divergence(cfg, n)), name
+            keep &= ~flip
+        err = rel_norm_err(a[keep], b[keep])
+        worst = max(worst, (err, name))
+        assert err <= 2e-2, (name, err, f"{flipped} sign-flipped elements excluded")
+    _say(f"  free-running {cfg.name}: worst per-tensor master error {worst[0]:.2e} ({worst[1]}); "
+         f"{flipped_total} zero-start elements with first-step gradient signs that differ")
 
 
 def test_mlp_lockstep_10_steps_with_injection():
@@ -133,6 +294,37 @@ def test_vit_b_reduced_lockstep():
 def test_vit_block_free_running_small_batch():
     cfg = workloads.scaled_down(workloads.get("vit_block"), batch=8)
     _free_running(cfg, 4)
+
+
+# ---- the workloads at their stated sizes (tile choice, split-K plan,
+# attention grid and two-stream order are those of the benchmarked step) ----
+
+@pytest.mark.timeout(900)
+def test_vit_s_full_size_lockstep():
+    """ViT-S as stated: batch 256, 12 blocks, 32x32x3 images, fp16, 2^16."""
+    _lockstep(workloads.get("vit_s"), 2)
+
+
+@pytest.mark.timeout(900)
+def test_vit_b_full_batch_lockstep():
+    """ViT-B at its full batch, token count and width (64 x 197 tokens,
+    d 768, 12 heads, 224x224x3 images, bf16); two blocks reach every kernel
+    path of the twelve."""
+    _lockstep(workloads.scaled_down(workloads.get("vit_b"), depth=2), 2)
+
+
+@pytest.mark.timeout(900)
+def test_vit_s_free_running_full_batch():
+    """fp16 ViT-S at batch 256 and scale 2^16, ten steps replayed from the
+    captured graph: flag and scale trajectories bit-exact, overflow margins
+    reported each step (two blocks: the oracle's ten steps stay short)."""
+    _free_running(workloads.scaled_down(workloads.get("vit_s"), depth=2), 10, graph=True)
+
+
+@pytest.mark.timeout(900)
+def test_vit_block_free_running_full_batch():
+    """The one-block bf16 workload as stated (batch 128), ten graph replays."""
+    _free_running(workloads.get("vit_block"), 10, graph=True)
 
 
 @pytest.mark.parametrize("name", ["mlp", "vit_block"])
