@@ -47,7 +47,8 @@
  *    gradient list, without reading the gradients again.  Activation
  *    cotangents (dX) are never counted.
  *  - The library keeps no state between calls except tensor-list objects
- *    (and their small device tables), which the caller creates and destroys.
+ *    (and their small device tables), which the caller creates and destroys,
+ *    and the static scratch array of mpx_linear_bwd_noalloc (one per GPU).
  */
 #ifndef MPX_H
 #define MPX_H
@@ -190,6 +191,30 @@ int mpx_linear_bwd(const void* X, const void* W, const void* dY, const void* Xpr
                    int64_t K, mpx_dtype dt, void* workspace, size_t ws_bytes,
                    int32_t* d_nonfinite, void* stream);
 size_t mpx_linear_bwd_workspace(int64_t M, int64_t N, int64_t K);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * mpx_linear_bwd without a workspace argument.  Same arguments, results
+ * (the same kernels, bit for bit) and errors as mpx_linear_bwd; the split-K
+ * and column partials live in a static device array of
+ * MPX_LINEAR_BWD_NOALLOC_SCRATCH bytes that the library holds on every GPU
+ * it runs on until the process ends.  The call allocates nothing (no
+ * hipMalloc, hipFree or allocating library routine).  A product whose
+ * mpx_linear_bwd_workspace(M, N, K) exceeds that size (column partials only,
+ * for a db-only call) is rejected with MPX_ERR_WORKSPACE before anything is
+ * launched.  The split-K partials of dW never exceed 32 MiB (at most 512
+ * output tiles of 128 x 128 float32 sums); the column partials of db take
+ * 4 bytes per output column per row slice, so only layers with more than
+ * about 16 million outputs are rejected (every weight gradient of the ViT
+ * workloads needs at most about 28 MB).  All calls on one GPU share its array: calls that overlap on that
+ * GPU (concurrent streams, or host threads) race and give wrong results;
+ * order them on one stream or with events.  The first call on a GPU looks up
+ * the array's device address (hipGetSymbolAddress, not a stream operation);
+ * make one call outside any graph capture first. */
+#define MPX_LINEAR_BWD_NOALLOC_SCRATCH (64u << 20)
+int mpx_linear_bwd_noalloc(const void* X, const void* W, const void* dY, const void* Xpre,
+                           int32_t x_act, void* dX, void* dW, void* db, int64_t M, int64_t N,
+                           int64_t K, mpx_dtype dt, int32_t* d_nonfinite, void* stream);
 
 /* Batched half GEMM with float32 accumulation (attention QK^T, PV and their
  * backward).  For i0 < nb0, i1 < nb1, with offsets o_X = i0*sX0 + i1*sX1

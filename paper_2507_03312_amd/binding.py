@@ -60,6 +60,7 @@ _SIGS = {
     "mpx_linear_fwd": (C.c_int, [P, P, P, P, P, P, I64, I64, I64, I32, I32, P]),
     "mpx_linear_bwd": (C.c_int, [P, P, P, P, I32, P, P, P, I64, I64, I64, I32, P, SZ, P, P]),
     "mpx_linear_bwd_workspace": (SZ, [I64, I64, I64]),
+    "mpx_linear_bwd_noalloc": (C.c_int, [P, P, P, P, I32, P, P, P, I64, I64, I64, I32, P, P]),
     "mpx_gemm_batched": (C.c_int, [I32, I32, I64, I64, I64, I64, I64, P, I64, I64, I64, P, I64,
                                    I64, I64, P, I64, I64, I64, I32, P]),
     "mpx_gemm_set_config": (C.c_int, [I32]),
@@ -165,6 +166,8 @@ def mpx_adamw_masked(p32: TensorList, m32: TensorList, v32: TensorList, grads: T
 
 mpx_linear_fwd = _call("mpx_linear_fwd")
 mpx_linear_bwd = _call("mpx_linear_bwd")
+mpx_linear_bwd_noalloc = _call("mpx_linear_bwd_noalloc")
+MPX_LINEAR_BWD_NOALLOC_SCRATCH = 64 << 20   # bytes (include/mpx.h)
 mpx_gemm_batched = _call("mpx_gemm_batched")
 mpx_gemm_set_config = _call("mpx_gemm_set_config")
 mpx_attention_fwd = _call("mpx_attention_fwd")

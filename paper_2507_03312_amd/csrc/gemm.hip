@@ -3,6 +3,8 @@
 // of gemm_kernels.h, which are compiled once per half type in gemm_f16.hip
 // and gemm_bf16.hip; float32 calls (full-precision training) go to the
 // kernels of gemm_f32.hip.
+#include <mutex>
+
 #include "gemm_f32.h"
 #include "gemm_kernels.h"
 
@@ -107,25 +109,34 @@ extern "C" size_t mpx_linear_bwd_workspace(int64_t M, int64_t N, int64_t K) {
   return std::max(ws, colsum_workspace(M, N)) + 256;
 }
 
-extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, const void* Xpre,
-                              int32_t x_act, void* dX, void* dW, void* db, int64_t M, int64_t N,
-                              int64_t K, mpx_dtype dt, void* workspace, size_t ws_bytes,
-                              int32_t* d_nonfinite, void* stream) {
-  clear_error();
-  MPX_REQUIRE(dY, "NULL dY");
-  MPX_REQUIRE(dX || dW || db, "nothing to compute: dX, dW and db are all NULL");
-  MPX_REQUIRE(!dX || W, "W is required for dX");
-  MPX_REQUIRE(!dW || X, "X is required for dW");
-  MPX_REQUIRE(M >= 1 && N >= 1 && K >= 1, "M, N, K must be >= 1");
-  MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
-  MPX_REQUIRE(x_act == MPX_ACT_NONE || x_act == MPX_ACT_GELU_TANH, "unknown activation");
-  MPX_REQUIRE(x_act == MPX_ACT_NONE || !dX || Xpre, "Xpre is required with x_act");
-  MPX_REQUIRE(dt != MPX_F32 || !d_nonfinite, "d_nonfinite is counted for half gradients only");
+// Shared body of mpx_linear_bwd and mpx_linear_bwd_noalloc (`fn` names the
+// entry point in error messages).
+#define MPX_REQUIRE_FN(cond, msg)                          \
+  do {                                                     \
+    if (!(cond)) {                                         \
+      ::mpx::set_error(std::string(fn) + ": " + (msg));    \
+      return MPX_ERR_INVALID;                              \
+    }                                                      \
+  } while (0)
+
+static int linear_bwd(const char* fn, const void* X, const void* W, const void* dY, const void* Xpre,
+                      int32_t x_act, void* dX, void* dW, void* db, int64_t M, int64_t N, int64_t K,
+                      mpx_dtype dt, void* workspace, size_t ws_bytes, int32_t* d_nonfinite,
+                      void* stream) {
+  MPX_REQUIRE_FN(dY, "NULL dY");
+  MPX_REQUIRE_FN(dX || dW || db, "nothing to compute: dX, dW and db are all NULL");
+  MPX_REQUIRE_FN(!dX || W, "W is required for dX");
+  MPX_REQUIRE_FN(!dW || X, "X is required for dW");
+  MPX_REQUIRE_FN(M >= 1 && N >= 1 && K >= 1, "M, N, K must be >= 1");
+  MPX_REQUIRE_FN(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
+  MPX_REQUIRE_FN(x_act == MPX_ACT_NONE || x_act == MPX_ACT_GELU_TANH, "unknown activation");
+  MPX_REQUIRE_FN(x_act == MPX_ACT_NONE || !dX || Xpre, "Xpre is required with x_act");
+  MPX_REQUIRE_FN(dt != MPX_F32 || !d_nonfinite, "d_nonfinite is counted for half gradients only");
   if (dW || db) {  // only the weight and bias gradients use the workspace
     // a bias-only call needs just the column partials
     const size_t need = dW ? mpx_linear_bwd_workspace(M, N, K) : colsum_workspace(M, N) + 256;
     if (ws_bytes < need || !workspace) {
-      set_error("mpx_linear_bwd: workspace of " + std::to_string(need) + " bytes required");
+      set_error(std::string(fn) + ": workspace of " + std::to_string(need) + " bytes required");
       return MPX_ERR_WORKSPACE;
     }
   }
@@ -214,6 +225,75 @@ extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, cons
   }
   return MPX_OK;
 }
+
+extern "C" int mpx_linear_bwd(const void* X, const void* W, const void* dY, const void* Xpre,
+                              int32_t x_act, void* dX, void* dW, void* db, int64_t M, int64_t N,
+                              int64_t K, mpx_dtype dt, void* workspace, size_t ws_bytes,
+                              int32_t* d_nonfinite, void* stream) {
+  clear_error();
+  return linear_bwd("mpx_linear_bwd", X, W, dY, Xpre, x_act, dX, dW, db, M, N, K, dt, workspace,
+                    ws_bytes, d_nonfinite, stream);
+}
+
+// ------------------------------------------- the variant that allocates nothing --
+//
+// mpx_linear_bwd_noalloc keeps its split-K and column partials in a
+// file-scope device array instead of a caller's workspace.  Each GPU the
+// library runs on holds its own copy of the array until the process ends.
+// In host code `scratch` names a host-side stand-in, not device memory: its
+// device address on the current GPU is looked up once per device with
+// hipGetSymbolAddress, kept in g_scratch, and only that address is passed to
+// kernels.  Nothing in the array needs to start at zero: every partial the
+// kernels read was written earlier in the same call.
+static __device__ __align__(256) unsigned char scratch[MPX_LINEAR_BWD_NOALLOC_SCRATCH];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices] = {};
+}  // namespace
+
+// Device address of the current GPU's scratch array (resolved on the first
+// call on that GPU).
+static int scratch_address(void** out) {
+  int dev = -1;
+  MPX_HIP(hipGetDevice(&dev));
+  MPX_REQUIRE(dev >= 0 && dev < kMaxDevices, "device index out of range");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    MPX_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    MPX_REQUIRE(p != nullptr, "scratch array has no device address");
+    g_scratch[dev] = p;
+  }
+  *out = g_scratch[dev];
+  return MPX_OK;
+}
+
+extern "C" int mpx_linear_bwd_noalloc(const void* X, const void* W, const void* dY,
+                                      const void* Xpre, int32_t x_act, void* dX, void* dW,
+                                      void* db, int64_t M, int64_t N, int64_t K, mpx_dtype dt,
+                                      int32_t* d_nonfinite, void* stream) {
+  clear_error();
+  const char* fn = "mpx_linear_bwd_noalloc";
+  MPX_REQUIRE_FN(M >= 1 && N >= 1 && K >= 1, "M, N, K must be >= 1");
+  if (dW || db) {  // the partials must fit the static array
+    const size_t need = dW ? mpx_linear_bwd_workspace(M, N, K) : colsum_workspace(M, N) + 256;
+    if (need > MPX_LINEAR_BWD_NOALLOC_SCRATCH) {
+      set_error(std::string(fn) + ": this product needs " + std::to_string(need) +
+                " bytes of partials, more than the " +
+                std::to_string((size_t)MPX_LINEAR_BWD_NOALLOC_SCRATCH) +
+                "-byte static scratch; use mpx_linear_bwd with a workspace");
+      return MPX_ERR_WORKSPACE;
+    }
+  }
+  void* ws = nullptr;
+  const int rc = scratch_address(&ws);
+  if (rc != MPX_OK) return rc;
+  return linear_bwd(fn, X, W, dY, Xpre, x_act, dX, dW, db, M, N, K, dt, ws,
+                    (size_t)MPX_LINEAR_BWD_NOALLOC_SCRATCH, d_nonfinite, stream);
+}
+#undef MPX_REQUIRE_FN
 
 extern "C" int mpx_gemm_batched(int32_t trans_a, int32_t trans_b, int64_t M, int64_t N, int64_t K,
                                 int64_t nb0, int64_t nb1, const void* A, int64_t lda, int64_t sA0,

@@ -58,5 +58,13 @@ def test_argument_checks_of_the_float32_and_fused_paths():
         mx.mpx_embed_assemble_bwd(p, p, p, p, 2, 3, 8, mx.MPX_F32, p, 0)
     with pytest.raises(mx.MPXError, match="MPX_F16 or MPX_BF16"):
         mx.mpx_layernorm_fwd_cast(p, 8, p, p, p, p, None, 4, 8, mx.MPX_F32, 0)
+    # the variant without a workspace rejects products whose partials exceed
+    # its static array before touching the device
+    M, N, K = 64, 1 << 25, 8   # 2^25 bias columns: 128 MiB of column partials
+    assert mx.mpx_linear_bwd_workspace(M, N, K) > mx.MPX_LINEAR_BWD_NOALLOC_SCRATCH
+    with pytest.raises(mx.MPXError, match="static scratch"):
+        mx.mpx_linear_bwd_noalloc(p, p, p, None, 0, None, p, p, M, N, K, mx.MPX_BF16, None, 0)
+    with pytest.raises(mx.MPXError, match="M, N, K"):
+        mx.mpx_linear_bwd_noalloc(p, p, p, None, 0, None, p, p, 0, N, K, mx.MPX_BF16, None, 0)
     with pytest.raises(mx.MPXError, match="MPX_F16, MPX_BF16 or MPX_F32"):
         mx.mpx_linear_fwd(p, p, None, None, p, None, 8, 8, 8, 7, 0, 0)
