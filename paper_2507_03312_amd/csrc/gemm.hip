@@ -13,8 +13,9 @@ namespace mpx {
 int g_forced_config = 0;
 
 static hipError_t gemm_dispatch(mpx_dtype dt, const GemmArgs& g, bool ak, bool bk, int64_t nbatch,
-                                hipStream_t s) {
-  return dt == MPX_F16 ? run_gemm_f16(g, ak, bk, nbatch, s) : run_gemm_bf16(g, ak, bk, nbatch, s);
+                                hipStream_t s, bool* db_fused = nullptr) {
+  return dt == MPX_F16 ? run_gemm_f16(g, ak, bk, nbatch, s, db_fused)
+                       : run_gemm_bf16(g, ak, bk, nbatch, s, db_fused);
 }
 
 static GemmArgs base_args() {
@@ -102,10 +103,22 @@ extern "C" int mpx_linear_fwd(const void* X, const void* W, const void* b, const
   return MPX_OK;
 }
 
+// Byte offset of the bias-gradient partials [splits][N] behind the split-K
+// partials [splits][N][K] in the workspace.
+static size_t db_partials_offset(int splits, int64_t N, int64_t K) {
+  return ((size_t)splits * N * K * sizeof(float) + 255) / 256 * 256;
+}
+
+// Bias-gradient partials of a split-K weight gradient: for each of the N
+// rows, one per split and 128-wide tile column of the K outputs.
+static size_t db_partials_count(int splits, int64_t N, int64_t K) {
+  return (size_t)splits * (size_t)((K + 127) / 128) * N;
+}
+
 extern "C" size_t mpx_linear_bwd_workspace(int64_t M, int64_t N, int64_t K) {
   if (M < 1 || N < 1 || K < 1) return 0;
   const int s = choose_splits(N, K, M);
-  size_t ws = s > 1 ? (size_t)s * N * K * sizeof(float) : 0;
+  size_t ws = s > 1 ? db_partials_offset(s, N, K) + db_partials_count(s, N, K) * sizeof(float) : 0;
   return std::max(ws, colsum_workspace(M, N)) + 256;
 }
 
@@ -187,6 +200,9 @@ static int linear_bwd(const char* fn, const void* X, const void* W, const void* 
     MPX_HIP(gemm_dispatch(dt, g, true, false, 1, s));
   }
   // dW[N,K] = dY^T X: A(m=n, k=m_tok) = dY[m_tok*N + n] (mn-major), B(n=k', k=m_tok) = X[m_tok*K + k']
+  // db[N] = sum over tokens of dY: summed by the same product's kernel from
+  // its dY fragments where that kernel can (db_fused), else column sums below
+  bool db_fused = false;
   if (dW) {
     GemmArgs g = base_args();
     g.A = (const uint16_t*)dY;
@@ -195,6 +211,7 @@ static int linear_bwd(const char* fn, const void* X, const void* W, const void* 
     g.M = N; g.N = K; g.K = M;
     g.lda = N; g.ldb = K; g.ldc = K;
     g.nonfinite = d_nonfinite;
+    g.db = (uint16_t*)db;
     int sp;
     int64_t ks;
     split_plan(N, K, M, sp, ks);
@@ -202,20 +219,24 @@ static int linear_bwd(const char* fn, const void* X, const void* W, const void* 
       g.splits = sp;
       g.k_split = ks;
       g.ws = (float*)workspace;
-      MPX_HIP(gemm_dispatch(dt, g, false, false, 1, s));
-      const int64_t MN = N * K;
+      g.dbp = db ? (float*)((char*)workspace + db_partials_offset(sp, N, K)) : nullptr;
+      MPX_HIP(gemm_dispatch(dt, g, false, false, 1, s, &db_fused));
+      // the GEMM wrote splits x (K / 128 tile columns) bias partials per row
+      const int64_t MN = N * K, nrows = db_fused ? N : 0;
+      const int dbparts = (int)(db_partials_count(sp, N, K) / N);
+      const unsigned blocks = splitk_reduce_blocks(MN, nrows);
       if (dt == MPX_F16)
-        splitk_reduce_kernel<MPX_F16><<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(g.ws, g.splits, MN, (uint16_t*)dW,
-                                                                            d_nonfinite);
+        splitk_reduce_kernel<MPX_F16><<<blocks, 256, 0, s>>>(g.ws, g.splits, MN, (uint16_t*)dW, d_nonfinite,
+                                                              g.dbp, dbparts, nrows, (uint16_t*)db);
       else
-        splitk_reduce_kernel<MPX_BF16><<<(unsigned)((MN + 255) / 256), 256, 0, s>>>(g.ws, g.splits, MN, (uint16_t*)dW,
-                                                                             d_nonfinite);
+        splitk_reduce_kernel<MPX_BF16><<<blocks, 256, 0, s>>>(g.ws, g.splits, MN, (uint16_t*)dW, d_nonfinite,
+                                                               g.dbp, dbparts, nrows, (uint16_t*)db);
       MPX_LAUNCHED();
     } else {
-      MPX_HIP(gemm_dispatch(dt, g, false, false, 1, s));
+      MPX_HIP(gemm_dispatch(dt, g, false, false, 1, s, &db_fused));
     }
   }
-  if (db) {
+  if (db && !db_fused) {
     if (dt == MPX_F16)
       MPX_HIP(colsum_run<MPX_F16>((const uint16_t*)dY, M, N, (float*)workspace, (uint16_t*)db,
                                            d_nonfinite, s));

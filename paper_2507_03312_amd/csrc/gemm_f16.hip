@@ -3,8 +3,9 @@
 
 namespace mpx {
 
-hipError_t run_gemm_f16(const GemmArgs& g, bool ak, bool bk, int64_t nbatch, hipStream_t s) {
-  return run_gemm<MPX_F16>(g, ak, bk, nbatch, s);
+hipError_t run_gemm_f16(const GemmArgs& g, bool ak, bool bk, int64_t nbatch, hipStream_t s,
+                         bool* db_fused) {
+  return run_gemm<MPX_F16>(g, ak, bk, nbatch, s, db_fused);
 }
 
 }  // namespace mpx

@@ -55,6 +55,13 @@ struct GemmArgs {
   // instead); such calls take the generic epilogue or the whole-tile one
   // compiled with EPI_COUNT
   int32_t* nonfinite;
+  // weight-gradient products (both operands mn-major) may also return the
+  // bias gradient db[m] = half(sum_k A(m, k)), summed from the A fragments
+  // the MFMAs read: set by the dispatcher only for the kernel variant that
+  // does it.  Split-K calls write float32 partial sums dbp[split][M] instead,
+  // which the split-K reduction adds in split order.
+  uint16_t* db;
+  float* dbp;
 };
 
 // Loader of one operand tile (ROWS output rows x BK reduction values) into
@@ -675,7 +682,29 @@ struct FragReader {
 
 // OCC: waves per SIMD the register budget is sized for.  E: the epilogue
 // variant of whole tiles (EPI_GENERIC: always the generic epilogue).
-template <int DT, int BM, int BN, int WM, int WN, int S, int OCC, bool AK, bool BKM, int E>
+// Sum of the 8 half values of an MFMA operand fragment, in a fixed pairwise order.
+template <int DT>
+__device__ __forceinline__ float frag_sum8(const uint4& f) {
+  const uint32_t w[4] = {f.x, f.y, f.z, f.w};
+  float p[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) p[k] = h2f<DT>((uint16_t)(w[k] & 0xFFFFu)) + h2f<DT>((uint16_t)(w[k] >> 16));
+  return (p[0] + p[1]) + (p[2] + p[3]);
+}
+
+// DBS: also sum the rows of A over this workgroup's k range (the bias
+// gradient of a weight-gradient product; see GemmArgs::db).  The waves of
+// the left half of the tile (wn0 == 0) add up their A fragments as the MFMAs
+// consume them: lane l holds 8 consecutive k of row l % 32 (k half l / 32),
+// so per lane a running float32 sum per fragment, in k order, and at the end
+// lane l plus lane l + 32 give the row's sum.  With split-K the work is
+// spread over the C tile columns that share the A rows: the workgroup of
+// column c sums the k tiles kt = c, c + C, ... of its split and writes
+// partial dbp[row][split * C + c] (the reduction adds a row's C x splits
+// partials with one wave, in a fixed order); without split-K column 0 sums
+// every k tile and writes db itself.
+template <int DT, int BM, int BN, int WM, int WN, int S, int OCC, bool AK, bool BKM, int E,
+          bool DBS = false>
 __global__ __launch_bounds__((BM / WM) * (BN / WN) * 64)
 __attribute__((amdgpu_waves_per_eu(OCC, OCC)))
 void gemm_dma_kernel(GemmArgs g) {
@@ -729,6 +758,15 @@ void gemm_dma_kernel(GemmArgs g) {
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.0f;
     });
   });
+  // bias-gradient sums: tile columns sharing the A rows, this one's index,
+  // and the next k tile this wave adds up (uniform over the wave)
+  const int db_cols = g.splits > 1 ? (int)((g.N + BN - 1) / BN) : 1;
+  const int db_col = g.splits > 1 ? (int)(n0 / BN) : 0;
+  const bool dbw = DBS && wn0 == 0 && (g.splits > 1 || n0 == 0);
+  int db_next = db_col;
+  float dbs[TM];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) dbs[i] = 0.0f;
 
   auto issue = [&](int kt) {
     const uint32_t st = lds0 + (uint32_t)((kt % S) * STAGE);
@@ -741,6 +779,8 @@ void gemm_dma_kernel(GemmArgs g) {
     if (s < nk) issue(s);
 
   for (int kt = 0; kt < nk; ++kt) {
+    const bool db_now = dbw && kt == db_next;
+    if (db_now) db_next += db_cols;
     // tile kt has landed once at most min(S - 2, nk - 1 - kt) later tiles are in flight
     const int later = min(S - 2, nk - 1 - kt);
     static_for<S - 1>([&](auto p) {
@@ -765,8 +805,31 @@ void gemm_dma_kernel(GemmArgs g) {
       static_for<TM>([&](auto i) {
         static_for<TN>([&](auto j) { acc[i][j] = mfma32<DT>(bf[cur][j], af[cur][i], acc[i][j]); });
       });
+      if constexpr (DBS) {
+        if (db_now) static_for<TM>([&](auto i) { dbs[i] += frag_sum8<DT>(af[cur][i]); });
+      }
       __builtin_amdgcn_sched_barrier(0);
     });
+  }
+  if constexpr (DBS) {
+    if (dbw) {
+      int bad = 0;
+      static_for<TM>([&](auto i) {
+        const float other = __shfl_xor(dbs[i], 32);  // the row's other 8 k of every step
+        const int64_t row = m0 + wm0 + 32 * i + lane;
+        if (lane < 32 && row < g.M) {
+          const float v = dbs[i] + other;
+          if (g.splits > 1) {
+            g.dbp[row * ((int64_t)g.splits * db_cols) + (int64_t)split * db_cols + db_col] = v;
+          } else {
+            const uint16_t h = f2h<DT>(v);
+            g.db[row] = h;
+            bad += h_nonfinite<DT>(h) ? 1 : 0;
+          }
+        }
+      });
+      if (g.nonfinite) add_nonfinite(g.nonfinite, bad);
+    }
   }
   // the accumulators hold C^T blocks (the MFMA operands are swapped above)
   if constexpr (E != EPI_GENERIC) {
@@ -884,19 +947,46 @@ void gemm_dma_persistent_kernel(GemmArgs g) {
   }
 }
 
-// Sum of split-K partials in split order, one rounding: C = half(sum_s W[s]);
-// non-finite results are added to *nonfinite when it is set.
+// Sum of split-K partials in split order, one rounding: C = half(sum_s W[s]),
+// one thread per output in the first ceil(MN / 256) workgroups.  The
+// workgroups after them reduce the bias-gradient partials dbp[row][p],
+// p < dbparts, one wave per row (nrows rows; 0: none): lane l adds p = l,
+// l + 64, ... in order, then the fixed wave tree of wave_sum; db = half of
+// that.  Non-finite results are added to *nonfinite when it is set.
 template <int DT>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ ws, int splits,
                                                             int64_t MN, uint16_t* __restrict__ C,
-                                                            int32_t* __restrict__ nonfinite) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= MN) return;
-  float s = ws[i];
-  for (int k = 1; k < splits; ++k) s += ws[(int64_t)k * MN + i];
-  const uint16_t h = f2h<DT>(s);
-  C[i] = h;
-  if (nonfinite) add_nonfinite(nonfinite, h_nonfinite<DT>(h) ? 1 : 0);
+                                                            int32_t* __restrict__ nonfinite,
+                                                            const float* __restrict__ dbp, int dbparts,
+                                                            int64_t nrows, uint16_t* __restrict__ db) {
+  const int64_t mn_blocks = (MN + 255) / 256;
+  if ((int64_t)blockIdx.x < mn_blocks) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= MN) return;
+    float s = ws[i];
+    for (int k = 1; k < splits; ++k) s += ws[(int64_t)k * MN + i];
+    const uint16_t h = f2h<DT>(s);
+    C[i] = h;
+    if (nonfinite) add_nonfinite(nonfinite, h_nonfinite<DT>(h) ? 1 : 0);
+    return;
+  }
+  const int64_t row = ((int64_t)blockIdx.x - mn_blocks) * 4 + (threadIdx.x >> 6);
+  if (row >= nrows) return;  // uniform over the wave
+  const int lane = threadIdx.x & 63;
+  const float* p = dbp + row * dbparts;
+  float s = 0.0f;
+  for (int k = lane; k < dbparts; k += 64) s += p[k];
+  s = wave_sum(s);
+  if (lane == 0) {
+    const uint16_t h = f2h<DT>(s);
+    db[row] = h;
+    if (nonfinite) add_nonfinite(nonfinite, h_nonfinite<DT>(h) ? 1 : 0);
+  }
+}
+
+// launch shape of splitk_reduce_kernel: MN outputs and nrows bias rows
+inline unsigned splitk_reduce_blocks(int64_t MN, int64_t nrows) {
+  return (unsigned)((MN + 255) / 256 + (nrows + 3) / 4);
 }
 
 // ------------------------------------------------------------ dispatch --
@@ -966,6 +1056,7 @@ static hipError_t launch_dma(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipSt
   // any other counting call takes the generic epilogue
   const int e = g.full_epi ? epilogue_mask(g) | (g.nonfinite ? EPI_COUNT : 0) : EPI_GENERIC;
 #define MPX_D(AKv, BKv, Ev) gemm_dma_kernel<DT, BM, BN, WM, WN, S, OCC, AKv, BKv, Ev><<<grid, NT, 0, s>>>(g)
+#define MPX_DB(Ev) gemm_dma_kernel<DT, BM, BN, WM, WN, S, OCC, false, false, Ev, true><<<grid, NT, 0, s>>>(g)
   if constexpr (BM == 64) {
     // 64 x 128 tiles (outputs too small to fill the CUs with 128 x 128): the
     // A operand must be k-major (dma_ok rejects the rest)
@@ -1005,6 +1096,10 @@ static hipError_t launch_dma(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipSt
     } else if (!ak && bk) {
       if (e == 0) MPX_D(false, true, 0);
       else MPX_D(false, true, EPI_GENERIC);
+    } else if (g.db) {  // weight gradient with the bias gradient summed alongside
+      if (e == 0) MPX_DB(0);
+      else if (e == EPI_COUNT) MPX_DB(EPI_COUNT);
+      else MPX_DB(EPI_GENERIC);
     } else {
       if (e == 0) MPX_D(false, false, 0);
       else if (e == EPI_COUNT) MPX_D(false, false, EPI_COUNT);
@@ -1017,6 +1112,7 @@ static hipError_t launch_dma(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipSt
     else MPX_D(false, false, EPI_GENERIC);
   }
 #undef MPX_D
+#undef MPX_DB
   return hipGetLastError();
 }
 
@@ -1170,11 +1266,23 @@ static hipError_t launch_small(const GemmArgs& g, bool ak, bool bk, hipStream_t 
   return hipGetLastError();
 }
 
-// ak: A is k-major; bk: B is k-major.
+// ak: A is k-major; bk: B is k-major.  A call with g.db set (a weight
+// gradient whose bias gradient is wanted) gets it from the GEMM when the
+// chosen kernel can sum it (the two-stage 128 x 128 direct-to-LDS kernel
+// with both operands mn-major); *db_fused tells the caller whether it did,
+// and otherwise the caller computes the column sums itself.
 template <int DT>
-static hipError_t run_gemm(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipStream_t s) {
+static hipError_t run_gemm(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipStream_t s,
+                           bool* db_fused) {
   const bool vec = aligned_vec(g.A, g.lda, g.sA0, g.sA1) && aligned_vec(g.B, g.ldb, g.sB0, g.sB1);
-  switch (choose_config(g, vec, ak, bk, nbatch)) {
+  const int cfg = choose_config(g, vec, ak, bk, nbatch);
+  const bool fuse = g.db && cfg == 7 && !ak && !bk && nbatch == 1 && (g.splits == 1 || g.dbp);
+  if (db_fused) *db_fused = fuse;
+  if (!fuse) {
+    g.db = nullptr;
+    g.dbp = nullptr;
+  }
+  switch (cfg) {
     case 8: return launch_small<DT>(g, ak, bk, s);
     case 1: return launch_cfg<DT, 64, 64, 32, 32>(g, ak, bk, vec, nbatch, s);
     case 2: return launch_cfg<DT, 128, 128, 64, 32, 64, 4>(g, ak, bk, vec, nbatch, s);
@@ -1191,7 +1299,9 @@ static hipError_t run_gemm(GemmArgs g, bool ak, bool bk, int64_t nbatch, hipStre
   }
 }
 
-hipError_t run_gemm_f16(const GemmArgs& g, bool ak, bool bk, int64_t nbatch, hipStream_t s);
-hipError_t run_gemm_bf16(const GemmArgs& g, bool ak, bool bk, int64_t nbatch, hipStream_t s);
+hipError_t run_gemm_f16(const GemmArgs& g, bool ak, bool bk, int64_t nbatch, hipStream_t s,
+                        bool* db_fused = nullptr);
+hipError_t run_gemm_bf16(const GemmArgs& g, bool ak, bool bk, int64_t nbatch, hipStream_t s,
+                         bool* db_fused = nullptr);
 
 }  // namespace mpx
