@@ -549,174 +549,6 @@ __global__ __launch_bounds__(NB * 64) void attn_bwd_dq_kernel(const uint16_t* __
   bwd_dq<DT, NB>(lds_u32(sK), Sr, dqkv + (int64_t)b * T * ld + h * HD + q * ld, q, T, lane);
 }
 
-// 8-byte LDS accesses at byte address addr
-__device__ __forceinline__ u32x2 lds_b64(uint32_t addr) {
-  return *(const __attribute__((address_space(3))) u32x2*)(uintptr_t)addr;
-}
-__device__ __forceinline__ void lds_st_b64(uint32_t addr, u32x2 v) {
-  *(__attribute__((address_space(3))) u32x2*)(uintptr_t)addr = v;
-}
-
-// The query block of bwd_query_block with V and the block's probability rows
-// read from LDS: V staged as [key][PD] (rows >= T zero), P as [query][pp]
-// (prow: byte address of the lane's query row).  Same arithmetic, same
-// results (rs adds the same products in the same order): a key >= T
-// contributes a zero dP there instead of a clamped one that the masks
-// discard.
-template <int DT, int NB>
-__device__ __forceinline__ void bwd_query_block_lds(uint32_t vbase, const uint16_t* G, int dm, uint32_t prow,
-                                                    int q, int T, float scale, int lane,
-                                                    u32x2 (&Pr)[NB][4], u32x2 (&Sr)[NB][4]) {
-  const int hi = lane >> 5;
-  const int qc = min(q, T - 1);
-  uint4 gf[4];
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) gf[kk] = ld_u4(G + qc * dm + 16 * kk + 8 * hi);
-  // dP^T block by block, rounded to half at once and kept packed (the
-  // float32 sums are needed only for that rounding): 4 registers per 16
-  // values instead of 16
-  u32x2 dph[NB][4];
-  static_for<NB>([&](auto j) {
-    const int key = 32 * j + (lane & 31);
-    f32x16 acc;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
-      acc = mfma32<DT>(lds_b128(vbase + (uint32_t)((key * PD + 16 * kk + 8 * hi) * 2)), gf[kk], acc);
-#pragma unroll
-    for (int gq = 0; gq < 4; ++gq)
-      dph[j][gq] = pack4(f2h<DT>(acc[4 * gq]), f2h<DT>(acc[4 * gq + 1]), f2h<DT>(acc[4 * gq + 2]),
-                         f2h<DT>(acc[4 * gq + 3]));
-    // one key block's V fragments at a time (hoisting every block's reads
-    // ahead of the MFMAs needs over a hundred more registers and spills)
-    __builtin_amdgcn_sched_barrier(0);
-  });
-  auto unpack = [](const u32x2& w, float (&f)[4]) {
-    f[0] = h2f<DT>((uint16_t)(w.x & 0xFFFFu));
-    f[1] = h2f<DT>((uint16_t)(w.x >> 16));
-    f[2] = h2f<DT>((uint16_t)(w.y & 0xFFFFu));
-    f[3] = h2f<DT>((uint16_t)(w.y >> 16));
-  };
-  float rs = 0.0f;
-  static_for<NB>([&](auto j) {
-#pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      const int key0 = 32 * j + 8 * gq + 4 * hi;
-      Pr[j][gq] = (q < T && key0 < T) ? lds_b64(prow + (uint32_t)(key0 * 2)) : u32x2{0u, 0u};
-      float d[4], ph[4];
-      unpack(dph[j][gq], d);
-      unpack(Pr[j][gq], ph);
-#pragma unroll
-      for (int c = 0; c < 4; ++c)
-        if (key0 + c < T) rs += d[c] * ph[c];
-    }
-  });
-  rs += __shfl_xor(rs, 32);
-  static_for<NB>([&](auto j) {
-#pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      const int key0 = 32 * j + 8 * gq + 4 * hi;
-      float d[4], ph[4];
-      unpack(dph[j][gq], d);
-      unpack(Pr[j][gq], ph);
-      uint16_t ds[4];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const bool ok = q < T && key0 + c < T;
-        ds[c] = ok ? f2h<DT>((scale * ph[c]) * (d[c] - rs)) : (uint16_t)0;
-      }
-      Sr[j][gq] = pack4(ds[0], ds[1], ds[2], ds[3]);
-    }
-  });
-}
-
-// 128 < T <= 224, first kernel, staged form: every global access coalesced.
-// The head's V rows and the [T, ldP] probability block are copied into LDS
-// with 16-byte loads (one pass for the workgroup, instead of each wave
-// reading all of V and each lane its own query's P row, 32 rows per
-// instruction); each wave's dS rows go back through the same LDS rows and
-// leave with 16-byte stores; V's LDS then takes K for the dQ product.  LDS: TK x 72 + TK x (TK + 4)
-// halves (131 KiB at T = 224).
-template <int DT, int NB>
-__global__ __launch_bounds__(NB * 64) void attn_bwd_dq_staged_kernel(const uint16_t* __restrict__ qkv,
-                                                                     const uint16_t* __restrict__ P,
-                                                                     const uint16_t* __restrict__ dO,
-                                                                     uint16_t* __restrict__ dqkv,
-                                                                     uint16_t* __restrict__ dS, int T, int H,
-                                                                     int ldP, float scale) {
-  constexpr int TK = 32 * NB;
-  constexpr int NT = NB * 64;
-  constexpr int PP = TK + 4;  // row pitch (halves) of the probability rows: 8-byte aligned rows
-                              // whose 32 starts spread over distinct pairs of banks
-  constexpr int PCH = (TK * (TK / 8) + NT - 1) / NT;  // 16-byte chunks per thread (ldP <= TK)
-  __shared__ __attribute__((aligned(16))) uint16_t sA[TK * PD];  // V, then K
-  __shared__ __attribute__((aligned(16))) uint16_t sP[TK * PP];  // P rows, then dS rows
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int bh = blockIdx.x, b = bh / H, h = bh % H;
-  const int dm = H * HD;
-  const int64_t ld = 3 * (int64_t)dm;
-  const uint16_t* Q = qkv + (int64_t)b * T * ld + h * HD;
-  const uint16_t* G = dO + (int64_t)b * T * dm + h * HD;
-  const uint16_t* Pb = P + (int64_t)bh * T * ldP;
-  uint16_t* Sb = dS + (int64_t)bh * T * ldP;
-  const uint32_t abase = lds_u32(sA), pbase = lds_u32(sP);
-  const int cpr = ldP / 8;  // 16-byte chunks per probability row
-  {
-    RowStage<4> vst;
-    vst.load(Q + 2 * dm, ld, T, TK, tid, NT);
-    u32x4 pv[PCH];
-#pragma unroll
-    for (int i = 0; i < PCH; ++i) {
-      const int c = tid + i * NT;
-      const int r = c / cpr, col = (c % cpr) * 8;
-      pv[i] = u32x4{0u, 0u, 0u, 0u};
-      if (r < T) pv[i] = *reinterpret_cast<const u32x4*>(Pb + (int64_t)r * ldP + col);
-    }
-    vst.store(sA, TK, tid, NT);
-#pragma unroll
-    for (int i = 0; i < PCH; ++i) {
-      const int c = tid + i * NT;
-      const int r = c / cpr, col = (c % cpr) * 8;
-      if (r < TK) {
-        const uint32_t a = pbase + (uint32_t)((r * PP + col) * 2);
-        lds_st_b64(a, u32x2{pv[i].x, pv[i].y});
-        lds_st_b64(a + 8, u32x2{pv[i].z, pv[i].w});
-      }
-    }
-  }
-  __syncthreads();  // V and P staged
-
-  const int q = 32 * w + (lane & 31);
-  const uint32_t prow = pbase + (uint32_t)(q * PP * 2);
-  u32x2 Pr[NB][4], Sr[NB][4];
-  bwd_query_block_lds<DT, NB>(abase, G, dm, prow, q, T, scale, lane, Pr, Sr);
-  // this wave's dS rows over its P rows (no other wave reads them)
-  static_for<NB>([&](auto j) {
-#pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      const int key0 = 32 * j + 8 * gq + 4 * (lane >> 5);
-      if (key0 < ldP) lds_st_b64(prow + (uint32_t)(key0 * 2), Sr[j][gq]);
-    }
-  });
-  __syncthreads();  // dS rows written; every wave is done with V
-  for (int c = lane; c < 32 * cpr; c += 64) {
-    const int r = 32 * w + c / cpr, col = (c % cpr) * 8;
-    if (r < T) {
-      const uint32_t a = pbase + (uint32_t)((r * PP + col) * 2);
-      const u32x2 lo = lds_b64(a), hi2 = lds_b64(a + 8);
-      *reinterpret_cast<u32x4*>(Sb + (int64_t)r * ldP + col) = u32x4{lo.x, lo.y, hi2.x, hi2.y};
-    }
-  }
-  {
-    RowStage<4> kst;
-    kst.load(Q + dm, ld, T, TK, tid, NT);
-    kst.store(sA, TK, tid, NT);
-  }
-  __syncthreads();  // K staged
-  bwd_dq<DT, NB>(abase, Sr, dqkv + (int64_t)b * T * ld + h * HD + q * ld, q, T, lane);
-}
-
 // 128 < T <= 256, second kernel: per key block (wave w) dK = dS^T Q and
 // dV = P^T dO, reduced over the queries in blocks of 32 staged through LDS.
 template <int DT, int NB>
@@ -826,24 +658,18 @@ hipError_t launch_bwd(const uint16_t* qkv, const uint16_t* P, const uint16_t* dO
     attn_bwd_dq_kernel<DT, NBv><<<grid, NBv * 64, 0, s>>>(qkv, P, dO, dqkv, dS, T, H, ldP, scale); \
     attn_bwd_dkv_kernel<DT, NBv><<<grid, NBv * 64, 0, s>>>(qkv, P, dO, dS, dqkv, T, H, ldP);       \
   } while (0)
-#define MPX_B3(NBv)                                                                                     \
-  do {                                                                                                  \
-    attn_bwd_dq_staged_kernel<DT, NBv><<<grid, NBv * 64, 0, s>>>(qkv, P, dO, dqkv, dS, T, H, ldP, scale); \
-    attn_bwd_dkv_kernel<DT, NBv><<<grid, NBv * 64, 0, s>>>(qkv, P, dO, dS, dqkv, T, H, ldP);              \
-  } while (0)
   switch (nb) {
     case 1: MPX_B(1); break;
     case 2: MPX_B(2); break;
     case 3: MPX_B(3); break;
     case 4: MPX_B(4); break;
-    case 5: MPX_B3(5); break;
-    case 6: MPX_B3(6); break;
-    case 7: MPX_B3(7); break;
-    default: MPX_B2(8); break;  // the staged form's LDS would exceed 160 KiB
+    case 5: MPX_B2(5); break;
+    case 6: MPX_B2(6); break;
+    case 7: MPX_B2(7); break;
+    default: MPX_B2(8); break;
   }
 #undef MPX_B
 #undef MPX_B2
-#undef MPX_B3
   return hipGetLastError();
 }
 
