@@ -452,6 +452,7 @@ def main():
     torch.cuda.synchronize()
     ms = t0.elapsed_time(t1) / steps
     if args.step_only:
+        calibration_copy(args, dev)
         print(f"step-only: {warm} eager steps, then {warm + steps} graph replays of the step "
               f"({2 * warm + steps} steps in all; the first eager step also casts the masters)",
               file=sys.stderr)

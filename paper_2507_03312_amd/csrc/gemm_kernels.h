@@ -794,10 +794,14 @@ void gemm_dma_kernel(GemmArgs g) {
     if (kt + S - 1 < nk) issue(kt + S - 1);
     const uint32_t sa = lds0 + (uint32_t)((kt % S) * STAGE), sb = sa + A_BYTES;
     // fragments double-buffered over the four k steps of 16: the LDS reads
-    // of step kk + 1 are issued while the MFMAs of step kk run, one MFMA
-    // then its share of the reads, alternately (scheduling group barriers;
-    // issuing all reads ahead of the step's MFMAs measured 5-15% slower on
-    // the ViT-B layer products)
+    // of step kk + 1 are issued ahead of the MFMAs of step kk.  Products
+    // with an mn-major operand (dX, dW: transposing reads, two per
+    // fragment) interleave one MFMA with its share of those reads
+    // (scheduling group barriers: dW +8-17% on the ViT-B layers); the
+    // forward products (both operands k-major) issue the step's reads as a
+    // group before its MFMAs (scheduling barriers), which measured 1-2%
+    // faster for them.
+    constexpr bool kInterleave = !(AK && BKM);
     uint4 af[2][TM], bf[2][TN];
     static_for<TM>([&](auto i) { af[0][i] = fa.template read<i, 0>(sa); });
     static_for<TN>([&](auto j) { bf[0][j] = fb.template read<j, 0>(sb); });
@@ -807,15 +811,18 @@ void gemm_dma_kernel(GemmArgs g) {
         static_for<TM>([&](auto i) { af[nxt][i] = fa.template read<i, kk + 1>(sa); });
         static_for<TN>([&](auto j) { bf[nxt][j] = fb.template read<j, kk + 1>(sb); });
       }
+      if constexpr (!kInterleave) __builtin_amdgcn_sched_barrier(0);
       static_for<TM>([&](auto i) {
         static_for<TN>([&](auto j) { acc[i][j] = mfma32<DT>(bf[cur][j], af[cur][i], acc[i][j]); });
       });
       if constexpr (DBS) {
         if (db_now) static_for<TM>([&](auto i) { dbs[i] += frag_sum8<DT>(af[cur][i]); });
       }
-      if constexpr (kk + 1 < 4) {
+      if constexpr (!kInterleave) {
+        __builtin_amdgcn_sched_barrier(0);
+      } else if constexpr (kk + 1 < 4) {
         static_for<TM * TN>([&](auto) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);        // one MFMA
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);              // one MFMA
           __builtin_amdgcn_sched_group_barrier(0x100, kReadsPerMfma, 0);  // its LDS reads
         });
       }
