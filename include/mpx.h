@@ -262,10 +262,10 @@ int mpx_attention_fwd(const void* qkv, void* O, void* P, int64_t B, int64_t T, i
  *   dS = half(scale P (dP - rowsum(dP P))) (float32 math, scale = 1/sqrt(hd));
  *   dQ = half(dS K);  dK = half(dS^T Q),
  * written into dqkv [B*T, 3*H*hd] in the layout of qkv.  Same limits and
- * alignment as the forward (dO and dqkv 16-byte aligned).  For T > 128 dS
- * passes through a caller-owned, 16-byte aligned workspace of
- * mpx_attention_bwd_workspace(B, T, H, hd) bytes (0 for T <= 128, where
- * workspace may be NULL); a smaller one returns MPX_ERR_WORKSPACE. */
+ * alignment as the forward (dO and dqkv 16-byte aligned).  One kernel, dS
+ * never leaves the chip: workspace and ws_bytes are accepted for
+ * compatibility and ignored (workspace may be NULL), and
+ * mpx_attention_bwd_workspace returns 0. */
 int mpx_attention_bwd(const void* qkv, const void* P, const void* dO, void* dqkv, int64_t B,
                       int64_t T, int64_t H, int64_t hd, mpx_dtype dt, void* workspace,
                       size_t ws_bytes, void* stream);

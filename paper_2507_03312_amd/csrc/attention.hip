@@ -18,10 +18,10 @@
 // accumulator layout into the MFMA B-operand layout (8 consecutive keys per
 // lane).  V, and in the backward K, Q, dO, P and dS, are staged in LDS and
 // read as transposed MFMA operands with ds_read_b64_tr_b16.  Up to T = 128
-// the backward is one kernel; beyond, the [T, T] probability and dS blocks no
-// longer fit in LDS next to K, Q and dO, so dS goes through a workspace: one
-// kernel per query block (dS, dQ), then one per key block (dK, dV, reducing
-// over queries in blocks of 32 staged through LDS).
+// the backward keeps the [T, T] probability and dS blocks in LDS; beyond,
+// they no longer fit next to K, V, Q and dO, and each wave keeps its own
+// query block's P and dS in registers and hands them to the others through
+// a [32, T] slab in LDS, one query block at a time (attn_bwd_fused_kernel).
 //
 // Layouts: qkv [B*T, 3*H*64] (Q | K | V, head h at columns h*64 of each
 // third), O and dO [B*T, H*64], dqkv like qkv, P [B*H, T, ldP] with
@@ -68,6 +68,25 @@ struct RowStage {
       const int c = tid + i * nthreads;
       v[i] = u32x4{0u, 0u, 0u, 0u};
       if (c < rows * 8 && (c >> 3) < T) v[i] = *reinterpret_cast<const u32x4*>(src + (c >> 3) * ld + (c & 7) * 8);
+    }
+  }
+  // The same without branches, for rows * 8 == PER * nthreads: rows >= T
+  // load row T - 1 and are replaced by 0 in store_clamped().
+  __device__ __forceinline__ void load_clamped(const uint16_t* src, int64_t ld, int T, int tid,
+                                               int nthreads) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * nthreads;
+      v[i] = *reinterpret_cast<const u32x4*>(src + min(c >> 3, T - 1) * ld + (c & 7) * 8);
+    }
+  }
+  __device__ __forceinline__ void store_clamped(uint16_t* lds, int T, int tid, int nthreads) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = tid + i * nthreads;
+      asm volatile("" : "+v"(v[i]));  // keeps the load unconditional
+      if ((c >> 3) >= T) v[i] = u32x4{0u, 0u, 0u, 0u};
+      *reinterpret_cast<u32x4*>(lds + (c >> 3) * PD + (c & 7) * 8) = v[i];
     }
   }
   __device__ __forceinline__ void store(uint16_t* lds, int rows, int tid, int nthreads) const {
@@ -329,35 +348,34 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_kernel(const uint16_t* __res
 
 // ---------------------------------------------------------------- backward --
 
-// Per query block (the wave's 32 queries q): dP^T = V dO^T rounded to half,
-// the probabilities P of query q, and dS = half(scale P (dP - rowsum(dP P)))
-// (0 for keys >= T and for queries >= T).  Pr / Sr hold 4 consecutive keys
-// 32 j + 8 gq + 4 hi + (0..3) per entry, as in the forward.
-template <int DT, int NB>
-__device__ __forceinline__ void bwd_query_block(const uint16_t* V, int64_t ld, const uint16_t* G, int dm,
-                                                const uint16_t* Prow, int q, int T, float scale,
-                                                int lane, u32x2 (&Pr)[NB][4], u32x2 (&Sr)[NB][4]) {
+// The probabilities of query q in the layout of an S^T accumulator (entry
+// [j][gq] holds keys 32 j + 8 gq + 4 hi + (0..3)); 0 past T and for q >= T.
+template <int NB>
+__device__ __forceinline__ void load_prob_rows(const uint16_t* Prow, int q, int T, int lane,
+                                               u32x2 (&Pr)[NB][4]) {
   const int hi = lane >> 5;
-  const int qc = min(q, T - 1);
-  uint4 gf[4];
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) gf[kk] = ld_u4(G + qc * dm + 16 * kk + 8 * hi);
-  f32x16 dp[NB];
-  static_for<NB>([&](auto j) {
-    const int key = min(32 * j + (lane & 31), T - 1);
-    f32x16 acc;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) acc = mfma32<DT>(ld_u4(V + key * ld + 16 * kk + 8 * hi), gf[kk], acc);
-    dp[j] = acc;
-  });
-  float rs = 0.0f;
   static_for<NB>([&](auto j) {
 #pragma unroll
     for (int gq = 0; gq < 4; ++gq) {
       const int key0 = 32 * j + 8 * gq + 4 * hi;
       Pr[j][gq] = (q < T && key0 < T) ? ld_u2(Prow + key0) : u32x2{0u, 0u};
+    }
+  });
+}
+
+// From the float32 accumulators dp (dP^T of the wave's queries, one block of
+// 32 keys each) and the probabilities Pr of query q: dP rounded to half, the
+// row sum rs = sum_k dP P over keys < T, and dS = half(scale P (dP - rs))
+// packed like Pr (0 for keys >= T and for queries >= T).
+template <int DT, int NB>
+__device__ __forceinline__ void probs_to_ds(f32x16 (&dp)[NB], const u32x2 (&Pr)[NB][4], int q, int T,
+                                            float scale, int lane, u32x2 (&Sr)[NB][4]) {
+  const int hi = lane >> 5;
+  float rs = 0.0f;
+  static_for<NB>([&](auto j) {
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const int key0 = 32 * j + 8 * gq + 4 * hi;
       const uint16_t ph[4] = {(uint16_t)(Pr[j][gq].x & 0xFFFFu), (uint16_t)(Pr[j][gq].x >> 16),
                               (uint16_t)(Pr[j][gq].y & 0xFFFFu), (uint16_t)(Pr[j][gq].y >> 16)};
 #pragma unroll
@@ -386,13 +404,94 @@ __device__ __forceinline__ void bwd_query_block(const uint16_t* V, int64_t ld, c
   });
 }
 
-// dQ^T = K^T dS^T for the wave's queries (K staged in LDS as [key][d]),
-// stored for queries < T.
+// Two halves packed in a dword <-> float32 (exact widening; narrowing
+// rounds to nearest even, as f2h).
+typedef float f32x2v __attribute__((ext_vector_type(2)));
+template <int DT> __device__ __forceinline__ void unpack2(uint32_t v, float& a, float& b);
+template <> __device__ __forceinline__ void unpack2<MPX_BF16>(uint32_t v, float& a, float& b) {
+  a = __builtin_bit_cast(float, v << 16);
+  b = __builtin_bit_cast(float, v & 0xFFFF0000u);
+}
+template <> __device__ __forceinline__ void unpack2<MPX_F16>(uint32_t v, float& a, float& b) {
+  a = (float)__builtin_bit_cast(_Float16, (uint16_t)(v & 0xFFFFu));
+  b = (float)__builtin_bit_cast(_Float16, (uint16_t)(v >> 16));
+}
+template <int DT> __device__ __forceinline__ uint32_t pack2(float a, float b);
+template <> __device__ __forceinline__ uint32_t pack2<MPX_BF16>(float a, float b) {
+  typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2v){a, b}, bf16x2v));
+}
+template <> __device__ __forceinline__ uint32_t pack2<MPX_F16>(float a, float b) {
+  // two scalar conversions: they keep half subnormals, as f2h does
+  return (uint32_t)f2h<MPX_F16>(a) | ((uint32_t)f2h<MPX_F16>(b) << 16);
+}
+
+// probs_to_ds for staged operands whose rows >= T are 0: then dP is 0 for
+// keys >= T and for queries >= T, and so are the loaded probabilities, so
+// the sums and products need no masks (a masked term is an exact 0, and dS
+// there is a zero of either sign).  Conversions go two values at a time.
 template <int DT, int NB>
-__device__ __forceinline__ void bwd_dq(uint32_t kbase, const u32x2 (&Sr)[NB][4], uint16_t* dQrow, int q,
-                                       int T, int lane) {
+__device__ __forceinline__ void probs_to_ds_zero_padded(f32x16 (&dp)[NB], const u32x2 (&Pr)[NB][4],
+                                                        float scale, u32x2 (&Sr)[NB][4]) {
+  float rs = 0.0f;
+  static_for<NB>([&](auto j) {
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      float p[4], d[4];
+      unpack2<DT>(Pr[j][gq].x, p[0], p[1]);
+      unpack2<DT>(Pr[j][gq].y, p[2], p[3]);
+      unpack2<DT>(pack2<DT>(dp[j][4 * gq], dp[j][4 * gq + 1]), d[0], d[1]);
+      unpack2<DT>(pack2<DT>(dp[j][4 * gq + 2], dp[j][4 * gq + 3]), d[2], d[3]);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        dp[j][4 * gq + c] = d[c];
+        rs += d[c] * p[c];
+      }
+    }
+  });
+  rs += __shfl_xor(rs, 32);
+  static_for<NB>([&](auto j) {
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      float p[4], ds[4];
+      unpack2<DT>(Pr[j][gq].x, p[0], p[1]);
+      unpack2<DT>(Pr[j][gq].y, p[2], p[3]);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) ds[c] = (scale * p[c]) * (dp[j][4 * gq + c] - rs);
+      Sr[j][gq] = u32x2{pack2<DT>(ds[0], ds[1]), pack2<DT>(ds[2], ds[3])};
+    }
+  });
+}
+
+// Per query block (the wave's 32 queries q), V and dO read from global
+// memory: dP^T = V dO^T, the probabilities P of query q and dS.
+template <int DT, int NB>
+__device__ __forceinline__ void bwd_query_block(const uint16_t* V, int64_t ld, const uint16_t* G, int dm,
+                                                const uint16_t* Prow, int q, int T, float scale,
+                                                int lane, u32x2 (&Pr)[NB][4], u32x2 (&Sr)[NB][4]) {
   const int hi = lane >> 5;
-  f32x16 o[2];
+  const int qc = min(q, T - 1);
+  uint4 gf[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) gf[kk] = ld_u4(G + qc * dm + 16 * kk + 8 * hi);
+  f32x16 dp[NB];
+  static_for<NB>([&](auto j) {
+    const int key = min(32 * j + (lane & 31), T - 1);
+    f32x16 acc;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) acc = mfma32<DT>(ld_u4(V + key * ld + 16 * kk + 8 * hi), gf[kk], acc);
+    dp[j] = acc;
+  });
+  load_prob_rows<NB>(Prow, q, T, lane, Pr);
+  probs_to_ds<DT, NB>(dp, Pr, q, T, scale, lane, Sr);
+}
+
+// dQ^T = K^T dS^T for the wave's queries (K staged in LDS as [key][d]):
+// the float32 accumulators (lane = query, d in registers).
+template <int DT, int NB>
+__device__ __forceinline__ void bwd_dq_acc(uint32_t kbase, const u32x2 (&Sr)[NB][4], int lane, f32x16 (&o)[2]) {
 #pragma unroll
   for (int db = 0; db < 2; ++db)
 #pragma unroll
@@ -402,15 +501,28 @@ __device__ __forceinline__ void bwd_dq(uint32_t kbase, const u32x2 (&Sr)[NB][4],
 #pragma unroll
     for (int db = 0; db < 2; ++db) o[db] = mfma32<DT>(frag_tr(kbase, PD, 16 * ks, 32 * db, lane), bf, o[db]);
   });
-  if (q < T) {
+}
+
+// The lane's dQ row (its query's 64 d) rounded to half: runs of 4 d.
+template <int DT>
+__device__ __forceinline__ void put_dq_row(const f32x16 (&o)[2], uint16_t* row, int lane) {
+  const int hi = lane >> 5;
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
+  for (int db = 0; db < 2; ++db)
 #pragma unroll
-      for (int gq = 0; gq < 4; ++gq)
-        st_u2(dQrow + 32 * db + 8 * gq + 4 * hi,
-              pack4(f2h<DT>(o[db][4 * gq]), f2h<DT>(o[db][4 * gq + 1]), f2h<DT>(o[db][4 * gq + 2]),
-                    f2h<DT>(o[db][4 * gq + 3])));
-  }
+    for (int gq = 0; gq < 4; ++gq)
+      st_u2(row + 32 * db + 8 * gq + 4 * hi,
+            pack4(f2h<DT>(o[db][4 * gq]), f2h<DT>(o[db][4 * gq + 1]), f2h<DT>(o[db][4 * gq + 2]),
+                  f2h<DT>(o[db][4 * gq + 3])));
+}
+
+// dQ for the wave's queries, stored for queries < T.
+template <int DT, int NB>
+__device__ __forceinline__ void bwd_dq(uint32_t kbase, const u32x2 (&Sr)[NB][4], uint16_t* dQrow, int q,
+                                       int T, int lane) {
+  f32x16 o[2];
+  bwd_dq_acc<DT, NB>(kbase, Sr, lane, o);
+  if (q < T) put_dq_row<DT>(o, dQrow, lane);
 }
 
 // Store dK and dV rows of the wave's key block (accumulator runs of 4
@@ -509,120 +621,180 @@ __global__ __launch_bounds__(NB * 64) void attn_bwd_kernel(const uint16_t* __res
   store_kv_block<DT>(dk, dv, dQ + dm, dQ + 2 * dm, ld, 32 * w, T, lane);
 }
 
-// 128 < T <= 256, first kernel: per query block dS (kept in the workspace,
-// [B*H, T, ldP] like P) and dQ.
+// Output staging of one wave: a [32][OP] half block in LDS, written from
+// the accumulator layouts and copied out as whole 128-byte rows (16 bytes
+// per lane, 8 lanes per row), instead of 8-byte pieces of 32 rows per store.
+constexpr int OP = HD + 8;
+__device__ __forceinline__ void copy_rows_out(const uint16_t* stage, uint16_t* dst, int64_t ld, int nrows,
+                                              int lane) {
+  asm volatile("" ::: "memory");  // the wave's writes to stage come first
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = 8 * i + (lane >> 3), c = (lane & 7) * 8;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(stage + r * OP + c);
+    if (r < nrows) *reinterpret_cast<u32x4*>(dst + r * ld + c) = v;
+  }
+  asm volatile("" ::: "memory");  // ... and the reads finish before it is written again
+}
+
+// dK or dV of the wave's key block through the staging block.
+template <int DT>
+__device__ __forceinline__ void put_kv_block(const f32x16 (&acc)[2], uint16_t* stage, int lane) {
+  const int hi = lane >> 5, q4 = lane & 3;
+  const int col = 4 * ((lane & 31) >> 2);
+#pragma unroll
+  for (int db = 0; db < 2; ++db)
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      float a[4] = {acc[db][4 * gq], acc[db][4 * gq + 1], acc[db][4 * gq + 2], acc[db][4 * gq + 3]};
+      quad_transpose(a, q4);
+      st_u2(stage + (8 * gq + 4 * hi + q4) * OP + 32 * db + col,
+            pack4(f2h<DT>(a[0]), f2h<DT>(a[1]), f2h<DT>(a[2]), f2h<DT>(a[3])));
+    }
+}
+
+// 128 < T <= 256: the whole backward of one (batch, head) in one workgroup,
+// without a [T, T] array in LDS.  K, V, Q and dO are staged in four [TK][PD]
+// regions.  Pass 1 (wave w = query block w): dP^T = V dO^T from LDS, P rows
+// from global memory, dS, then dQ = dS K; the wave keeps its P and dS
+// blocks in registers.  Pass 2 (wave w = key block w): dK = dS^T Q and
+// dV = P^T dO reduced over the query blocks in order: in round r wave r's
+// P and dS blocks ([32 queries][TK keys]) are read from a slab in LDS, the
+// slabs alternating between the K and V regions (free after pass 1) so
+// that wave r + 1 writes the next one while round r is computed.  The
+// arithmetic, and its order, is that of the two-kernel form: the same dS,
+// dQ, dK and dV bits.
 template <int DT, int NB>
-__global__ __launch_bounds__(NB * 64) void attn_bwd_dq_kernel(const uint16_t* __restrict__ qkv,
-                                                              const uint16_t* __restrict__ P,
-                                                              const uint16_t* __restrict__ dO,
-                                                              uint16_t* __restrict__ dqkv,
-                                                              uint16_t* __restrict__ dS, int T, int H,
-                                                              int ldP, float scale) {
+__global__ __launch_bounds__(NB * 64) void attn_bwd_fused_kernel(const uint16_t* __restrict__ qkv,
+                                                                 const uint16_t* __restrict__ P,
+                                                                 const uint16_t* __restrict__ dO,
+                                                                 uint16_t* __restrict__ dqkv, int T, int H,
+                                                                 int ldP, float scale) {
   constexpr int TK = 32 * NB;
-  __shared__ __attribute__((aligned(16))) uint16_t sK[TK * PD];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  constexpr int PK = TK + 16;  // slab pitch (halves)
+  static_assert(2 * 32 * PK <= TK * PD, "a P slab and a dS slab fit in one staging region");
+  __shared__ __attribute__((aligned(16))) uint16_t sK[TK * PD];  // pass 2: slabs of even rounds
+  __shared__ __attribute__((aligned(16))) uint16_t sV[TK * PD];  // pass 2: slabs of odd rounds
+  __shared__ __attribute__((aligned(16))) uint16_t sQ[TK * PD];
+  __shared__ __attribute__((aligned(16))) uint16_t sdO[TK * PD];
+  // per-wave output staging where it fits next to the four regions
+  constexpr bool kStage = (4 * TK * PD + NB * 32 * OP) * 2 <= 160 * 1024;
+  __shared__ __attribute__((aligned(16))) uint16_t sOut[kStage ? NB * 32 * OP : 8];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, hi = lane >> 5;
   const int bh = blockIdx.x, b = bh / H, h = bh % H;
   const int dm = H * HD;
   const int64_t ld = 3 * (int64_t)dm;
   const uint16_t* Q = qkv + (int64_t)b * T * ld + h * HD;
   const uint16_t* G = dO + (int64_t)b * T * dm + h * HD;
-  {
-    RowStage<4> kst;
-    kst.load(Q + dm, ld, T, TK, tid, NB * 64);
-    kst.store(sK, TK, tid, NB * 64);
-  }
-
+  uint16_t* dQ = dqkv + (int64_t)b * T * ld + h * HD;
   const int q = 32 * w + (lane & 31);
-  const int64_t row = (int64_t)bh * T + min(q, T - 1);
+  uint16_t* stage = sOut + (kStage ? w * 32 * OP : 0);
+  const int nrows = min(32, T - 32 * w);  // rows of the wave's block below T (may be <= 0)
+
   u32x2 Pr[NB][4], Sr[NB][4];
-  bwd_query_block<DT, NB>(Q + 2 * dm, ld, G, dm, P + row * ldP, q, T, scale, lane, Pr, Sr);
-  if (q < T) {
+  {
+    // every load issued, out-of-range entries replaced by 0 afterwards
+    const uint16_t* Prow = P + ((int64_t)bh * T + min(q, T - 1)) * ldP;
     static_for<NB>([&](auto j) {
 #pragma unroll
       for (int gq = 0; gq < 4; ++gq) {
-        const int key0 = 32 * j + 8 * gq + 4 * (lane >> 5);
-        if (key0 < ldP) st_u2(dS + row * ldP + key0, Sr[j][gq]);
+        const int key0 = 32 * j + 8 * gq + 4 * hi;
+        Pr[j][gq] = ld_u2(Prow + min(key0, ldP - 4));
       }
     });
   }
-  __syncthreads();  // sK staged
-  bwd_dq<DT, NB>(lds_u32(sK), Sr, dqkv + (int64_t)b * T * ld + h * HD + q * ld, q, T, lane);
-}
+  {
+    RowStage<4> kst, vst, qst, gst;  // 32 NB rows each over 64 NB threads
+    kst.load_clamped(Q + dm, ld, T, tid, NB * 64);
+    vst.load_clamped(Q + 2 * dm, ld, T, tid, NB * 64);
+    gst.load_clamped(G, dm, T, tid, NB * 64);
+    qst.load_clamped(Q, ld, T, tid, NB * 64);
+    kst.store_clamped(sK, T, tid, NB * 64);
+    vst.store_clamped(sV, T, tid, NB * 64);
+    gst.store_clamped(sdO, T, tid, NB * 64);
+    qst.store_clamped(sQ, T, tid, NB * 64);
+  }
+  __syncthreads();
+  const uint32_t kbase = lds_u32(sK), vbase = lds_u32(sV), qbase = lds_u32(sQ), gbase = lds_u32(sdO);
 
-// 128 < T <= 256, second kernel: per key block (wave w) dK = dS^T Q and
-// dV = P^T dO, reduced over the queries in blocks of 32 staged through LDS.
-template <int DT, int NB>
-__global__ __launch_bounds__(NB * 64) void attn_bwd_dkv_kernel(const uint16_t* __restrict__ qkv,
-                                                               const uint16_t* __restrict__ P,
-                                                               const uint16_t* __restrict__ dO,
-                                                               const uint16_t* __restrict__ dS,
-                                                               uint16_t* __restrict__ dqkv, int T, int H,
-                                                               int ldP) {
-  constexpr int TK = 32 * NB;
-  constexpr int PK = TK + 16;
-  __shared__ __attribute__((aligned(16))) uint16_t sQ[32 * PD];
-  __shared__ __attribute__((aligned(16))) uint16_t sdO[32 * PD];
-  __shared__ __attribute__((aligned(16))) uint16_t sP[32 * PK];
-  __shared__ __attribute__((aligned(16))) uint16_t sdS[32 * PK];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int nthreads = NB * 64;
-  const int bh = blockIdx.x, b = bh / H, h = bh % H;
-  const int dm = H * HD;
-  const int64_t ld = 3 * (int64_t)dm;
-  const uint16_t* Q = qkv + (int64_t)b * T * ld + h * HD;
-  const uint16_t* G = dO + (int64_t)b * T * dm + h * HD;
-  const uint16_t* Pb = P + (int64_t)bh * T * ldP;
-  const uint16_t* Sb = dS + (int64_t)bh * T * ldP;
-  const uint32_t qbase = lds_u32(sQ), gbase = lds_u32(sdO), pbase = lds_u32(sP), sbase = lds_u32(sdS);
+  // pass 1: dP^T = V dO^T (rows >= T of the staged arrays are 0), dS, dQ
+  {
+    uint4 gf[4];
+    const uint32_t grow = gbase + (uint32_t)((q * PD + 8 * hi) * 2);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) gf[kk] = lds_b128(grow + 32 * kk);
+    f32x16 dp[NB];
+    static_for<NB>([&](auto j) {
+      const uint32_t vrow = vbase + (uint32_t)(((32 * j + (lane & 31)) * PD + 8 * hi) * 2);
+      f32x16 acc;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) acc = mfma32<DT>(lds_b128(vrow + 32 * kk), gf[kk], acc);
+      dp[j] = acc;
+    });
+    static_for<NB>([&](auto j) {
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        asm volatile("" : "+v"(Pr[j][gq]));  // keeps the load above unconditional
+        if (!(q < T && 32 * j + 8 * gq + 4 * hi < T)) Pr[j][gq] = u32x2{0u, 0u};
+      }
+    });
+    probs_to_ds_zero_padded<DT, NB>(dp, Pr, scale, Sr);
+  }
+  if constexpr (kStage) {
+    f32x16 o[2];
+    bwd_dq_acc<DT, NB>(kbase, Sr, lane, o);
+    put_dq_row<DT>(o, stage + (lane & 31) * OP, lane);
+    copy_rows_out(stage, dQ + 32 * w * ld, ld, nrows, lane);
+  } else {
+    bwd_dq<DT, NB>(kbase, Sr, dQ + q * ld, q, T, lane);
+  }
+  __syncthreads();  // the K and V regions are free
+
+  // pass 2
+  auto write_slab = [&](uint16_t* slab) {
+    const int ql = lane & 31;
+    static_for<NB>([&](auto j) {
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+        const int key0 = 32 * j + 8 * gq + 4 * hi;
+        *reinterpret_cast<u32x2*>(slab + ql * PK + key0) = Pr[j][gq];
+        *reinterpret_cast<u32x2*>(slab + 32 * PK + ql * PK + key0) = Sr[j][gq];
+      }
+    });
+  };
   f32x16 dk[2], dv[2];
 #pragma unroll
   for (int db = 0; db < 2; ++db)
 #pragma unroll
     for (int e = 0; e < 16; ++e) dk[db][e] = dv[db][e] = 0.0f;
-  for (int q0 = 0; q0 < T; q0 += 32) {
-    __syncthreads();  // the previous block's reads are done
-    static_assert(NB >= 4 && 32 * (TK / 8) == 2 * NB * 64, "staging shape of the dK / dV kernel");
-    // every load of the block in flight before any LDS write: 32 rows of Q
-    // and dO (one chunk per thread at most: 256 <= 64 NB), 32 x TK of P and
-    // dS (exactly two chunks per thread)
-    RowStage<1> qst, gst;
-    qst.load(Q + q0 * ld, ld, T - q0, 32, tid, nthreads);
-    gst.load(G + q0 * dm, dm, T - q0, 32, tid, nthreads);
-    u32x4 pv[2], sv[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + i * nthreads;
-      const int r = c / (TK / 8), col = (c % (TK / 8)) * 8;
-      pv[i] = u32x4{0u, 0u, 0u, 0u};
-      sv[i] = u32x4{0u, 0u, 0u, 0u};
-      if (q0 + r < T && col < ldP) {
-        pv[i] = *reinterpret_cast<const u32x4*>(Pb + (int64_t)(q0 + r) * ldP + col);
-        sv[i] = *reinterpret_cast<const u32x4*>(Sb + (int64_t)(q0 + r) * ldP + col);
-      }
-    }
-    qst.store(sQ, 32, tid, nthreads);
-    gst.store(sdO, 32, tid, nthreads);
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + i * nthreads;
-      const int r = c / (TK / 8), col = (c % (TK / 8)) * 8;
-      *reinterpret_cast<u32x4*>(sP + r * PK + col) = pv[i];
-      *reinterpret_cast<u32x4*>(sdS + r * PK + col) = sv[i];
-    }
-    __syncthreads();
+  if (w == 0) write_slab(sK);
+  __syncthreads();
+  for (int r = 0; r < NB; ++r) {
+    // wave r + 1 fills the other slab: its last readers finished round r - 1
+    if (w == r + 1) write_slab((r & 1) ? sK : sV);
+    const uint32_t pbase = (r & 1) ? vbase : kbase, sbase = pbase + 32 * PK * 2;
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       const uint4 sa = frag_tr(sbase, PK, 16 * ks, 32 * w, lane);
       const uint4 pa = frag_tr(pbase, PK, 16 * ks, 32 * w, lane);
 #pragma unroll
       for (int db = 0; db < 2; ++db) {
-        dk[db] = mfma32<DT>(sa, frag_tr(qbase, PD, 16 * ks, 32 * db, lane), dk[db]);
-        dv[db] = mfma32<DT>(pa, frag_tr(gbase, PD, 16 * ks, 32 * db, lane), dv[db]);
+        dk[db] = mfma32<DT>(sa, frag_tr(qbase, PD, 32 * r + 16 * ks, 32 * db, lane), dk[db]);
+        dv[db] = mfma32<DT>(pa, frag_tr(gbase, PD, 32 * r + 16 * ks, 32 * db, lane), dv[db]);
       }
     }
+    __syncthreads();
   }
-  uint16_t* dQ = dqkv + (int64_t)b * T * ld + h * HD;
-  store_kv_block<DT>(dk, dv, dQ + dm, dQ + 2 * dm, ld, 32 * w, T, lane);
+  if constexpr (kStage) {
+    put_kv_block<DT>(dk, stage, lane);
+    copy_rows_out(stage, dQ + dm + 32 * w * ld, ld, nrows, lane);
+    put_kv_block<DT>(dv, stage, lane);
+    copy_rows_out(stage, dQ + 2 * dm + 32 * w * ld, ld, nrows, lane);
+  } else {
+    store_kv_block<DT>(dk, dv, dQ + dm, dQ + 2 * dm, ld, 32 * w, T, lane);
+  }
 }
 
 template <int DT>
@@ -648,16 +820,12 @@ hipError_t launch_fwd(const uint16_t* qkv, uint16_t* O, uint16_t* P, int B, int 
 }
 
 template <int DT>
-hipError_t launch_bwd(const uint16_t* qkv, const uint16_t* P, const uint16_t* dO, uint16_t* dqkv,
-                      uint16_t* dS, int B, int T, int H, int ldP, float scale, hipStream_t s) {
+hipError_t launch_bwd(const uint16_t* qkv, const uint16_t* P, const uint16_t* dO, uint16_t* dqkv, int B,
+                      int T, int H, int ldP, float scale, hipStream_t s) {
   const dim3 grid((unsigned)(B * H));
   const int nb = (T + 31) / 32;
 #define MPX_B(NBv) attn_bwd_kernel<DT, NBv><<<grid, NBv * 64, 0, s>>>(qkv, P, dO, dqkv, T, H, ldP, scale)
-#define MPX_B2(NBv)                                                                              \
-  do {                                                                                           \
-    attn_bwd_dq_kernel<DT, NBv><<<grid, NBv * 64, 0, s>>>(qkv, P, dO, dqkv, dS, T, H, ldP, scale); \
-    attn_bwd_dkv_kernel<DT, NBv><<<grid, NBv * 64, 0, s>>>(qkv, P, dO, dS, dqkv, T, H, ldP);       \
-  } while (0)
+#define MPX_B2(NBv) attn_bwd_fused_kernel<DT, NBv><<<grid, NBv * 64, 0, s>>>(qkv, P, dO, dqkv, T, H, ldP, scale)
   switch (nb) {
     case 1: MPX_B(1); break;
     case 2: MPX_B(2); break;
@@ -705,10 +873,7 @@ extern "C" int mpx_attention_fwd(const void* qkv, void* O, void* P, int64_t B, i
   return MPX_OK;
 }
 
-extern "C" size_t mpx_attention_bwd_workspace(int64_t B, int64_t T, int64_t H, int64_t hd) {
-  if (B < 1 || T <= 128 || H < 1 || hd != 64 || T > 256) return 0;
-  return (size_t)(B * H * T * ((T + 7) / 8 * 8)) * 2;
-}
+extern "C" size_t mpx_attention_bwd_workspace(int64_t, int64_t, int64_t, int64_t) { return 0; }
 
 extern "C" int mpx_attention_bwd(const void* qkv, const void* P, const void* dO, void* dqkv, int64_t B,
                                  int64_t T, int64_t H, int64_t hd, mpx_dtype dt, void* workspace,
@@ -725,22 +890,16 @@ extern "C" int mpx_attention_bwd(const void* qkv, const void* P, const void* dO,
   MPX_REQUIRE(aligned16(qkv) && aligned16(dO) && aligned16(dqkv) &&
                   (reinterpret_cast<uintptr_t>(P) & 7u) == 0,
               "qkv, dO and dqkv must be 16-byte aligned, P 8-byte aligned");
-  const size_t need = mpx_attention_bwd_workspace(B, T, H, hd);
-  if (need && (!workspace || ws_bytes < need || !aligned16(workspace))) {
-    set_error("mpx_attention_bwd: a 16-byte aligned workspace of " + std::to_string(need) +
-              " bytes is required");
-    return MPX_ERR_WORKSPACE;
-  }
+  (void)workspace;  // no workspace is used
+  (void)ws_bytes;
   const int ldP = (int)((T + 7) / 8 * 8);
   const float scale = (float)(1.0 / std::sqrt((double)hd));
   hipStream_t s = (hipStream_t)stream;
   if (dt == MPX_F16)
     MPX_HIP(launch_bwd<MPX_F16>((const uint16_t*)qkv, (const uint16_t*)P, (const uint16_t*)dO,
-                                (uint16_t*)dqkv, (uint16_t*)workspace, (int)B, (int)T, (int)H, ldP, scale,
-                                s));
+                                (uint16_t*)dqkv, (int)B, (int)T, (int)H, ldP, scale, s));
   else
     MPX_HIP(launch_bwd<MPX_BF16>((const uint16_t*)qkv, (const uint16_t*)P, (const uint16_t*)dO,
-                                 (uint16_t*)dqkv, (uint16_t*)workspace, (int)B, (int)T, (int)H, ldP,
-                                 scale, s));
+                                 (uint16_t*)dqkv, (int)B, (int)T, (int)H, ldP, scale, s));
   return MPX_OK;
 }

@@ -41,6 +41,8 @@ def test_binding_loads_and_covers_the_header():
     # a pure host call: size queries need no device
     assert binding.mpx_linear_bwd_workspace(64, 512, 1024) > 0
     assert binding.mpx_layernorm_bwd_workspace(100, 384) > 0
+    # the attention backward keeps dS on chip at every supported length
+    assert all(binding.mpx_attention_bwd_workspace(64, T, 12, 64) == 0 for T in (65, 128, 129, 197, 256))
 
 
 @pytest.mark.skipif(not os.path.exists(LIB), reason="libmpx.so not built")
