@@ -253,7 +253,7 @@ int mpx_gemm_set_config(int32_t config);
  * multiple of 8: the probabilities, kept for the backward pass (columns
  * T..ldP-1 are written as 0).  Buffers are caller-owned device memory.
  * Implemented for hd == 64 and 1 <= T <= 256 (else MPX_ERR_UNSUPPORTED);
- * qkv and O 16-byte aligned, P 8-byte aligned (else MPX_ERR_INVALID). */
+ * qkv, O and P 16-byte aligned (else MPX_ERR_INVALID). */
 int mpx_attention_fwd(const void* qkv, void* O, void* P, int64_t B, int64_t T, int64_t H,
                       int64_t hd, mpx_dtype dt, void* stream);
 
@@ -261,8 +261,8 @@ int mpx_attention_fwd(const void* qkv, void* O, void* P, int64_t B, int64_t T, i
  *   dP = half(dO V^T);  dV = half(P^T dO);
  *   dS = half(scale P (dP - rowsum(dP P))) (float32 math, scale = 1/sqrt(hd));
  *   dQ = half(dS K);  dK = half(dS^T Q),
- * written into dqkv [B*T, 3*H*hd] in the layout of qkv.  Same limits and
- * alignment as the forward (dO and dqkv 16-byte aligned).  One kernel, dS
+ * written into dqkv [B*T, 3*H*hd] in the layout of qkv.  Same limits as the
+ * forward; qkv, dO and dqkv 16-byte aligned, P 8-byte aligned.  One kernel, dS
  * never leaves the chip: workspace and ws_bytes are accepted for
  * compatibility and ignored (workspace may be NULL), and
  * mpx_attention_bwd_workspace returns 0. */

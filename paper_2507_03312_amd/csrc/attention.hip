@@ -103,6 +103,23 @@ __device__ __forceinline__ u32x2 pack4(uint16_t a, uint16_t b, uint16_t c, uint1
   return u32x2{a | ((uint32_t)b << 16), c | ((uint32_t)d << 16)};
 }
 
+// A 32 x 32 accumulator block whose rows run along a stored row (lane =
+// column n, rows 8 gq + 4 hi + 0..3 in entries 4 gq + 0..3), rounded to
+// half and stored as that row's 32 consecutive elements: one exchange with
+// the lane 32 apart gives each lane 8 consecutive ones, so the row goes out
+// in two 16-byte stores per lane.  row must be 16-byte aligned.
+template <int DT>
+__device__ __forceinline__ void store_acc_row32(const f32x16& o, uint16_t* row, int hi) {
+#pragma unroll
+  for (int m = 0; m < 2; ++m) {
+    u32x2 x = pack4(f2h<DT>(o[8 * m]), f2h<DT>(o[8 * m + 1]), f2h<DT>(o[8 * m + 2]), f2h<DT>(o[8 * m + 3]));
+    u32x2 y = pack4(f2h<DT>(o[8 * m + 4]), f2h<DT>(o[8 * m + 5]), f2h<DT>(o[8 * m + 6]),
+                    f2h<DT>(o[8 * m + 7]));
+    half_swap(x, y);
+    *reinterpret_cast<u32x4*>(row + 16 * m + 8 * hi) = u32x4{x.x, x.y, y.x, y.y};
+  }
+}
+
 // B operand (n = query, 16 keys starting at 16 ks) from the packed
 // probabilities of the lane's query: R[j][gq] holds keys 32 j + 8 gq + 4 hi +
 // (0..3).  Half 0 needs keys 8 g' + 0..7 with g' = 2s, half 1 with g' = 2s+1;
@@ -188,8 +205,6 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_rows_kernel(const uint16_t* 
 #pragma unroll
       for (int c = 0; c < 4; ++c) p[c] = f2h<DT>(s[j][4 * gq + c] * inv);
       R[j][gq] = pack4(p[0], p[1], p[2], p[3]);
-      const int key0 = 32 * j + 8 * gq + 4 * hi;
-      if (q < T && key0 < ldP) st_u2(P + ((int64_t)bh * T + q) * ldP + key0, R[j][gq]);
     }
   });
 
@@ -202,20 +217,17 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_rows_kernel(const uint16_t* 
   for (int db = 0; db < 2; ++db)
 #pragma unroll
     for (int e = 0; e < 16; ++e) o[db][e] = 0.0f;
+  uint16_t* prow = P + ((int64_t)bh * T + q) * ldP;
   static_for<2 * NB>([&](auto ks) {
-    const uint4 bf = keys_operand<NB>(R, ks);
+    const uint4 bf = keys_operand<NB>(R, ks);  // keys 16 ks + 8 hi + 0..7
+    if (q < T && 16 * ks + 8 * hi < ldP) *reinterpret_cast<uint4*>(prow + 16 * ks + 8 * hi) = bf;
 #pragma unroll
     for (int db = 0; db < 2; ++db) o[db] = mfma32<DT>(frag_tr(vbase, PD, 16 * ks, 32 * db, lane), bf, o[db]);
   });
   if (q < T) {
     uint16_t* out = O + ((int64_t)b * T + q) * dm + h * HD;
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
-#pragma unroll
-      for (int gq = 0; gq < 4; ++gq)
-        st_u2(out + 32 * db + 8 * gq + 4 * hi,
-              pack4(f2h<DT>(o[db][4 * gq]), f2h<DT>(o[db][4 * gq + 1]), f2h<DT>(o[db][4 * gq + 2]),
-                    f2h<DT>(o[db][4 * gq + 3])));
+    for (int db = 0; db < 2; ++db) store_acc_row32<DT>(o[db], out + 32 * db, hi);
   }
 }
 
@@ -323,12 +335,12 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_kernel(const uint16_t* __res
         pv[c] = f2h<DT>(ex * inv);
       }
       R4[gq] = pack4(pv[0], pv[1], pv[2], pv[3]);
-      const int key0 = 32 * j + 8 * gq + 4 * hi;
-      if (q < T && key0 < ldP) st_u2(prow + key0, R4[gq]);
     }
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
-      const uint4 bf = block_keys_operand(R4, hh);
+      const uint4 bf = block_keys_operand(R4, hh);  // keys 32 j + 16 hh + 8 hi + 0..7
+      const int key0 = 32 * j + 16 * hh + 8 * hi;
+      if (q < T && key0 < ldP) *reinterpret_cast<uint4*>(prow + key0) = bf;
 #pragma unroll
       for (int db = 0; db < 2; ++db)
         o[db] = mfma32<DT>(frag_tr(vbase, PD, 32 * j + 16 * hh, 32 * db, lane), bf, o[db]);
@@ -337,12 +349,7 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_kernel(const uint16_t* __res
   if (q < T) {
     uint16_t* out = O + ((int64_t)b * T + q) * dm + h * HD;
 #pragma unroll
-    for (int db = 0; db < 2; ++db)
-#pragma unroll
-      for (int gq = 0; gq < 4; ++gq)
-        st_u2(out + 32 * db + 8 * gq + 4 * hi,
-              pack4(f2h<DT>(o[db][4 * gq]), f2h<DT>(o[db][4 * gq + 1]), f2h<DT>(o[db][4 * gq + 2]),
-                    f2h<DT>(o[db][4 * gq + 3])));
+    for (int db = 0; db < 2; ++db) store_acc_row32<DT>(o[db], out + 32 * db, hi);
   }
 }
 
@@ -506,14 +513,8 @@ __device__ __forceinline__ void bwd_dq_acc(uint32_t kbase, const u32x2 (&Sr)[NB]
 // The lane's dQ row (its query's 64 d) rounded to half: runs of 4 d.
 template <int DT>
 __device__ __forceinline__ void put_dq_row(const f32x16 (&o)[2], uint16_t* row, int lane) {
-  const int hi = lane >> 5;
 #pragma unroll
-  for (int db = 0; db < 2; ++db)
-#pragma unroll
-    for (int gq = 0; gq < 4; ++gq)
-      st_u2(row + 32 * db + 8 * gq + 4 * hi,
-            pack4(f2h<DT>(o[db][4 * gq]), f2h<DT>(o[db][4 * gq + 1]), f2h<DT>(o[db][4 * gq + 2]),
-                  f2h<DT>(o[db][4 * gq + 3])));
+  for (int db = 0; db < 2; ++db) store_acc_row32<DT>(o[db], row + 32 * db, lane >> 5);
 }
 
 // dQ for the wave's queries, stored for queries < T.
@@ -859,8 +860,7 @@ extern "C" int mpx_attention_fwd(const void* qkv, void* O, void* P, int64_t B, i
     set_error("mpx_attention_fwd: implemented for head dimension 64 and T <= 256");
     return MPX_ERR_UNSUPPORTED;
   }
-  MPX_REQUIRE(aligned16(qkv) && aligned16(O) && (reinterpret_cast<uintptr_t>(P) & 7u) == 0,
-              "qkv and O must be 16-byte aligned, P 8-byte aligned");
+  MPX_REQUIRE(aligned16(qkv) && aligned16(O) && aligned16(P), "qkv, O and P must be 16-byte aligned");
   const int ldP = (int)((T + 7) / 8 * 8);
   const float scale = (float)(1.0 / std::sqrt((double)hd));
   hipStream_t s = (hipStream_t)stream;
