@@ -103,6 +103,28 @@ __device__ __forceinline__ u32x2 pack4(uint16_t a, uint16_t b, uint16_t c, uint1
   return u32x2{a | ((uint32_t)b << 16), c | ((uint32_t)d << 16)};
 }
 
+// Two halves packed in a dword <-> float32 (exact widening; narrowing
+// rounds to nearest even, as f2h).
+typedef float f32x2v __attribute__((ext_vector_type(2)));
+template <int DT> __device__ __forceinline__ void unpack2(uint32_t v, float& a, float& b);
+template <> __device__ __forceinline__ void unpack2<MPX_BF16>(uint32_t v, float& a, float& b) {
+  a = __builtin_bit_cast(float, v << 16);
+  b = __builtin_bit_cast(float, v & 0xFFFF0000u);
+}
+template <> __device__ __forceinline__ void unpack2<MPX_F16>(uint32_t v, float& a, float& b) {
+  a = (float)__builtin_bit_cast(_Float16, (uint16_t)(v & 0xFFFFu));
+  b = (float)__builtin_bit_cast(_Float16, (uint16_t)(v >> 16));
+}
+template <int DT> __device__ __forceinline__ uint32_t pack2(float a, float b);
+template <> __device__ __forceinline__ uint32_t pack2<MPX_BF16>(float a, float b) {
+  typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2v){a, b}, bf16x2v));
+}
+template <> __device__ __forceinline__ uint32_t pack2<MPX_F16>(float a, float b) {
+  // two scalar conversions: they keep half subnormals, as f2h does
+  return (uint32_t)f2h<MPX_F16>(a) | ((uint32_t)f2h<MPX_F16>(b) << 16);
+}
+
 // A 32 x 32 accumulator block whose rows run along a stored row (lane =
 // column n, rows 8 gq + 4 hi + 0..3 in entries 4 gq + 0..3), rounded to
 // half and stored as that row's 32 consecutive elements: one exchange with
@@ -174,38 +196,46 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_rows_kernel(const uint16_t* 
   });
 
   // softmax over the keys of query q (float32; S rounded to half first)
+  // (blocks below nfull have no key past T: no masks there)
+  const int nfull = T / 32;
   float mx = -INFINITY;
   static_for<NB>([&](auto j) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int key = 32 * j + 8 * (e >> 2) + 4 * hi + (e & 3);
-      const float z = h2f<DT>(f2h<DT>(s[j][e])) * scale;
-      s[j][e] = key < T ? z : -INFINITY;
-      mx = fmaxf(mx, s[j][e]);
+    for (int e = 0; e < 16; e += 2) {
+      float a, c;
+      unpack2<DT>(pack2<DT>(s[j][e], s[j][e + 1]), a, c);
+      s[j][e] = a * scale;
+      s[j][e + 1] = c * scale;
     }
+    if (j >= nfull) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (32 * j + 8 * (e >> 2) + 4 * hi + (e & 3) >= T) s[j][e] = -INFINITY;
+    }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[j][e]);
   });
   mx = fmaxf(mx, __shfl_xor(mx, 32));
   float sum = 0.0f;
   static_for<NB>([&](auto j) {
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int key = 32 * j + 8 * (e >> 2) + 4 * hi + (e & 3);
-      const float ex = key < T ? __expf(s[j][e] - mx) : 0.0f;
-      s[j][e] = ex;
-      sum += ex;
+    for (int e = 0; e < 16; ++e) s[j][e] = __expf(s[j][e] - mx);
+    if (j >= nfull) {  // exact zeros past T, whatever mx is
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (32 * j + 8 * (e >> 2) + 4 * hi + (e & 3) >= T) s[j][e] = 0.0f;
     }
+#pragma unroll
+    for (int e = 0; e < 16; ++e) sum += s[j][e];
   });
   sum += __shfl_xor(sum, 32);
   const float inv = 1.0f / sum;
   u32x2 R[NB][4];
   static_for<NB>([&](auto j) {
 #pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      uint16_t p[4];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) p[c] = f2h<DT>(s[j][4 * gq + c] * inv);
-      R[j][gq] = pack4(p[0], p[1], p[2], p[3]);
-    }
+    for (int gq = 0; gq < 4; ++gq)
+      R[j][gq] = u32x2{pack2<DT>(s[j][4 * gq] * inv, s[j][4 * gq + 1] * inv),
+                       pack2<DT>(s[j][4 * gq + 2] * inv, s[j][4 * gq + 3] * inv)};
   });
 
   // O^T = V^T P^T: rows = d (two blocks of 32), columns = the wave's queries
@@ -272,13 +302,15 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_kernel(const uint16_t* __res
 #pragma unroll
   for (int kk = 0; kk < 4; ++kk) qf[kk] = ld_u4(Q + qc * ld + 16 * kk + 8 * hi);
   RowStage<4> kst, vst;  // K and V: 32 NB rows over 64 NB threads
-  kst.load(K, ld, T, TK, tid, NB * 64);
-  vst.load(V, ld, T, TK, tid, NB * 64);
-  kst.store(sK, TK, tid, NB * 64);
+  kst.load_clamped(K, ld, T, tid, NB * 64);
+  vst.load_clamped(V, ld, T, tid, NB * 64);
+  kst.store_clamped(sK, T, tid, NB * 64);
   __syncthreads();
   const uint32_t kbase = lds_u32(sK), vbase = lds_u32(sV);
 
-  // z = half(S) * scale for the lane's 16 keys of block j (-inf past T)
+  // z = half(S) * scale for the lane's 16 keys of block j (-inf past T;
+  // blocks below nfull have no key past T)
+  const int nfull = T / 32;
   auto scores = [&](int j, float (&z)[16]) {
     f32x16 acc;
 #pragma unroll
@@ -287,9 +319,15 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_kernel(const uint16_t* __res
 #pragma unroll
     for (int kk = 0; kk < 4; ++kk) acc = mfma32<DT>(lds_b128(row + 32 * kk), qf[kk], acc);
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int key = 32 * j + 8 * (e >> 2) + 4 * hi + (e & 3);
-      z[e] = key < T ? h2f<DT>(f2h<DT>(acc[e])) * scale : -INFINITY;
+    for (int e = 0; e < 16; e += 2) {
+      unpack2<DT>(pack2<DT>(acc[e], acc[e + 1]), z[e], z[e + 1]);
+      z[e] *= scale;
+      z[e + 1] *= scale;
+    }
+    if (j >= nfull) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (32 * j + 8 * (e >> 2) + 4 * hi + (e & 3) >= T) z[e] = -INFINITY;
     }
   };
 
@@ -309,7 +347,7 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_kernel(const uint16_t* __res
     l = (m == -INFINITY ? 0.0f : l * __expf(m - mn)) + t;
     m = mn;
   }
-  vst.store(sV, TK, tid, NB * 64);
+  vst.store_clamped(sV, T, tid, NB * 64);
   __syncthreads();
   const float M = fmaxf(m, __shfl_xor(m, 32));  // finite: key 0 is in every row
   const float lc = m == -INFINITY ? 0.0f : l * __expf(m - M);
@@ -326,16 +364,17 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_kernel(const uint16_t* __res
     float z[16];
     scores(j, z);
     u32x2 R4[4];
+    float ex[16];
 #pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      uint16_t pv[4];
+    for (int e = 0; e < 16; ++e) ex[e] = __expf(z[e] - M) * inv;
+    if (j >= nfull) {  // exact zeros past T, whatever M is
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const float ex = z[4 * gq + c] == -INFINITY ? 0.0f : __expf(z[4 * gq + c] - M);
-        pv[c] = f2h<DT>(ex * inv);
-      }
-      R4[gq] = pack4(pv[0], pv[1], pv[2], pv[3]);
+      for (int e = 0; e < 16; ++e)
+        if (32 * j + 8 * (e >> 2) + 4 * hi + (e & 3) >= T) ex[e] = 0.0f;
     }
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq)
+      R4[gq] = u32x2{pack2<DT>(ex[4 * gq], ex[4 * gq + 1]), pack2<DT>(ex[4 * gq + 2], ex[4 * gq + 3])};
 #pragma unroll
     for (int hh = 0; hh < 2; ++hh) {
       const uint4 bf = block_keys_operand(R4, hh);  // keys 32 j + 16 hh + 8 hi + 0..7
@@ -409,28 +448,6 @@ __device__ __forceinline__ void probs_to_ds(f32x16 (&dp)[NB], const u32x2 (&Pr)[
       Sr[j][gq] = pack4(ds[0], ds[1], ds[2], ds[3]);
     }
   });
-}
-
-// Two halves packed in a dword <-> float32 (exact widening; narrowing
-// rounds to nearest even, as f2h).
-typedef float f32x2v __attribute__((ext_vector_type(2)));
-template <int DT> __device__ __forceinline__ void unpack2(uint32_t v, float& a, float& b);
-template <> __device__ __forceinline__ void unpack2<MPX_BF16>(uint32_t v, float& a, float& b) {
-  a = __builtin_bit_cast(float, v << 16);
-  b = __builtin_bit_cast(float, v & 0xFFFF0000u);
-}
-template <> __device__ __forceinline__ void unpack2<MPX_F16>(uint32_t v, float& a, float& b) {
-  a = (float)__builtin_bit_cast(_Float16, (uint16_t)(v & 0xFFFFu));
-  b = (float)__builtin_bit_cast(_Float16, (uint16_t)(v >> 16));
-}
-template <int DT> __device__ __forceinline__ uint32_t pack2(float a, float b);
-template <> __device__ __forceinline__ uint32_t pack2<MPX_BF16>(float a, float b) {
-  typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
-  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2v){a, b}, bf16x2v));
-}
-template <> __device__ __forceinline__ uint32_t pack2<MPX_F16>(float a, float b) {
-  // two scalar conversions: they keep half subnormals, as f2h does
-  return (uint32_t)f2h<MPX_F16>(a) | ((uint32_t)f2h<MPX_F16>(b) << 16);
 }
 
 // probs_to_ds for staged operands whose rows >= T are 0: then dP is 0 for
