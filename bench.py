@@ -56,28 +56,28 @@ DEFAULT_CONFIG = "vit_b"
 # they no longer match, the figure is stale and reported as null.
 TRAFFIC = {
     "vit_block/blk0.up.fwd": {
-        "fetch_kib": 13932.2, "write_kib": 49920.0,
-        "fetch_factor": 262144.0 / 131089.0, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 13926.8, "write_kib": 49920.0,
+        "fetch_factor": 262144.0 / 131088.9, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/gemm_kernels.h": "b366ba284d399186b2b6f06b2b68e0b01c0fa9e1426ce688bbe91db7f0e42c3f",
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "e3478098a5cf87c150bb9a4360abcada1cb1559e508675526f6d67d4f8912c68",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
             "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
     },
     "vit_s/blk0.up.fwd": {
-        "fetch_kib": 25552.8, "write_kib": 99840.0,
-        "fetch_factor": 262144.0 / 131094.2, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 24015.3, "write_kib": 99840.0,
+        "fetch_factor": 262144.0 / 131089.0, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/gemm_kernels.h": "b366ba284d399186b2b6f06b2b68e0b01c0fa9e1426ce688bbe91db7f0e42c3f",
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "e3478098a5cf87c150bb9a4360abcada1cb1559e508675526f6d67d4f8912c68",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
             "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
     },
     "vit_b/blk0.up.fwd": {
-        "fetch_kib": 70847.6, "write_kib": 151310.6,
-        "fetch_factor": 262144.0 / 131091.0, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 70843.0, "write_kib": 151323.6,
+        "fetch_factor": 262144.0 / 131093.8, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/gemm_kernels.h": "b366ba284d399186b2b6f06b2b68e0b01c0fa9e1426ce688bbe91db7f0e42c3f",
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "e3478098a5cf87c150bb9a4360abcada1cb1559e508675526f6d67d4f8912c68",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
             "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
@@ -97,7 +97,6 @@ def traffic_bytes(name):
     """HBM bytes of one launch of a workload's dominant kernel ("workload/site"),
     from the stored counter readings, or None when none were taken for that
     workload or a source they depend on has changed since."""
-    """Measured HBM bytes per launch of kernel site `name`, or None."""
     import hashlib
     t = TRAFFIC.get(name)
     if not t:
