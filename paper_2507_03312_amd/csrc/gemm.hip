@@ -28,18 +28,19 @@ static GemmArgs base_args() {
 
 // split-K plan for a reduction of length K over an MxN output (the weight
 // gradients, whose outputs have far fewer 128 x 128 tiles than the chip has
-// workgroup slots): as many splits as fit in ONE round of the 512 slots of
-// the 128 x 128 kernel (2 per CU), at most 16 and at least 1024 reduction
-// values each.  One more split that spills into a second round costs a
-// whole round: measured on the ViT-B weight gradients, 144 tiles x 4 splits
-// (576 workgroups) took 84-88 us, 144 x 3 (432) 66-71 us.  Against the
-// earlier rule (at most 8, at least 512 values) this one gave the ViT-S
-// step +1.2% (16 splits of 1040 rows where there were 8) and left the
-// one-block and ViT-B steps unchanged; 16 splits of 520 rows had cost the
-// one-block step 0.7%.
+// workgroup slots): enough splits for one workgroup per CU (256 tiles x
+// splits, rounded up), at most 16 and at least 1024 reduction values each.
+// The weight gradients run on a second stream beside the critical path, so
+// filling the 512 slots of two workgroups per CU (the earlier rule) bought
+// latency no one waited for with more float32 partials to write and reduce:
+// this rule measured ViT-B +1.2% and ViT-S +2.0% on one box and leaves the
+// one-block model's splits as they were (the 1024-value floor binds there);
+// 192 slots: ViT-S -1.5%; at least 2048 values per split: ViT-S -2.3%, one
+// block -3%; rounding 256 / tiles down left the ViT-B MLP gradients unsplit:
+// -7%.
 static int choose_splits(int64_t M, int64_t N, int64_t K) {
   const int64_t tiles = ((M + 127) / 128) * ((N + 127) / 128);
-  int64_t s = 512 / tiles;
+  int64_t s = (256 + tiles - 1) / tiles;
   s = std::min<int64_t>(s, 16);
   s = std::min<int64_t>(s, std::max<int64_t>(1, K / 1024));
   return (int)std::max<int64_t>(s, 1);
