@@ -566,6 +566,52 @@ __device__ __forceinline__ void store_kv_block(const f32x16 (&dk)[2], const f32x
     }
 }
 
+// bwd_query_block without branches and with exact zeros past T: V rows of
+// keys >= T and the dO row and probabilities of a query >= T are loaded from
+// clamped addresses and masked to 0, so dP is 0 there and dS needs no masks
+// (probs_to_ds_zero_padded).  The masks are ANDs, not selects: a select lets
+// the compiler turn the load into a branch around it.
+template <int DT, int NB>
+__device__ __forceinline__ void bwd_query_block_zp(const uint16_t* V, int64_t ld, const uint16_t* G, int dm,
+                                                   const uint16_t* Pbh, int ldP, int q, int T, float scale,
+                                                   int lane, u32x2 (&Pr)[NB][4], u32x2 (&Sr)[NB][4]) {
+  const int hi = lane >> 5;
+  const int qc = min(q, T - 1);
+  const uint32_t qmask = q < T ? 0xFFFFFFFFu : 0u;
+  const uint16_t* Prow = Pbh + (int64_t)qc * ldP;
+  static_for<NB>([&](auto j) {
+#pragma unroll
+    for (int gq = 0; gq < 4; ++gq) {
+      const int key0 = 32 * j + 8 * gq + 4 * hi;
+      const uint32_t m = key0 < T ? qmask : 0u;
+      const u32x2 v = ld_u2(Prow + min(key0, ldP - 4));
+      Pr[j][gq] = u32x2{v.x & m, v.y & m};
+    }
+  });
+  uint4 gf[4];
+#pragma unroll
+  for (int kk = 0; kk < 4; ++kk) {
+    const uint4 v = ld_u4(G + qc * dm + 16 * kk + 8 * hi);
+    gf[kk] = make_uint4(v.x & qmask, v.y & qmask, v.z & qmask, v.w & qmask);
+  }
+  f32x16 dp[NB];
+  static_for<NB>([&](auto j) {
+    const int key = 32 * j + (lane & 31);
+    const uint32_t km = key < T ? 0xFFFFFFFFu : 0u;
+    const uint16_t* vrow = V + min(key, T - 1) * ld + 8 * hi;
+    f32x16 acc;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const uint4 v = ld_u4(vrow + 16 * kk);
+      acc = mfma32<DT>(make_uint4(v.x & km, v.y & km, v.z & km, v.w & km), gf[kk], acc);
+    }
+    dp[j] = acc;
+  });
+  probs_to_ds_zero_padded<DT, NB>(dp, Pr, scale, Sr);
+}
+
 // T <= 128: the whole backward of one (batch, head) in one workgroup.
 template <int DT, int NB>
 __global__ __launch_bounds__(NB * 64) void attn_bwd_kernel(const uint16_t* __restrict__ qkv,
@@ -595,18 +641,17 @@ __global__ __launch_bounds__(NB * 64) void attn_bwd_kernel(const uint16_t* __res
 
   {
     RowStage<4> kst, qst, gst;  // 32 NB rows each over 64 NB threads
-    kst.load(K, ld, T, TK, tid, NB * 64);
-    qst.load(Q, ld, T, TK, tid, NB * 64);
-    gst.load(G, dm, T, TK, tid, NB * 64);
-    kst.store(sK, TK, tid, NB * 64);
-    qst.store(sQ, TK, tid, NB * 64);
-    gst.store(sdO, TK, tid, NB * 64);
+    kst.load_clamped(K, ld, T, tid, NB * 64);
+    qst.load_clamped(Q, ld, T, tid, NB * 64);
+    gst.load_clamped(G, dm, T, tid, NB * 64);
+    kst.store_clamped(sK, T, tid, NB * 64);
+    qst.store_clamped(sQ, T, tid, NB * 64);
+    gst.store_clamped(sdO, T, tid, NB * 64);
   }
 
   const int q = 32 * w + (lane & 31);
   u32x2 Pr[NB][4], Sr[NB][4];
-  bwd_query_block<DT, NB>(V, ld, G, dm, P + ((int64_t)bh * T + min(q, T - 1)) * ldP, q, T, scale, lane,
-                          Pr, Sr);
+  bwd_query_block_zp<DT, NB>(V, ld, G, dm, P + (int64_t)bh * T * ldP, ldP, q, T, scale, lane, Pr, Sr);
   // the [query][key] copies for the dK / dV products (rows >= T are 0)
   static_for<NB>([&](auto j) {
 #pragma unroll
