@@ -53,25 +53,15 @@ __device__ __forceinline__ uint4 frag_tr(uint32_t base, int pitch, int k0, int m
   return make_uint4(lo.x, lo.y, hi.x, hi.y);
 }
 
-// Rows [0, rows) of a [T, 64] head slice (row stride ld) staged into LDS
-// [rows][PD] in two steps, PER 16-byte chunks per thread: load() puts every
-// global load of the thread in flight, store() writes them (rows >= T are
-// zero).  A loop that stores each chunk before loading the next waits one
-// memory latency per chunk.  Requires rows * 8 <= PER * nthreads.
+// The rows of a [T, 64] head slice (row stride ld) staged into LDS
+// [PER * nthreads / 8][PD] in two steps, PER 16-byte chunks per thread:
+// load() puts every global load of the thread in flight, store() writes
+// them.  No branches: rows past T load row T - 1 and are written as zeros.
+// A loop that stores each chunk before loading the next waits one memory
+// latency per chunk.
 template <int PER>
 struct RowStage {
   u32x4 v[PER];
-  __device__ __forceinline__ void load(const uint16_t* src, int64_t ld, int T, int rows, int tid,
-                                       int nthreads) {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = tid + i * nthreads;
-      v[i] = u32x4{0u, 0u, 0u, 0u};
-      if (c < rows * 8 && (c >> 3) < T) v[i] = *reinterpret_cast<const u32x4*>(src + (c >> 3) * ld + (c & 7) * 8);
-    }
-  }
-  // The same without branches, for rows * 8 == PER * nthreads: rows >= T
-  // load row T - 1 and are replaced by 0 in store_clamped().
   __device__ __forceinline__ void load_clamped(const uint16_t* src, int64_t ld, int T, int tid,
                                                int nthreads) {
 #pragma unroll
@@ -87,13 +77,6 @@ struct RowStage {
       asm volatile("" : "+v"(v[i]));  // keeps the load unconditional
       if ((c >> 3) >= T) v[i] = u32x4{0u, 0u, 0u, 0u};
       *reinterpret_cast<u32x4*>(lds + (c >> 3) * PD + (c & 7) * 8) = v[i];
-    }
-  }
-  __device__ __forceinline__ void store(uint16_t* lds, int rows, int tid, int nthreads) const {
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = tid + i * nthreads;
-      if (c < rows * 8) *reinterpret_cast<u32x4*>(lds + (c >> 3) * PD + (c & 7) * 8) = v[i];
     }
   }
 };
@@ -176,7 +159,7 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_rows_kernel(const uint16_t* 
   const uint16_t* V = Q + 2 * dm;
 
   RowStage<4> vst;  // V: 32 NB rows over 64 NB threads
-  vst.load(V, ld, T, TK, tid, NB * 64);
+  vst.load_clamped(V, ld, T, tid, NB * 64);
 
   // S^T blocks: rows = keys of block j, columns = the wave's 32 queries
   const int q = 32 * w + (lane & 31);
@@ -239,7 +222,7 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_rows_kernel(const uint16_t* 
   });
 
   // O^T = V^T P^T: rows = d (two blocks of 32), columns = the wave's queries
-  vst.store(sV, TK, tid, NB * 64);
+  vst.store_clamped(sV, T, tid, NB * 64);
   __syncthreads();
   const uint32_t vbase = lds_u32(sV);
   f32x16 o[2];
@@ -394,66 +377,15 @@ __global__ __launch_bounds__(NB * 64) void attn_fwd_kernel(const uint16_t* __res
 
 // ---------------------------------------------------------------- backward --
 
-// The probabilities of query q in the layout of an S^T accumulator (entry
-// [j][gq] holds keys 32 j + 8 gq + 4 hi + (0..3)); 0 past T and for q >= T.
-template <int NB>
-__device__ __forceinline__ void load_prob_rows(const uint16_t* Prow, int q, int T, int lane,
-                                               u32x2 (&Pr)[NB][4]) {
-  const int hi = lane >> 5;
-  static_for<NB>([&](auto j) {
-#pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      const int key0 = 32 * j + 8 * gq + 4 * hi;
-      Pr[j][gq] = (q < T && key0 < T) ? ld_u2(Prow + key0) : u32x2{0u, 0u};
-    }
-  });
-}
-
 // From the float32 accumulators dp (dP^T of the wave's queries, one block of
-// 32 keys each) and the probabilities Pr of query q: dP rounded to half, the
-// row sum rs = sum_k dP P over keys < T, and dS = half(scale P (dP - rs))
-// packed like Pr (0 for keys >= T and for queries >= T).
-template <int DT, int NB>
-__device__ __forceinline__ void probs_to_ds(f32x16 (&dp)[NB], const u32x2 (&Pr)[NB][4], int q, int T,
-                                            float scale, int lane, u32x2 (&Sr)[NB][4]) {
-  const int hi = lane >> 5;
-  float rs = 0.0f;
-  static_for<NB>([&](auto j) {
-#pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      const int key0 = 32 * j + 8 * gq + 4 * hi;
-      const uint16_t ph[4] = {(uint16_t)(Pr[j][gq].x & 0xFFFFu), (uint16_t)(Pr[j][gq].x >> 16),
-                              (uint16_t)(Pr[j][gq].y & 0xFFFFu), (uint16_t)(Pr[j][gq].y >> 16)};
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const float d = h2f<DT>(f2h<DT>(dp[j][4 * gq + c]));
-        dp[j][4 * gq + c] = d;
-        if (key0 + c < T) rs += d * h2f<DT>(ph[c]);
-      }
-    }
-  });
-  rs += __shfl_xor(rs, 32);
-  static_for<NB>([&](auto j) {
-#pragma unroll
-    for (int gq = 0; gq < 4; ++gq) {
-      const int key0 = 32 * j + 8 * gq + 4 * hi;
-      const uint16_t ph[4] = {(uint16_t)(Pr[j][gq].x & 0xFFFFu), (uint16_t)(Pr[j][gq].x >> 16),
-                              (uint16_t)(Pr[j][gq].y & 0xFFFFu), (uint16_t)(Pr[j][gq].y >> 16)};
-      uint16_t ds[4];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const bool ok = q < T && key0 + c < T;
-        ds[c] = ok ? f2h<DT>((scale * h2f<DT>(ph[c])) * (dp[j][4 * gq + c] - rs)) : (uint16_t)0;
-      }
-      Sr[j][gq] = pack4(ds[0], ds[1], ds[2], ds[3]);
-    }
-  });
-}
-
-// probs_to_ds for staged operands whose rows >= T are 0: then dP is 0 for
-// keys >= T and for queries >= T, and so are the loaded probabilities, so
-// the sums and products need no masks (a masked term is an exact 0, and dS
-// there is a zero of either sign).  Conversions go two values at a time.
+// 32 keys each; lane = query, entry [j][gq] holding keys 32 j + 8 gq + 4 hi
+// + (0..3)) and the probabilities Pr of the lane's query in the same
+// layout: dP rounded to half, the row sum rs = sum_k dP P, and
+// dS = half(scale P (dP - rs)) packed like Pr.  The operands' rows past T
+// are zero where these come from, so dP is 0 for keys >= T and for queries
+// >= T and so are the probabilities: the sums and products need no masks (a
+// masked term is an exact 0, and dS there is a zero of either sign).
+// Conversions go two values at a time.
 template <int DT, int NB>
 __device__ __forceinline__ void probs_to_ds_zero_padded(f32x16 (&dp)[NB], const u32x2 (&Pr)[NB][4],
                                                         float scale, u32x2 (&Sr)[NB][4]) {
@@ -485,31 +417,6 @@ __device__ __forceinline__ void probs_to_ds_zero_padded(f32x16 (&dp)[NB], const 
       Sr[j][gq] = u32x2{pack2<DT>(ds[0], ds[1]), pack2<DT>(ds[2], ds[3])};
     }
   });
-}
-
-// Per query block (the wave's 32 queries q), V and dO read from global
-// memory: dP^T = V dO^T, the probabilities P of query q and dS.
-template <int DT, int NB>
-__device__ __forceinline__ void bwd_query_block(const uint16_t* V, int64_t ld, const uint16_t* G, int dm,
-                                                const uint16_t* Prow, int q, int T, float scale,
-                                                int lane, u32x2 (&Pr)[NB][4], u32x2 (&Sr)[NB][4]) {
-  const int hi = lane >> 5;
-  const int qc = min(q, T - 1);
-  uint4 gf[4];
-#pragma unroll
-  for (int kk = 0; kk < 4; ++kk) gf[kk] = ld_u4(G + qc * dm + 16 * kk + 8 * hi);
-  f32x16 dp[NB];
-  static_for<NB>([&](auto j) {
-    const int key = min(32 * j + (lane & 31), T - 1);
-    f32x16 acc;
-#pragma unroll
-    for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
-#pragma unroll
-    for (int kk = 0; kk < 4; ++kk) acc = mfma32<DT>(ld_u4(V + key * ld + 16 * kk + 8 * hi), gf[kk], acc);
-    dp[j] = acc;
-  });
-  load_prob_rows<NB>(Prow, q, T, lane, Pr);
-  probs_to_ds<DT, NB>(dp, Pr, q, T, scale, lane, Sr);
 }
 
 // dQ^T = K^T dS^T for the wave's queries (K staged in LDS as [key][d]):
@@ -566,9 +473,11 @@ __device__ __forceinline__ void store_kv_block(const f32x16 (&dk)[2], const f32x
     }
 }
 
-// bwd_query_block without branches and with exact zeros past T: V rows of
-// keys >= T and the dO row and probabilities of a query >= T are loaded from
-// clamped addresses and masked to 0, so dP is 0 there and dS needs no masks
+// Per query block (the wave's 32 queries q), V and dO read from global
+// memory: dP^T = V dO^T, the probabilities P of query q and dS, without
+// branches and with exact zeros past T: V rows of keys >= T and the dO row
+// and probabilities of a query >= T are loaded from clamped addresses and
+// masked to 0, so dP is 0 there and dS needs no masks
 // (probs_to_ds_zero_padded).  The masks are ANDs, not selects: a select lets
 // the compiler turn the load into a branch around it.
 template <int DT, int NB>
