@@ -261,10 +261,12 @@ enum : int { EPI_BIAS = 1, EPI_GELU = 2, EPI_DACT = 4, EPI_RESID = 8, EPI_COUNT 
 // layout: lane = 8 consecutive columns of one row): the pre-activation store,
 // GELU, GELU' of the previous layer and the residual add with 16-byte
 // accesses, each store writing 8 rows x 128 contiguous bytes.
+// pf (nullable): the wave's GELU' or residual operand rows, already loaded
+// in the row layout (16 bytes of row (lane >> 3) + 8 t per entry t).
 template <int DT, int TM, int TN, int E>
 __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, const f32x16 (&acc)[TM][TN],
                                                   int64_t mw, int64_t nw, int lane, int64_t offC,
-                                                  uint16_t* lds) {
+                                                  uint16_t* lds, const u32x4* pf = nullptr) {
   static_assert((TM == 1 || TM == 2) && TN == 2, "32 x 64 or 64 x 64 wave tiles");
   constexpr int PITCH = 68;  // halves (34 banks): a column of 32 rows spreads over all banks
   const int hi = lane >> 5, r32 = lane & 31;
@@ -323,13 +325,13 @@ __device__ __forceinline__ void gemm_epilogue_lds(const GemmArgs& g, const f32x1
     }
     if constexpr ((E & EPI_DACT) != 0) {
       uint16_t da[8];
-      h8(*reinterpret_cast<const u32x4*>(dact + off), da);
+      h8(pf ? pf[t] : *reinterpret_cast<const u32x4*>(dact + off), da);
 #pragma unroll
       for (int c = 0; c < 8; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) * gelu_tanh_grad(h2f<DT>(da[c])));
     }
     if constexpr ((E & EPI_RESID) != 0) {
       uint16_t rv[8];
-      h8(*reinterpret_cast<const u32x4*>(res + (uint32_t)(row * g.ldr + c8)), rv);
+      h8(pf ? pf[t] : *reinterpret_cast<const u32x4*>(res + (uint32_t)(row * g.ldr + c8)), rv);
 #pragma unroll
       for (int c = 0; c < 8; ++c) h[c] = f2h<DT>(h2f<DT>(h[c]) + h2f<DT>(rv[c]));
     }
@@ -772,6 +774,22 @@ void gemm_dma_kernel(GemmArgs g) {
 #pragma unroll
   for (int i = 0; i < TM; ++i) dbs[i] = 0.0f;
 
+  // A whole tile's GELU' or residual operand is loaded into registers before
+  // the first copies (the oldest loads, so the first tile's wait covers
+  // them): the epilogue then starts without a memory round trip.
+  constexpr bool kPF = E != EPI_GENERIC && (E & (EPI_DACT | EPI_RESID)) != 0;
+  const bool whole = E != EPI_GENERIC && g.full_epi && m0 + BM <= g.M && n0 + BN <= g.N;
+  u32x4 pf[kPF ? 4 * TM : 1];
+  if constexpr (kPF) {
+    if (whole) {
+      const int64_t ldp = (E & EPI_DACT) ? g.ldc : g.ldr;
+      const uint16_t* src = ((E & EPI_DACT) ? g.dact : g.resid) + ((m0 + wm0) * ldp + n0 + wn0);
+#pragma unroll
+      for (int t = 0; t < 4 * TM; ++t)
+        pf[t] = *reinterpret_cast<const u32x4*>(src + (uint32_t)(((lane >> 3) + 8 * t) * ldp + 8 * (lane & 7)));
+    }
+  }
+
   auto issue = [&](int kt) {
     const uint32_t st = lds0 + (uint32_t)((kt % S) * STAGE);
     da.issue(reinterpret_cast<const uint16_t*>(reinterpret_cast<const uint8_t*>(Ab) + kt * da.step), st, wave);
@@ -850,10 +868,11 @@ void gemm_dma_kernel(GemmArgs g) {
   }
   // the accumulators hold C^T blocks (the MFMA operands are swapped above)
   if constexpr (E != EPI_GENERIC) {
-    if (g.full_epi && m0 + BM <= g.M && n0 + BN <= g.N) {  // uniform over the workgroup
+    if (whole) {  // uniform over the workgroup
       __syncthreads();  // every wave is done reading the stage buffers
       gemm_epilogue_lds<DT, TM, TN, E>(g, acc, m0 + wm0, n0 + wn0, lane, offC,
-                                       reinterpret_cast<uint16_t*>(smem) + wave * (WM * 68));
+                                       reinterpret_cast<uint16_t*>(smem) + wave * (WM * 68),
+                                       kPF ? pf : nullptr);
       return;
     }
   }
