@@ -56,28 +56,28 @@ DEFAULT_CONFIG = "vit_b"
 # they no longer match, the figure is stale and reported as null.
 TRAFFIC = {
     "vit_block/blk0.up.fwd": {
-        "fetch_kib": 13926.8, "write_kib": 49920.0,
+        "fetch_kib": 13948.5, "write_kib": 49920.0,
         "fetch_factor": 262144.0 / 131088.9, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/gemm_kernels.h": "e3478098a5cf87c150bb9a4360abcada1cb1559e508675526f6d67d4f8912c68",
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "dd6947be2a489bb2aab4eab10bf49f1c70469f16a898583dc92638554d426731",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
             "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
     },
     "vit_s/blk0.up.fwd": {
-        "fetch_kib": 24015.3, "write_kib": 99840.0,
-        "fetch_factor": 262144.0 / 131089.0, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 23835.0, "write_kib": 99840.0,
+        "fetch_factor": 262144.0 / 131088.3, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/gemm_kernels.h": "e3478098a5cf87c150bb9a4360abcada1cb1559e508675526f6d67d4f8912c68",
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "dd6947be2a489bb2aab4eab10bf49f1c70469f16a898583dc92638554d426731",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
             "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
     },
     "vit_b/blk0.up.fwd": {
-        "fetch_kib": 70843.0, "write_kib": 151323.6,
-        "fetch_factor": 262144.0 / 131093.8, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 70864.7, "write_kib": 151323.2,
+        "fetch_factor": 262144.0 / 131094.1, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/gemm_kernels.h": "e3478098a5cf87c150bb9a4360abcada1cb1559e508675526f6d67d4f8912c68",
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "dd6947be2a489bb2aab4eab10bf49f1c70469f16a898583dc92638554d426731",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
             "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
