@@ -27,8 +27,11 @@ if HAVE_GPU:
     from paper_2507_03312_amd import binding as mx
 
 HD = 64
+# (B, H, T): every key-block count NB = ceil(T / 32) from 1 to 8 with ragged
+# and full last blocks, both sides of the 128-token switch of the backward
 SHAPES = [(2, 2, 1), (2, 3, 5), (1, 2, 32), (2, 2, 33), (2, 3, 65), (1, 2, 97), (1, 2, 128),
-          (1, 2, 129), (2, 2, 197), (1, 1, 200), (1, 2, 256)]
+          (1, 2, 129), (1, 2, 160), (1, 2, 161), (1, 1, 192), (2, 2, 197), (1, 1, 200),
+          (1, 2, 224), (1, 1, 225), (1, 2, 256)]
 
 
 def _s():
