@@ -406,7 +406,9 @@ class ViTStep(TrainStep):
         ws = max(mx.mpx_layernorm_bwd_workspace(M, d), mx.mpx_loss_workspace(B),
                  mx.mpx_attention_bwd_workspace(B, T, H, cfg.head_dim),
                  mx.mpx_classifier_head_workspace(B, d),
-                 0 if cfg.image else mx.mpx_linear_bwd_workspace(M, 3 * d, d))  # last QKV bias
+                 # the last QKV bias (tokens) or the patch embedding's gradients (images)
+                 mx.mpx_linear_bwd_workspace(B * cfg.n_patches, d, cfg.patch_dim) if cfg.image
+                 else mx.mpx_linear_bwd_workspace(M, 3 * d, d))
         self.ws = torch.zeros(ws, dtype=torch.uint8, device=dev)
         ws2 = max(max(mx.mpx_linear_bwd_workspace(*s) for s in shapes),
                   mx.mpx_layernorm_bwd_workspace(M, d))
@@ -415,6 +417,7 @@ class ViTStep(TrainStep):
         self.side_ln = None  # None: LayerNorm gamma / beta on the second stream
         self.split_last_ln = True
         self.last_bias_on_main = True
+        self.patch_wgrad_on_main = True
 
     def _dominant_call(self, s):
         c, a, blk = self.cfg, self.arena, self.blocks[0]
@@ -693,8 +696,16 @@ class ViTStep(TrainStep):
         if c.image:
             mx.mpx_embed_assemble_bwd(_ptr(dx), _ptr(self.dE), _ptr(G("cls")), _ptr(G("pos")),
                                       B, T, d, dt, nf, s)
-            wgrad(self.patches, self.dE, G("patch.w"), G("patch.b"), B * c.n_patches, d,
-                  c.patch_dim)
+            if self.patch_wgrad_on_main:
+                # the step's last weight gradient: on the step's stream, idle
+                # once the embedding backward is done, beside the second
+                # stream's last LayerNorm gamma / beta instead of after it
+                mx.mpx_linear_bwd(_ptr(self.patches), None, _ptr(self.dE), None, NONE, None,
+                                  _ptr(G("patch.w")), _ptr(G("patch.b")), B * c.n_patches, d,
+                                  c.patch_dim, dt, wsp, wsb, nf, s)
+            else:
+                wgrad(self.patches, self.dE, G("patch.w"), G("patch.b"), B * c.n_patches, d,
+                      c.patch_dim)
         main.wait_stream(side)  # join: the optimizer reads every gradient
 
 
