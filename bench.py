@@ -83,10 +83,10 @@ TRAFFIC = {
         },
     },
     "sweep/adamw": {
-        "fetch_kib": 686822.3, "write_kib": 1367203.6,
-        "fetch_factor": 262144.0 / 131089.0, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 686821.7, "write_kib": 1367203.9,
+        "fetch_factor": 262144.0 / 131088.6, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/sweep.hip": "c602435f1b696d1b01bd40828d85fbd12bbbce651354540e554f5fb723602496",
+            "paper_2507_03312_amd/csrc/sweep.hip": "f6f3065d68b04a498769c3ad2b517512429bc5c108dc6a722f6d23eff5d6b987",
             "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
     },

@@ -4,6 +4,7 @@
  * The calls follow MPX (Gräfe & Trimpe, "MPX: Mixed Precision Training for
  * JAX", arXiv 2507.03312):
  *   §3.1  cast_to_half_precision         -> mpx_cast_to_half
+ *   §3.1  cast_to_float32                -> mpx_cast_to_float
  *   §2, §3.4 half forward/backward       -> mpx_linear_fwd, mpx_linear_bwd,
  *                                            mpx_gemm_batched (+ support ops)
  *   §3.3  DynamicLossScaling.unscale      -> mpx_unscale_check (with the
@@ -113,6 +114,14 @@ int64_t mpx_tlist_numel(mpx_tlist list);
  * in one multi-tensor launch.  `dst` must have the same numels as `src`;
  * `half` is MPX_F16 or MPX_BF16. */
 int mpx_cast_to_half(mpx_tlist src_f32, mpx_tlist dst_half, mpx_dtype half, void* stream);
+
+/* MPX §3.1 cast_to_float32, the other direction: dst[i][j] = float32(src[i][j])
+ * for every tensor i of the half list `src` (dtype `half`), exact, in one
+ * multi-tensor launch.  `dst` (float32) must have the same numels as `src`.
+ * With mpx_cast_to_half it carries the PyTree casts of §3.1 and the
+ * function casts of §3.2 (cast_function, force_full_precision), which the
+ * Python layer composes. */
+int mpx_cast_to_float(mpx_tlist src_half, mpx_tlist dst_f32, mpx_dtype half, void* stream);
 
 /* MPX §3.3 unscale and the finite check of §3.4 (the "convert to float32,
  * divide by the scale, check for overflow" steps of the recipe in §2.1).

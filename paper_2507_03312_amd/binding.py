@@ -54,6 +54,7 @@ _SIGS = {
     "mpx_tlist_destroy": (C.c_int, [P]),
     "mpx_tlist_numel": (I64, [P]),
     "mpx_cast_to_half": (C.c_int, [P, P, I32, P]),
+    "mpx_cast_to_float": (C.c_int, [P, P, I32, P]),
     "mpx_unscale_check": (C.c_int, [P, I32, P, P, P, P]),
     "mpx_scale_update": (C.c_int, [P, P, P]),
     "mpx_adamw_masked": (C.c_int, [P, P, P, P, I32, C.POINTER(AdamWHP), P, P, P, P, I32, P]),
@@ -144,6 +145,10 @@ def _h(t):
 
 def mpx_cast_to_half(src: TensorList, dst: TensorList, half: int, stream: int):
     _check(lib.mpx_cast_to_half(src.handle, dst.handle, half, stream), "mpx_cast_to_half")
+
+
+def mpx_cast_to_float(src: TensorList, dst: TensorList, half: int, stream: int):
+    _check(lib.mpx_cast_to_float(src.handle, dst.handle, half, stream), "mpx_cast_to_float")
 
 
 def mpx_unscale_check(grads: TensorList, gdt: int, d_state: int, d_nonfinite: int,

@@ -140,6 +140,35 @@ __global__ __launch_bounds__(kThreads) void cast_kernel(const Chunk* __restrict_
   for (int i = done + threadIdx.x; i < len; i += kThreads) dst[i] = f2h<HDT>(src[i]);
 }
 
+// The inverse direction: half -> float32, exact (every half value is a
+// float32 value).
+template <int HDT>
+__global__ __launch_bounds__(kThreads) void widen_kernel(const Chunk* __restrict__ chunks,
+                                                         void* const* __restrict__ src_ptrs,
+                                                         void* const* __restrict__ dst_ptrs) {
+  const Chunk c = chunks[blockIdx.x];
+  const uint16_t* src = reinterpret_cast<const uint16_t*>(src_ptrs[c.tensor]) + c.start;
+  float* dst = reinterpret_cast<float*>(dst_ptrs[c.tensor]) + c.start;
+  const int len = c.len;
+  int done = 0;
+  if (aligned16(src) && aligned16(dst)) {
+    for (; done + kStep <= len; done += kStep) {
+      uint2 raw[kUnroll];
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u)
+        raw[u] = ld_nt(src + done + (u * kThreads + threadIdx.x) * kGroup);
+#pragma unroll
+      for (int u = 0; u < kUnroll; ++u) {
+        uint16_t h[4];
+        unpack_h4(raw[u], h);
+        st_nt(dst + done + (u * kThreads + threadIdx.x) * kGroup,
+              make_float4(h2f<HDT>(h[0]), h2f<HDT>(h[1]), h2f<HDT>(h[2]), h2f<HDT>(h[3])));
+      }
+    }
+  }
+  for (int i = done + threadIdx.x; i < len; i += kThreads) dst[i] = h2f<HDT>(src[i]);
+}
+
 // -------------------------------------------------------- unscale/check --
 
 template <int GDT, bool WRITE>
@@ -420,6 +449,21 @@ extern "C" int mpx_cast_to_half(mpx_tlist src, mpx_tlist dst, mpx_dtype half, vo
     cast_kernel<MPX_F16><<<src->nchunks, kThreads, 0, s>>>(src->d_chunks, src->d_ptrs, dst->d_ptrs);
   else
     cast_kernel<MPX_BF16><<<src->nchunks, kThreads, 0, s>>>(src->d_chunks, src->d_ptrs, dst->d_ptrs);
+  MPX_LAUNCHED();
+  return MPX_OK;
+}
+
+extern "C" int mpx_cast_to_float(mpx_tlist src, mpx_tlist dst, mpx_dtype half, void* stream) {
+  clear_error();
+  MPX_REQUIRE(src && dst, "NULL list");
+  MPX_REQUIRE(is_half(half), "half must be MPX_F16 or MPX_BF16");
+  MPX_REQUIRE(same_shape(src, dst), "src and dst lists differ in shape");
+  if (src->nchunks == 0) return MPX_OK;
+  hipStream_t s = (hipStream_t)stream;
+  if (half == MPX_F16)
+    widen_kernel<MPX_F16><<<src->nchunks, kThreads, 0, s>>>(src->d_chunks, src->d_ptrs, dst->d_ptrs);
+  else
+    widen_kernel<MPX_BF16><<<src->nchunks, kThreads, 0, s>>>(src->d_chunks, src->d_ptrs, dst->d_ptrs);
   MPX_LAUNCHED();
   return MPX_OK;
 }
