@@ -25,7 +25,10 @@ linear-layer GEMM call of one block against the dense MFMA peak.  `sweep`
 1e8 fp16 gradient elements in 200 tensors: unscale + check + masked AdamW +
 scale update GB/s on applied steps (28 B per element), and the time of a
 skipped step (a non-finite gradient: check, no AdamW write, scale halved)
-separately.  `cpu_baseline` times the CPU oracle on a bounded sample.
+separately.  `step_roofline` is the whole step's lower bound: every call of
+the step at the larger of its MFMA time and its HBM time at peak for its
+algorithmic flops and bytes, summed, and its ratio to the measured step
+time.  `cpu_baseline` times the CPU oracle on a bounded sample.
 
 --step-only runs the warmup and the timed steps and nothing else (no
 per-kernel timing graphs, no sweep, no oracle), so that a kernel trace of
@@ -221,6 +224,101 @@ def calibration_copy(args, dev):
     dst = torch.empty_like(src)
     dst.copy_(src)
     torch.cuda.synchronize()
+
+
+def step_calls(cfg, n_params: int):
+    """(kind, name, flops, bytes) of every call of one mixed-precision step:
+    the algorithmic work, each operand read once and each result written once
+    (half values 2 B, float32 4 B; split-K partials, re-reads and workspaces
+    are not algorithmic).  kind is "gemm", "attention", "support" or
+    "optimizer"."""
+    h = 2
+    out = []
+
+    def gemm(name, M, N, K, extra_in=0, outs=1, bias=True, kind="gemm"):
+        # C[M, N] = A[M, K] B[N, K]^T (+ bias, + extra operands of M x N)
+        b = h * (M * K + N * K + (N if bias else 0) + (extra_in + outs) * M * N)
+        out.append((kind, name, 2.0 * M * N * K, b))
+
+    def support(name, b):
+        out.append(("support", name, 0.0, b))
+
+    B = cfg.batch
+    if cfg.kind == "mlp":
+        D, Hd = cfg.d_in, cfg.d_hidden
+        support("cast inputs, targets", 2 * B * D * (4 + h))
+        gemm("fc1.fwd+gelu", B, Hd, D, outs=2)
+        gemm("fc2.fwd", B, D, Hd)
+        support("mse", 2 * B * D * h + B * D * h)
+        gemm("fc2.dW", D, Hd, B, bias=False)                       # dW = dY^T H (+ db)
+        gemm("fc2.dX+gelu'", B, Hd, D, extra_in=1, bias=False)
+        gemm("fc1.dW", Hd, D, B, bias=False)
+    else:
+        T, d, F, H, hd, L, C = cfg.tokens, cfg.d_model, cfg.d_mlp, cfg.heads, cfg.head_dim, cfg.depth, cfg.classes
+        M, ldP = B * T, -(-T // 8) * 8
+        att_f = B * H * (4.0 * T * T * hd)
+        att_fb = h * B * H * (4 * T * hd + T * ldP)               # Q, K, V read; O, P written
+        att_bf = B * H * (10.0 * T * T * hd)
+        att_bb = h * B * H * (7 * T * hd + T * ldP)               # Q, K, V, dO, P read; dQKV written
+        if cfg.image:
+            G, Pd = cfg.n_patches, cfg.patch_dim
+            support("patchify+cast", B * cfg.image * cfg.image * cfg.channels * 4 + B * G * Pd * h)
+            gemm("patch.fwd", B * G, d, Pd)
+            support("embed assemble", h * (B * G * d + T * d + M * d))
+        for i in range(L):
+            p = f"blk{i}."
+            if i == 0 and not cfg.image:
+                support(p + "ln1.fwd+cast", M * d * (4 + 2 * h))
+            else:
+                support(p + "ln1.fwd", 2 * h * M * d)
+            gemm(p + "qkv.fwd", M, 3 * d, d)
+            out.append(("attention", p + "attn.fwd", att_f, att_fb))
+            gemm(p + "proj.fwd+res", M, d, d, extra_in=1)
+            support(p + "ln2.fwd", 2 * h * M * d)
+            gemm(p + "up.fwd+gelu", M, F, d, outs=2)
+            gemm(p + "down.fwd+res", M, d, F, extra_in=1)
+        # fused head: final LN on the CLS rows, logits, CE with the scale seed,
+        # backward to the LN input; its weight gradient
+        gemm("head.fwd", B, C, d)
+        gemm("head.dX", B, d, C, bias=False)
+        gemm("head.dW", C, d, B, bias=False)
+        for i in reversed(range(L)):
+            p = f"blk{i}."
+            gemm(p + "down.dW", d, F, M, bias=False)
+            gemm(p + "down.dX+gelu'", M, F, d, extra_in=1, bias=False)
+            gemm(p + "up.dW", F, d, M, bias=False)
+            gemm(p + "up.dX", M, d, F, bias=False)
+            support(p + "ln2.bwd", 4 * h * M * d)                   # x1, dc, residual read; dx1 written
+            gemm(p + "proj.dW", d, d, M, bias=False)
+            gemm(p + "proj.dX", M, d, d, bias=False)
+            out.append(("attention", p + "attn.bwd", att_bf, att_bb))
+            gemm(p + "qkv.dW", 3 * d, d, M, bias=False)
+            gemm(p + "qkv.dX", M, d, 3 * d, bias=False)
+            last_tokens = i == 0 and not cfg.image                 # gamma / beta only
+            support(p + "ln1.bwd", (2 if last_tokens else 4) * h * M * d)
+        if cfg.image:
+            support("embed assemble.bwd", h * (M * d + B * G * d))
+            gemm("patch.dW", d, Pd, B * G, bias=False)
+    out.append(("optimizer", "masked AdamW + half copy", 0.0, 28 * n_params))
+    return out
+
+
+def step_roofline(cfg, n_params: int, peak_tflops: float, ms_per_step: float):
+    """The step's lower bound: each call at the larger of its MFMA time and
+    its HBM time at peak, summed (calls that run side by side could overlap
+    one's compute with another's traffic, so this is the serial bound)."""
+    parts = {}
+    flops = byts = 0.0
+    for kind, _, f, b in step_calls(cfg, n_params):
+        t = max(f / (peak_tflops * 1e12), b / (PEAK_HBM_GBS * 1e9)) * 1e3
+        parts[kind] = parts.get(kind, 0.0) + t
+        flops += f
+        byts += b
+    ms = sum(parts.values())
+    return {"ms": round(ms, 4), "frac": round(ms / ms_per_step, 4),
+            "parts_ms": {k: round(v, 4) for k, v in parts.items()},
+            "flops": flops, "bytes": int(byts),
+            "rule": "sum over the step's calls of max(flops / MFMA peak, algorithmic bytes / HBM peak)"}
 
 
 def gemm_table(st, peak):
@@ -484,6 +582,8 @@ def main():
             "roofline": roof}
     if gemm:
         line["gemm"] = gemm
+    n_params = sum(int(np.prod(shape)) for _, shape, _ in workloads.param_specs(cfg))
+    line["step_roofline"] = step_roofline(cfg, n_params, peak, ms)
     del st
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
