@@ -77,6 +77,47 @@ def test_layernorm_fwd_bwd(fmt, rows, d):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("rows,d", [(12608, 768), (16640, 384), (37, 768), (9, 384), (1, 768), (3, 384)])
+def test_layernorm_row_groups_match_one_wave_rows(fmt, rows, d):
+    """At d = 384 and 768 with 16-byte aligned rows, the forward and the
+    dX-only backward give each row 16 or 32 lanes; the same values with rows
+    4 halves apart (ldx = d + 4) take the one-wave-per-row kernels.  The two
+    sum in the same order, so every output bit agrees: normal rows, a
+    constant row (zero variance), an all-zero row, an all -0 row, and row
+    counts that leave the last wave partly empty."""
+    x = _rand((rows, d), fmt, 31, 2.0, 0.5)
+    x[0] = 0.0
+    if rows > 1:
+        x[1] = 3.0
+    if rows > 2:
+        x[2] = -0.0
+    g, b = _rand((d,), fmt, 32, 0.2, 1.0), _rand((d,), fmt, 33, 0.2)
+    dy, rg = _rand((rows, d), fmt, 34), _rand((rows, d), fmt, 35)
+    tx, tg, tb, tdy, trg = (to_dev_half(a, fmt) for a in (x, g, b, dy, rg))
+    wide = _empty((rows, d + 4), fmt)
+    wide[:, :d] = tx
+    dt = mx.DTYPES[fmt]
+    y1, y2 = _empty((rows, d), fmt), _empty((rows, d), fmt)
+    mr1 = torch.zeros(2 * rows, dtype=torch.float32, device="cuda")
+    mr2 = torch.zeros_like(mr1)
+    mx.mpx_layernorm_fwd(tx.data_ptr(), d, tg.data_ptr(), tb.data_ptr(), y1.data_ptr(), mr1.data_ptr(),
+                         rows, d, dt, _s())
+    mx.mpx_layernorm_fwd(wide.data_ptr(), d + 4, tg.data_ptr(), tb.data_ptr(), y2.data_ptr(),
+                         mr2.data_ptr(), rows, d, dt, _s())
+    for res in (None, trg):
+        dx1, dx2 = _empty((rows, d), fmt), _empty((rows, d), fmt)
+        rp = None if res is None else res.data_ptr()
+        mx.mpx_layernorm_bwd(tx.data_ptr(), d, tg.data_ptr(), tdy.data_ptr(), rp, dx1.data_ptr(), d,
+                             None, None, rows, d, dt, None, 0, None, _s())
+        mx.mpx_layernorm_bwd(wide.data_ptr(), d + 4, tg.data_ptr(), tdy.data_ptr(), rp, dx2.data_ptr(), d,
+                             None, None, rows, d, dt, None, 0, None, _s())
+        torch.cuda.synchronize()
+        assert torch.equal(dx1.view(torch.int16), dx2.view(torch.int16)), ("dX", res is None)
+    assert torch.equal(y1.view(torch.int16), y2.view(torch.int16)), "Y"
+    assert torch.equal(mr1.view(torch.int32), mr2.view(torch.int32)), "mean / rstd"
+
+
+@pytest.mark.parametrize("fmt", FMTS)
 def test_layernorm_bwd_subsets_match_full_call(fmt):
     """dX alone (no workspace) and dgamma / dbeta alone, as the two-stream
     backward issues them, give the bits of the full call."""
