@@ -989,21 +989,45 @@ void gemm_dma_persistent_kernel(GemmArgs g) {
 // p < dbparts, one wave per row (nrows rows; 0: none): lane l adds p = l,
 // l + 64, ... in order, then the fixed wave tree of wave_sum; db = half of
 // that.  Non-finite results are added to *nonfinite when it is set.
-template <int DT>
+// VEC (MN a multiple of 4, ws 16-byte and C 8-byte aligned): each thread
+// reduces 4 consecutive outputs with 16-byte loads and one 8-byte store, each
+// output summed in the same split order as the scalar form (the same bits):
+// 3072 x 768 from 2 splits alone 6.3 -> 5.4 us, 768 x 768 from 8 splits 6.2 -> 4.9.
+template <int DT, bool VEC>
 __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restrict__ ws, int splits,
                                                             int64_t MN, uint16_t* __restrict__ C,
                                                             int32_t* __restrict__ nonfinite,
                                                             const float* __restrict__ dbp, int dbparts,
                                                             int64_t nrows, uint16_t* __restrict__ db) {
-  const int64_t mn_blocks = (MN + 255) / 256;
+  constexpr int PER = VEC ? 4 : 1;
+  const int64_t mn_blocks = (MN + 256 * PER - 1) / (256 * PER);
   if ((int64_t)blockIdx.x < mn_blocks) {
-    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * PER;
     if (i >= MN) return;
-    float s = ws[i];
-    for (int k = 1; k < splits; ++k) s += ws[(int64_t)k * MN + i];
-    const uint16_t h = f2h<DT>(s);
-    C[i] = h;
-    if (nonfinite) add_nonfinite(nonfinite, h_nonfinite<DT>(h) ? 1 : 0);
+    if constexpr (VEC) {
+      f32x4 s = *reinterpret_cast<const f32x4*>(ws + i);
+      for (int k = 1; k < splits; ++k) {
+        const f32x4 t = *reinterpret_cast<const f32x4*>(ws + (int64_t)k * MN + i);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s[e] += t[e];
+      }
+      uint16_t h[4];
+      int bad = 0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        h[e] = f2h<DT>(s[e]);
+        bad += h_nonfinite<DT>(h[e]) ? 1 : 0;
+      }
+      *reinterpret_cast<uint2*>(C + i) =
+          make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+      if (nonfinite) add_nonfinite(nonfinite, bad);
+    } else {
+      float s = ws[i];
+      for (int k = 1; k < splits; ++k) s += ws[(int64_t)k * MN + i];
+      const uint16_t h = f2h<DT>(s);
+      C[i] = h;
+      if (nonfinite) add_nonfinite(nonfinite, h_nonfinite<DT>(h) ? 1 : 0);
+    }
     return;
   }
   const int64_t row = ((int64_t)blockIdx.x - mn_blocks) * 4 + (threadIdx.x >> 6);
@@ -1021,8 +1045,14 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* __restr
 }
 
 // launch shape of splitk_reduce_kernel: MN outputs and nrows bias rows
-inline unsigned splitk_reduce_blocks(int64_t MN, int64_t nrows) {
-  return (unsigned)((MN + 255) / 256 + (nrows + 3) / 4);
+inline unsigned splitk_reduce_blocks(int64_t MN, int64_t nrows, bool vec) {
+  const int64_t per = vec ? 1024 : 256;
+  return (unsigned)((MN + per - 1) / per + (nrows + 3) / 4);
+}
+
+inline bool splitk_reduce_vec(const float* ws, int64_t MN, const uint16_t* C) {
+  return MN % 4 == 0 && (reinterpret_cast<uintptr_t>(ws) & 15u) == 0 &&
+         (reinterpret_cast<uintptr_t>(C) & 7u) == 0;
 }
 
 // ------------------------------------------------------------ dispatch --

@@ -85,7 +85,7 @@ def test_linear_fwd(fmt, mnk):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
-@pytest.mark.parametrize("mnk", SHAPES + [(4096, 384, 384), (2500, 96, 40)],
+@pytest.mark.parametrize("mnk", SHAPES + [(4096, 384, 384), (2500, 96, 40), (8192, 33, 50)],
                          ids=lambda s: "x".join(map(str, s)))
 def test_linear_bwd(fmt, mnk):
     M, N, K = mnk
