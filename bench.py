@@ -59,28 +59,28 @@ DEFAULT_CONFIG = "vit_b"
 # they no longer match, the figure is stale and reported as null.
 TRAFFIC = {
     "vit_block/blk0.up.fwd": {
-        "fetch_kib": 13948.5, "write_kib": 49920.0,
-        "fetch_factor": 262144.0 / 131088.9, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 13947.7, "write_kib": 49920.0,
+        "fetch_factor": 262144.0 / 131088.8, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/gemm_kernels.h": "dd6947be2a489bb2aab4eab10bf49f1c70469f16a898583dc92638554d426731",
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "8e0c308ac1b5d6809b80c6ae9e9dc05a12e6987d72d8b54d85ccd4a643a873ca",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
             "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
     },
     "vit_s/blk0.up.fwd": {
-        "fetch_kib": 23835.0, "write_kib": 99840.0,
+        "fetch_kib": 23660.5, "write_kib": 99840.0,
         "fetch_factor": 262144.0 / 131088.3, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/gemm_kernels.h": "dd6947be2a489bb2aab4eab10bf49f1c70469f16a898583dc92638554d426731",
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "8e0c308ac1b5d6809b80c6ae9e9dc05a12e6987d72d8b54d85ccd4a643a873ca",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
             "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
     },
     "vit_b/blk0.up.fwd": {
-        "fetch_kib": 70864.7, "write_kib": 151323.2,
-        "fetch_factor": 262144.0 / 131094.1, "write_factor": 262144.0 / 262144.0,
+        "fetch_kib": 70788.5, "write_kib": 151342.8,
+        "fetch_factor": 262144.0 / 131093.6, "write_factor": 262144.0 / 262144.0,
         "sources": {
-            "paper_2507_03312_amd/csrc/gemm_kernels.h": "dd6947be2a489bb2aab4eab10bf49f1c70469f16a898583dc92638554d426731",
+            "paper_2507_03312_amd/csrc/gemm_kernels.h": "8e0c308ac1b5d6809b80c6ae9e9dc05a12e6987d72d8b54d85ccd4a643a873ca",
             "paper_2507_03312_amd/csrc/mfma.h": "46e04f5162db64f2c8dc7bd5c5aae35c9ba491888000bfd3597337920e363231",
             "paper_2507_03312_amd/csrc/common.h": "2084a1c1294723c666ae58a2f812b765b2e5ea388fca5027c911b15626f0d620",
         },
