@@ -1033,6 +1033,105 @@ __global__ __launch_bounds__(256) void embed_assemble_bwd_kernel(const uint16_t*
   }
 }
 
+// Vector forms of the three kernels above for the usual shapes (rows of
+// 8-element multiples, 16-byte aligned operands): each thread moves 8
+// consecutive values (4 in the backward) with 16-byte (8-byte) accesses and
+// does the same arithmetic per value, in the same order, as the scalar form.
+// ViT-B shapes alone: patchify 35.5 -> 10.2 us, assembly 21.2 -> 7.1, its
+// backward 13.9 -> 8.8.  The backward takes the vector form only from 65536
+// outputs (T d) on: with ViT-S's 24960 its 98 workgroups ran 13.5 -> 17.2.
+template <int DT>
+__global__ __launch_bounds__(256) void patchify_cast_vec_kernel(const float* __restrict__ img,
+                                                                uint16_t* __restrict__ out, int B, int H,
+                                                                int W, int C, int p) {
+  const int pc = p * C, pd = p * pc, pd8 = pd / 8;
+  const int gw = W / p, G = (H / p) * gw;
+  const int64_t t = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t >= (int64_t)B * G * pd8) return;
+  const int row = (int)(t / pd8), e = (int)(t - (int64_t)row * pd8) * 8;
+  const int i = e / pc, r = e - i * pc;
+  const int b = row / G, g = row - b * G;
+  const int gy = g / gw, gx = g - gy * gw;
+  const float* src = img + (((int64_t)b * H + gy * p + i) * W + (int64_t)gx * p) * C + r;
+  const f32x4 a = *reinterpret_cast<const f32x4*>(src);
+  const f32x4 c = *reinterpret_cast<const f32x4*>(src + 4);
+  uint32_t o[4];
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    o[j] = (uint32_t)f2h<DT>(a[2 * j]) | ((uint32_t)f2h<DT>(a[2 * j + 1]) << 16);
+    o[2 + j] = (uint32_t)f2h<DT>(c[2 * j]) | ((uint32_t)f2h<DT>(c[2 * j + 1]) << 16);
+  }
+  *reinterpret_cast<u32x4*>(out + (int64_t)row * pd + e) = u32x4{o[0], o[1], o[2], o[3]};
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void embed_assemble_vec_kernel(const uint16_t* __restrict__ E,
+                                                                 const uint16_t* __restrict__ cls,
+                                                                 const uint16_t* __restrict__ pos,
+                                                                 uint16_t* __restrict__ X, int B, int T,
+                                                                 int64_t d) {
+  const int64_t d8 = d / 8;
+  const int64_t t8 = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (t8 >= (int64_t)B * T * d8) return;
+  const int64_t row = t8 / d8, c = (t8 - row * d8) * 8;
+  const int b = (int)(row / T), t = (int)(row - (int64_t)b * T);
+  const uint16_t* bsrc = t == 0 ? cls + c : E + ((int64_t)b * (T - 1) + t - 1) * d + c;
+  const u32x4 bv = *reinterpret_cast<const u32x4*>(bsrc);
+  const u32x4 pv = *reinterpret_cast<const u32x4*>(pos + (int64_t)t * d + c);
+  uint32_t o[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint16_t lo = f2h<DT>(h2f<DT>((uint16_t)(bv[j] & 0xFFFFu)) + h2f<DT>((uint16_t)(pv[j] & 0xFFFFu)));
+    const uint16_t hi = f2h<DT>(h2f<DT>((uint16_t)(bv[j] >> 16)) + h2f<DT>((uint16_t)(pv[j] >> 16)));
+    o[j] = (uint32_t)lo | ((uint32_t)hi << 16);
+  }
+  *reinterpret_cast<u32x4*>(X + row * d + c) = u32x4{o[0], o[1], o[2], o[3]};
+}
+
+// the backward with 4 consecutive outputs per lane (a wave owns 256)
+template <int DT>
+__global__ __launch_bounds__(256) void embed_assemble_bwd_vec_kernel(const uint16_t* __restrict__ dX,
+                                                                     uint16_t* __restrict__ dE,
+                                                                     uint16_t* __restrict__ dcls,
+                                                                     uint16_t* __restrict__ dpos,
+                                                                     int64_t B, int64_t T, int64_t d,
+                                                                     int32_t* __restrict__ nonfinite) {
+  __shared__ float red[4][4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t total = T * d;
+  const int64_t o = ((int64_t)blockIdx.x * 64 + lane) * 4;
+  float s[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  if (o < total) {
+    const bool body = o >= d;  // d % 4 == 0: the 4 outputs are all CLS or all patch tokens
+#pragma unroll 4
+    for (int64_t b = w; b < B; b += 4) {
+      const uint2 v = *reinterpret_cast<const uint2*>(dX + b * total + o);
+      s[0] += h2f<DT>((uint16_t)(v.x & 0xFFFFu));
+      s[1] += h2f<DT>((uint16_t)(v.x >> 16));
+      s[2] += h2f<DT>((uint16_t)(v.y & 0xFFFFu));
+      s[3] += h2f<DT>((uint16_t)(v.y >> 16));
+      if (body) *reinterpret_cast<uint2*>(dE + b * (total - d) + (o - d)) = v;
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) red[e][w][lane] = s[e];
+  __syncthreads();
+  if (w == 0 && o < total) {
+    uint16_t h[4];
+    int bad = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      h[e] = f2h<DT>((red[e][0][lane] + red[e][1][lane]) + (red[e][2][lane] + red[e][3][lane]));
+      bad += h_nonfinite<DT>(h[e]) ? (o < d ? 2 : 1) : 0;
+    }
+    const uint2 hv = make_uint2((uint32_t)h[0] | ((uint32_t)h[1] << 16), (uint32_t)h[2] | ((uint32_t)h[3] << 16));
+    *reinterpret_cast<uint2*>(dpos + o) = hv;
+    if (o < d) *reinterpret_cast<uint2*>(dcls + o) = hv;
+    // dpos and, for the CLS position, dcls: one or two parameter elements each
+    if (nonfinite) add_nonfinite(nonfinite, bad);
+  }
+}
+
 __global__ __launch_bounds__(256) void gather_rows_kernel(const uint16_t* __restrict__ src, int64_t stride,
                                                           uint16_t* __restrict__ dst, int64_t rows,
                                                           int64_t d) {
@@ -1419,6 +1518,13 @@ extern "C" int mpx_patchify_cast(const float* images, void* patches, int64_t B, 
     return MPX_OK;
   }
   MPX_REQUIRE(B * H * W * C < ((int64_t)1 << 31), "at most 2^31 - 1 image values");
+  if ((p * C) % 8 == 0 && (W * C) % 4 == 0 && (reinterpret_cast<uintptr_t>(images) & 15u) == 0 &&
+      (reinterpret_cast<uintptr_t>(patches) & 15u) == 0) {
+    const int64_t n8 = B * H * W * C / 8;  // one thread per 8 patch values
+    MPX_DT_DISPATCH(dt, patchify_cast_vec_kernel, (unsigned)((n8 + 255) / 256), 256, stream, images,
+                    (uint16_t*)patches, (int)B, (int)H, (int)W, (int)C, (int)p);
+    return MPX_OK;
+  }
   {
     const int64_t pd = p * p * C, rows = B * (H / p) * (W / p);
     const dim3 grid((unsigned)((pd + 255) / 256), (unsigned)std::min<int64_t>(rows, 65535));
@@ -1440,6 +1546,14 @@ extern "C" int mpx_embed_assemble(const void* E, const void* cls, const void* po
     return MPX_OK;
   }
   MPX_REQUIRE(B * T < ((int64_t)1 << 31), "at most 2^31 - 1 token rows");
+  auto al16 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 15u) == 0; };
+  if (d % 8 == 0 && al16(E) && al16(cls) && al16(pos) && al16(X)) {
+    const int64_t n8 = B * T * (d / 8);
+    MPX_DT_DISPATCH(dt, embed_assemble_vec_kernel, (unsigned)((n8 + 255) / 256), 256, stream,
+                    (const uint16_t*)E, (const uint16_t*)cls, (const uint16_t*)pos, (uint16_t*)X, (int)B,
+                    (int)T, d);
+    return MPX_OK;
+  }
   {
     const dim3 grid((unsigned)((d + 255) / 256), (unsigned)std::min<int64_t>(B * T, 65535));
     MPX_DT_DISPATCH(dt, embed_assemble_kernel, grid, 256, stream, (const uint16_t*)E,
@@ -1459,6 +1573,13 @@ extern "C" int mpx_embed_assemble_bwd(const void* dX, void* dE, void* dcls, void
     MPX_REQUIRE(!d_nonfinite, "d_nonfinite is counted for half gradients only");
     MPX_HIP(launch_embed_assemble_bwd_f32((const float*)dX, (float*)dE, (float*)dcls, (float*)dpos, B,
                                           T, d, (hipStream_t)stream));
+    return MPX_OK;
+  }
+  auto al8 = [](const void* q) { return (reinterpret_cast<uintptr_t>(q) & 7u) == 0; };
+  if (d % 4 == 0 && T * d >= 65536 && al8(dX) && al8(dE) && al8(dcls) && al8(dpos)) {
+    MPX_DT_DISPATCH(dt, embed_assemble_bwd_vec_kernel, (unsigned)((T * d + 255) / 256), 256, stream,
+                    (const uint16_t*)dX, (uint16_t*)dE, (uint16_t*)dcls, (uint16_t*)dpos, B, T, d,
+                    d_nonfinite);
     return MPX_OK;
   }
   MPX_DT_DISPATCH(dt, embed_assemble_bwd_kernel, (unsigned)((T * d + 63) / 64), 256, stream,

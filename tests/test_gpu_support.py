@@ -77,6 +77,34 @@ def test_layernorm_fwd_bwd(fmt, rows, d):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("B,T,d", [(64, 197, 768), (5, 3, 12)])
+def test_embed_assemble_bwd_vector_form_matches_scalar_form(fmt, B, T, d):
+    """The token-assembly backward on 8-byte aligned operands (4 outputs per
+    lane from 65536 outputs T d on) and on a cotangent one element off that
+    alignment (one output per lane) sum in the same order: dpos, dcls, dE and
+    the non-finite count agree bit for bit, with overflowing columns
+    included (the small shape takes the one-output form both times)."""
+    dX = _rand((B * T, d), fmt, 41, 100.0)
+    big = 60000.0 if fmt == "f16" else 3e38
+    dX[:, 0] = big  # column 0 (a CLS and a patch position) overflows when summed
+    flat = np.concatenate([np.zeros(1, np.float32), dX.reshape(-1)])
+    tflat = to_dev_half(flat, fmt)
+    t_al = tflat[1:].clone()              # 8-byte aligned copy
+    outs = []
+    for src in (t_al, tflat[1:]):         # the view is 2 bytes off
+        dE, dcls, dpos = _empty((B * (T - 1), d), fmt), _empty((d,), fmt), _empty((T, d), fmt)
+        nf = torch.zeros(1, dtype=torch.int32, device="cuda")
+        mx.mpx_embed_assemble_bwd(src.data_ptr(), dE.data_ptr(), dcls.data_ptr(), dpos.data_ptr(), B, T, d,
+                                  mx.DTYPES[fmt], nf.data_ptr(), _s())
+        torch.cuda.synchronize()
+        outs.append((dE, dcls, dpos, int(nf.item())))
+    (e1, c1, p1, n1), (e2, c2, p2, n2) = outs
+    for a, b_, what in ((e1, e2, "dE"), (c1, c2, "dcls"), (p1, p2, "dpos")):
+        assert torch.equal(a.view(torch.int16), b_.view(torch.int16)), what
+    assert n1 == n2 and n1 >= T + 1
+
+
+@pytest.mark.parametrize("fmt", FMTS)
 @pytest.mark.parametrize("rows,d", [(12608, 768), (16640, 384), (37, 768), (9, 384), (1, 768), (3, 384)])
 def test_layernorm_row_groups_match_one_wave_rows(fmt, rows, d):
     """At d = 384 and 768 with 16-byte aligned rows, the forward and the
@@ -247,7 +275,8 @@ def test_mse(fmt):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
-@pytest.mark.parametrize("B,Hh,C,p,d", [(3, 8, 3, 4, 16), (9, 32, 3, 4, 384), (2, 48, 3, 16, 100)],
+@pytest.mark.parametrize("B,Hh,C,p,d", [(3, 8, 3, 4, 16), (9, 32, 3, 4, 384), (2, 48, 3, 16, 100),
+                                         (2, 64, 3, 16, 768), (3, 8, 3, 4, 50)],
                          ids=lambda v: str(v))
 def test_patchify_embed_assemble_and_backward(fmt, B, Hh, C, p, d):
     pol = Policy(fmt)
