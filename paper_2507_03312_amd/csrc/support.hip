@@ -88,6 +88,25 @@ __device__ __forceinline__ float ln_affine(float x, float mean, float rstd, floa
   return y;
 }
 
+// The LayerNorm backward's per-element arithmetic with every multiply-add
+// written out and every rounded product kept as such (the empty asm), so
+// each kernel that evaluates it (one wave per row, rows of 16 or 32 lanes,
+// the classifier head) rounds identically whatever the compiler would
+// otherwise contract:
+//   dxh = dy g (rounded), s1 += dxh, s2 = fma(dxh, xhat, s2),
+//   dx = rstd fma(-xhat, m2, fma(dy, g, -m1)) (rounded before the cast),
+//   dgamma partial = fma(dy, xhat, p), dbeta partial += dy.
+__device__ __forceinline__ float ln_dxh(float dy, float g) {
+  float t = dy * g;
+  asm volatile("" : "+v"(t));
+  return t;
+}
+__device__ __forceinline__ float ln_dx(float dy, float g, float xh, float m1, float m2, float rstd) {
+  float t = rstd * __builtin_fmaf(-xh, m2, __builtin_fmaf(dy, g, -m1));
+  asm volatile("" : "+v"(t));
+  return t;
+}
+
 // mean and 1/sqrt(var + eps) of one row held by a wave (two-pass)
 template <int VPL>
 __device__ __forceinline__ void row_stats(const RowVec<VPL>& r, int64_t d, int lane, float& mean,
@@ -104,7 +123,7 @@ __device__ __forceinline__ void row_stats(const RowVec<VPL>& r, int64_t d, int l
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       const float c = col_ok(d, lane, v, j) ? r.x[v][j] - mean : 0.0f;
-      q += c * c;
+      q = __builtin_fmaf(c, c, q);
     }
   rstd = 1.0f / sqrtf(wave_sum(q) / (float)d + kLnEps);
 }
@@ -298,11 +317,11 @@ __global__ __launch_bounds__(64 * kLnBwdWaves) void layernorm_bwd_kernel(
         const float xh = col_ok(d, lane, v, j) ? (xf.x[v][j] - mean) * rstd : 0.0f;
         xf.x[v][j] = xh;
         const float dyv = hx<DT>(dy.w[v], j);
-        const float dxh = dyv * g.x[v][j];
+        const float dxh = ln_dxh(dyv, g.x[v][j]);
         s1 += dxh;
-        s2 += dxh * xh;
+        s2 = __builtin_fmaf(dxh, xh, s2);
         if (PART) {
-          pg[v][j] += dyv * xh;
+          pg[v][j] = __builtin_fmaf(dyv, xh, pg[v][j]);
           pb[v][j] += dyv;
         }
       }
@@ -314,7 +333,7 @@ __global__ __launch_bounds__(64 * kLnBwdWaves) void layernorm_bwd_kernel(
       for (int v = 0; v < VPL; ++v)
 #pragma unroll
         for (int j = 0; j < 8; ++j) {
-          const float dx = rstd * (hx<DT>(dy.w[v], j) * g.x[v][j] - s1 - xf.x[v][j] * s2);
+          const float dx = ln_dx(hx<DT>(dy.w[v], j), g.x[v][j], xf.x[v][j], s1, s2, rstd);
           uint16_t o = f2h<DT>(dx);
           if (Rg) o = f2h<DT>(hx<DT>(rg.w[v], j) + h2f<DT>(o));
           h[v][j] = o;
@@ -455,7 +474,7 @@ __device__ __forceinline__ void group_row_stats(const GroupRow<DT, LPR, VPL, NCH
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
         const float c = G::valid(k, v) ? x.f(k, v, j) - mean : 0.0f;
-        s[k] += c * c;
+        s[k] = __builtin_fmaf(c, c, s[k]);
       }
   }
   rstd = 1.0f / sqrtf(group_total<LPR>(s) / (float)G::D + kLnEps);
@@ -497,8 +516,59 @@ __global__ __launch_bounds__(256) void layernorm_fwd_group_kernel(
   }
 }
 
+// dX of one group row from its loaded x, dY, gamma (and residual
+// cotangent): the arithmetic of layernorm_bwd_kernel's dX, shared by the
+// grouped kernels with and without gamma / beta (the same bits either way).
+// Returns mean and rstd for the caller's gamma / beta terms.
+template <int DT, int LPR, int VPL, int NCH>
+__device__ __forceinline__ void group_dx_row(const GroupRow<DT, LPR, VPL, NCH>& x,
+                                             const GroupRow<DT, LPR, VPL, NCH>& dy,
+                                             const GroupRow<DT, LPR, VPL, NCH>& g,
+                                             const GroupRow<DT, LPR, VPL, NCH>& rg, bool has_rg,
+                                             uint16_t* __restrict__ out, bool store, int li, float& mean,
+                                             float& rstd) {
+  using G = LnGroup<LPR, VPL, NCH>;
+  group_row_stats(x, mean, rstd);
+  float s1[G::K], s2[G::K];
+#pragma unroll
+  for (int k = 0; k < G::K; ++k) {
+    s1[k] = 0.0f;
+    s2[k] = 0.0f;
+#pragma unroll
+    for (int v = 0; v < VPL; ++v)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float xh = G::valid(k, v) ? (x.f(k, v, j) - mean) * rstd : 0.0f;
+        const float dxh = ln_dxh(dy.f(k, v, j), g.f(k, v, j));
+        s1[k] += dxh;
+        s2[k] = __builtin_fmaf(dxh, xh, s2[k]);
+      }
+  }
+  const float m1 = group_total<LPR>(s1) / (float)G::D;
+  const float m2 = group_total<LPR>(s2) / (float)G::D;
+  if (!store) return;
+#pragma unroll
+  for (int k = 0; k < G::K; ++k)
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      if (!G::valid(k, v)) continue;
+      uint16_t h[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float xh = (x.f(k, v, j) - mean) * rstd;
+        const float dx = ln_dx(dy.f(k, v, j), g.f(k, v, j), xh, m1, m2, rstd);
+        uint16_t o = f2h<DT>(dx);
+        if (has_rg) o = f2h<DT>(rg.f(k, v, j) + h2f<DT>(o));
+        h[j] = o;
+      }
+      *reinterpret_cast<u32x4*>(out + 8 * G::chunk(li, k, v)) =
+          u32x4{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16), h[4] | ((uint32_t)h[5] << 16),
+                h[6] | ((uint32_t)h[7] << 16)};
+    }
+}
+
 // dX alone (the call without gamma / beta), optionally plus a residual
-// cotangent: the arithmetic of layernorm_bwd_kernel<DT, VPL, true, false>
+// cotangent: one group row per group, no partials.
 template <int DT, int LPR, int VPL, int NCH>
 __global__ __launch_bounds__(256) void layernorm_bwd_dx_group_kernel(
     const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __restrict__ gamma,
@@ -514,43 +584,86 @@ __global__ __launch_bounds__(256) void layernorm_bwd_dx_group_kernel(
   if (Rg) rg.load(Rg + rc * ldo, li);
   g.load(gamma, li);
   float mean, rstd;
-  group_row_stats(x, mean, rstd);
-  float s1[G::K], s2[G::K];
+  group_dx_row(x, dy, g, rg, Rg != nullptr, dX + rc * ldo, r < rows, li, mean, rstd);
+}
+
+// gamma / beta column partials (and dX when DX), grouped: the workgroups
+// (at most kLnBwdMaxBlocks) stride over tiles of 4 K rows, each group of a
+// wave taking one row of the tile; each lane accumulates its columns' terms
+// dy xhat and dy over its group's rows in order, and the 4 K group sums of
+// a workgroup are added in group order through LDS into one partial row.
+// The gamma / beta call and the full call share this kernel and so give
+// the same gamma / beta bits; their dX equals the dX-only kernel's.
+template <int DT, int LPR, int VPL, int NCH, bool DX>
+__global__ __launch_bounds__(256) void layernorm_bwd_part_group_kernel(
+    const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __restrict__ gamma,
+    const uint16_t* __restrict__ dY, const uint16_t* __restrict__ Rg, uint16_t* __restrict__ dX,
+    int64_t ldo, int64_t rows, float* __restrict__ part) {
+  using G = LnGroup<LPR, VPL, NCH>;
+  constexpr int K = G::K, D = G::D;
+  const int lane = threadIdx.x & 63, li = lane % LPR, gi = lane / LPR, w = threadIdx.x >> 6;
+  GroupRow<DT, LPR, VPL, NCH> g;
+  g.load(gamma, li);
+  float pg[K][VPL][8], pb[K][VPL][8];
 #pragma unroll
-  for (int k = 0; k < G::K; ++k) {
-    s1[k] = 0.0f;
-    s2[k] = 0.0f;
+  for (int k = 0; k < K; ++k)
 #pragma unroll
     for (int v = 0; v < VPL; ++v)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float xh = G::valid(k, v) ? (x.f(k, v, j) - mean) * rstd : 0.0f;
-        const float dxh = dy.f(k, v, j) * g.f(k, v, j);
-        s1[k] += dxh;
-        s2[k] += dxh * xh;
-      }
-  }
-  const float m1 = group_total<LPR>(s1) / (float)G::D;
-  const float m2 = group_total<LPR>(s2) / (float)G::D;
-  if (r >= rows) return;
+      for (int j = 0; j < 8; ++j) pg[k][v][j] = pb[k][v][j] = 0.0f;
+  const int64_t stride = (int64_t)gridDim.x * 4 * K;
+  for (int64_t base = ((int64_t)blockIdx.x * 4 + w) * K; base < rows; base += stride) {  // uniform
+    const int64_t r = base + gi;
+    const bool ok = r < rows;
+    const int64_t rc = ok ? r : rows - 1;
+    GroupRow<DT, LPR, VPL, NCH> x, dy, rg;
+    x.load(X + rc * ldx, li);
+    dy.load(dY + rc * D, li);
+    if (DX && Rg) rg.load(Rg + rc * ldo, li);
+    float mean, rstd;
+    if (DX) {
+      group_dx_row(x, dy, g, rg, Rg != nullptr, dX + rc * ldo, ok, li, mean, rstd);
+    } else {
+      group_row_stats(x, mean, rstd);
+    }
+    if (ok) {
 #pragma unroll
-  for (int k = 0; k < G::K; ++k)
+      for (int k = 0; k < K; ++k)
+#pragma unroll
+        for (int v = 0; v < VPL; ++v)
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            if (!G::valid(k, v)) continue;
+            const float xh = (x.f(k, v, j) - mean) * rstd;
+            const float dyv = dy.f(k, v, j);
+            pg[k][v][j] = __builtin_fmaf(dyv, xh, pg[k][v][j]);
+            pb[k][v][j] += dyv;
+          }
+    }
+  }
+  // the 4 K group sums of the workgroup, added in group order
+  __shared__ float red[4 * K][2][D];
+#pragma unroll
+  for (int k = 0; k < K; ++k)
 #pragma unroll
     for (int v = 0; v < VPL; ++v) {
       if (!G::valid(k, v)) continue;
-      uint16_t h[8];
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        const float xh = (x.f(k, v, j) - mean) * rstd;
-        const float dx = rstd * (dy.f(k, v, j) * g.f(k, v, j) - m1 - xh * m2);
-        uint16_t o = f2h<DT>(dx);
-        if (Rg) o = f2h<DT>(rg.f(k, v, j) + h2f<DT>(o));
-        h[j] = o;
+        const int col = 8 * G::chunk(li, k, v) + j;
+        red[w * K + gi][0][col] = pg[k][v][j];
+        red[w * K + gi][1][col] = pb[k][v][j];
       }
-      *reinterpret_cast<u32x4*>(dX + r * ldo + 8 * G::chunk(li, k, v)) =
-          u32x4{h[0] | ((uint32_t)h[1] << 16), h[2] | ((uint32_t)h[3] << 16), h[4] | ((uint32_t)h[5] << 16),
-                h[6] | ((uint32_t)h[7] << 16)};
     }
+  __syncthreads();
+  float* out = part + (int64_t)blockIdx.x * 2 * D;
+  for (int i = threadIdx.x; i < 2 * D; i += 256) {
+    const int which = i / D, col = i - which * D;
+    float t = red[0][which][col];
+#pragma unroll
+    for (int q = 1; q < 4 * K; ++q) t += red[q][which][col];
+    out[i] = t;
+  }
 }
 
 // Whether a call takes the grouped kernels: d of 384 or 768 and every row
@@ -853,10 +966,10 @@ __global__ __launch_bounds__(64 * kHeadWaves) void classifier_head_kernel(
         dz[v][j] = dyv;
         const float xh = col_ok(d, lane, v, j) ? (x.x[v][j] - mean) * rstd : 0.0f;
         x.x[v][j] = xh;
-        const float dxh = dyv * g.x[v][j];
+        const float dxh = ln_dxh(dyv, g.x[v][j]);
         s1 += dxh;
-        s2 += dxh * xh;
-        pg[v][j] += dyv * xh;
+        s2 = __builtin_fmaf(dxh, xh, s2);
+        pg[v][j] = __builtin_fmaf(dyv, xh, pg[v][j]);
         pb[v][j] += dyv;
       }
     s1 = wave_sum(s1) / (float)d;
@@ -865,7 +978,7 @@ __global__ __launch_bounds__(64 * kHeadWaves) void classifier_head_kernel(
 #pragma unroll
     for (int v = 0; v < VPL; ++v)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) h[v][j] = f2h<DT>(rstd * (dz[v][j] * g.x[v][j] - s1 - x.x[v][j] * s2));
+      for (int j = 0; j < 8; ++j) h[v][j] = f2h<DT>(ln_dx(dz[v][j], g.x[v][j], x.x[v][j], s1, s2, rstd));
     store_row<DT, VPL>(dX + r * ldo, d, lane, h);
   }
   // the waves' column partials, combined in wave order through LDS
@@ -1292,6 +1405,35 @@ extern "C" int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, 
     return MPX_OK;
   }
   hipStream_t s = (hipStream_t)stream;
+  if (part && ln_grouped(d, {X, gamma, dY, Rgrad, dX}, {ldx, ldo})) {
+    const int rows_per_tile = d == 768 ? 8 : 16;
+    const int nbg = (int)std::min<int64_t>((rows + rows_per_tile - 1) / rows_per_tile, kLnBwdMaxBlocks);
+#define MPX_LNGP(DTv, LPR, VPL, NCH, DXv)                                                                \
+  layernorm_bwd_part_group_kernel<DTv, LPR, VPL, NCH, DXv><<<nbg, 256, 0, s>>>(                         \
+      (const uint16_t*)X, ldx, (const uint16_t*)gamma, (const uint16_t*)dY, (const uint16_t*)Rgrad,     \
+      (uint16_t*)dX, ldo, rows, part)
+#define MPX_LNGP_D(DTv, DXv)                        \
+  do {                                              \
+    if (d == 768) MPX_LNGP(DTv, 32, 2, 96, DXv);    \
+    else MPX_LNGP(DTv, 16, 1, 48, DXv);             \
+  } while (0)
+    const unsigned fin2 = colsum_final_blocks(2 * d);
+    if (dt == MPX_F16) {
+      if (dX) MPX_LNGP_D(MPX_F16, true);
+      else MPX_LNGP_D(MPX_F16, false);
+      colsum_final_kernel<MPX_F16><<<fin2, 256, 0, s>>>(part, nbg, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta,
+                                                        d, d_nonfinite);
+    } else {
+      if (dX) MPX_LNGP_D(MPX_BF16, true);
+      else MPX_LNGP_D(MPX_BF16, false);
+      colsum_final_kernel<MPX_BF16><<<fin2, 256, 0, s>>>(part, nbg, 2 * d, (uint16_t*)dgamma, (uint16_t*)dbeta,
+                                                         d, d_nonfinite);
+    }
+#undef MPX_LNGP_D
+#undef MPX_LNGP
+    MPX_LAUNCHED();
+    return MPX_OK;
+  }
   if (dX && !part && ln_grouped(d, {X, gamma, dY, Rgrad, dX}, {ldx, ldo})) {
     const int rows_per_block = d == 768 ? 8 : 16;
     const unsigned g2 = (unsigned)((rows + rows_per_block - 1) / rows_per_block);
