@@ -516,6 +516,64 @@ __global__ __launch_bounds__(256) void layernorm_fwd_group_kernel(
   }
 }
 
+// The input cast fused with the first LayerNorm, in row groups: each float32
+// chunk is rounded to half, written out, and normalised as the grouped
+// forward normalises that half row (the bits of the cast followed by the
+// LayerNorm, as layernorm_fwd_cast_kernel).
+template <int DT, int LPR, int VPL, int NCH>
+__global__ __launch_bounds__(256) void layernorm_fwd_cast_group_kernel(
+    const float* __restrict__ X, int64_t ldx, const uint16_t* __restrict__ gamma,
+    const uint16_t* __restrict__ beta, uint16_t* __restrict__ Xh, uint16_t* __restrict__ Y,
+    float* __restrict__ mr, int64_t rows) {
+  using G = LnGroup<LPR, VPL, NCH>;
+  const int lane = threadIdx.x & 63, li = lane % LPR;
+  const int64_t r = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * G::K + lane / LPR;
+  const int64_t rc = r < rows ? r : rows - 1;
+  GroupRow<DT, LPR, VPL, NCH> x, g, b;
+#pragma unroll
+  for (int k = 0; k < G::K; ++k)
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      if (!G::valid(k, v)) {
+        x.w[k][v] = u32x4{0u, 0u, 0u, 0u};
+        continue;
+      }
+      const float* src = X + rc * ldx + 8 * G::chunk(li, k, v);
+      const f32x4 lo = *reinterpret_cast<const f32x4*>(src);
+      const f32x4 hi = *reinterpret_cast<const f32x4*>(src + 4);
+      x.w[k][v] = u32x4{(uint32_t)f2h<DT>(lo[0]) | ((uint32_t)f2h<DT>(lo[1]) << 16),
+                        (uint32_t)f2h<DT>(lo[2]) | ((uint32_t)f2h<DT>(lo[3]) << 16),
+                        (uint32_t)f2h<DT>(hi[0]) | ((uint32_t)f2h<DT>(hi[1]) << 16),
+                        (uint32_t)f2h<DT>(hi[2]) | ((uint32_t)f2h<DT>(hi[3]) << 16)};
+    }
+  g.load(gamma, li);
+  b.load(beta, li);
+  float mean, rstd;
+  group_row_stats(x, mean, rstd);
+  if (r >= rows) return;
+#pragma unroll
+  for (int k = 0; k < G::K; ++k)
+#pragma unroll
+    for (int v = 0; v < VPL; ++v) {
+      if (!G::valid(k, v)) continue;
+      const int64_t off = r * G::D + 8 * G::chunk(li, k, v);
+      *reinterpret_cast<u32x4*>(Xh + off) = x.w[k][v];
+      uint32_t o[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const uint16_t lo = f2h<DT>(ln_affine(x.f(k, v, 2 * j), mean, rstd, g.f(k, v, 2 * j), b.f(k, v, 2 * j)));
+        const uint16_t hi =
+            f2h<DT>(ln_affine(x.f(k, v, 2 * j + 1), mean, rstd, g.f(k, v, 2 * j + 1), b.f(k, v, 2 * j + 1)));
+        o[j] = lo | ((uint32_t)hi << 16);
+      }
+      *reinterpret_cast<u32x4*>(Y + off) = u32x4{o[0], o[1], o[2], o[3]};
+    }
+  if (mr && li == 0) {
+    mr[2 * r] = mean;
+    mr[2 * r + 1] = rstd;
+  }
+}
+
 // dX of one group row from its loaded x, dY, gamma (and residual
 // cotangent): the arithmetic of layernorm_bwd_kernel's dX, shared by the
 // grouped kernels with and without gamma / beta (the same bits either way).
@@ -1351,8 +1409,25 @@ extern "C" int mpx_layernorm_fwd_cast(const float* X, int64_t ldx, const void* g
   MPX_REQUIRE(X && gamma && beta && Xh && Y, "NULL argument");
   MPX_REQUIRE(rows >= 1 && d >= 1 && d <= 2048 && ldx >= d, "bad sizes (1 <= d <= 2048, ldx >= d)");
   MPX_REQUIRE(is_half(dt), "dt must be MPX_F16 or MPX_BF16");
-  const unsigned grid = (unsigned)((rows + 3) / 4);
   hipStream_t s = (hipStream_t)stream;
+  if (ldx % 4 == 0 && ln_grouped(d, {X, gamma, beta, Xh, Y}, {})) {
+    const int rows_per_block = d == 768 ? 8 : 16;
+    const unsigned g2 = (unsigned)((rows + rows_per_block - 1) / rows_per_block);
+#define MPX_LNGC(DTv, LPR, VPL, NCH)                                                              \
+  layernorm_fwd_cast_group_kernel<DTv, LPR, VPL, NCH><<<g2, 256, 0, s>>>(                         \
+      X, ldx, (const uint16_t*)gamma, (const uint16_t*)beta, (uint16_t*)Xh, (uint16_t*)Y, mean_rstd, rows)
+    if (dt == MPX_F16) {
+      if (d == 768) MPX_LNGC(MPX_F16, 32, 2, 96);
+      else MPX_LNGC(MPX_F16, 16, 1, 48);
+    } else {
+      if (d == 768) MPX_LNGC(MPX_BF16, 32, 2, 96);
+      else MPX_LNGC(MPX_BF16, 16, 1, 48);
+    }
+#undef MPX_LNGC
+    MPX_LAUNCHED();
+    return MPX_OK;
+  }
+  const unsigned grid = (unsigned)((rows + 3) / 4);
   const int vpl = vpl_for(d);
 #define MPX_LNC(DTv, V)                                                                          \
   layernorm_fwd_cast_kernel<DTv, V><<<grid, 256, 0, s>>>(X, ldx, (const uint16_t*)gamma,        \

@@ -647,7 +647,8 @@ def test_nonfinite_counts_of_layernorm_head_and_embedding(fmt):
 
 
 @pytest.mark.parametrize("fmt", ["f16", "bf16"])
-@pytest.mark.parametrize("rows,d,ldx", [(8320, 384, 384), (65, 100, 104), (7, 768, 768), (33, 1500, 1501)])
+@pytest.mark.parametrize("rows,d,ldx", [(8320, 384, 384), (65, 100, 104), (7, 768, 768), (33, 1500, 1501),
+                                        (9, 384, 386), (12608, 768, 768)])
 def test_layernorm_fwd_cast_matches_cast_then_layernorm(fmt, rows, d, ldx):
     """The input cast fused with the first LayerNorm gives the same bits as
     the cast followed by the LayerNorm (both outputs and the row stats)."""
