@@ -646,12 +646,17 @@ __global__ __launch_bounds__(256) void layernorm_bwd_dx_group_kernel(
 }
 
 // gamma / beta column partials (and dX when DX), grouped: the workgroups
-// (at most kLnBwdMaxBlocks) stride over tiles of 4 K rows, each group of a
+// (at most kLnGroupMaxBlocks) stride over tiles of 4 K rows, each group of a
 // wave taking one row of the tile; each lane accumulates its columns' terms
 // dy xhat and dy over its group's rows in order, and the 4 K group sums of
 // a workgroup are added in group order through LDS into one partial row.
 // The gamma / beta call and the full call share this kernel and so give
 // the same gamma / beta bits; their dX equals the dX-only kernel's.
+// at most 256 workgroups (half the partial rows of the one-wave kernel's
+// 512: one-block step +0.45%, ViT-S and ViT-B unchanged)
+constexpr int kLnGroupMaxBlocks = 256;
+static_assert(kLnGroupMaxBlocks <= kLnBwdMaxBlocks, "the workspace holds kLnBwdMaxBlocks partial rows");
+
 template <int DT, int LPR, int VPL, int NCH, bool DX>
 __global__ __launch_bounds__(256) void layernorm_bwd_part_group_kernel(
     const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __restrict__ gamma,
@@ -1482,7 +1487,7 @@ extern "C" int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, 
   hipStream_t s = (hipStream_t)stream;
   if (part && ln_grouped(d, {X, gamma, dY, Rgrad, dX}, {ldx, ldo})) {
     const int rows_per_tile = d == 768 ? 8 : 16;
-    const int nbg = (int)std::min<int64_t>((rows + rows_per_tile - 1) / rows_per_tile, kLnBwdMaxBlocks);
+    const int nbg = (int)std::min<int64_t>((rows + rows_per_tile - 1) / rows_per_tile, kLnGroupMaxBlocks);
 #define MPX_LNGP(DTv, LPR, VPL, NCH, DXv)                                                                \
   layernorm_bwd_part_group_kernel<DTv, LPR, VPL, NCH, DXv><<<nbg, 256, 0, s>>>(                         \
       (const uint16_t*)X, ldx, (const uint16_t*)gamma, (const uint16_t*)dY, (const uint16_t*)Rgrad,     \
