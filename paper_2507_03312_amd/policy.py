@@ -21,6 +21,7 @@ belong around a step, not inside a captured one.
 from __future__ import annotations
 
 import collections
+import copy
 import functools
 from typing import Any, Callable, List, Optional, Tuple
 
@@ -68,7 +69,12 @@ def _flatten(tree) -> Tuple[List[Any], Callable[[List[Any]], Any]]:
             out.append(rb(new[i:i + n]))
             i += n
         if keys is not None:
-            return type(tree)(zip(keys, out)) if type(tree) is not dict else dict(zip(keys, out))
+            if type(tree) is dict:
+                return dict(zip(keys, out))
+            new = copy.copy(tree)  # dict subclasses keep their type and state (a default factory)
+            new.clear()
+            new.update(zip(keys, out))
+            return new
         if isinstance(tree, tuple) and hasattr(tree, "_fields"):  # named tuple
             return type(tree)(*out)
         return type(tree)(out)

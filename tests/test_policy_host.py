@@ -20,6 +20,15 @@ def test_trees_without_floating_leaves_pass_through_unchanged():
         assert type(out["y"]) is T and type(out["x"][1]) is tuple
 
 
+def test_dict_subclasses_keep_their_type_and_state():
+    dd = collections.defaultdict(list, {"a": torch.arange(2)})
+    od = collections.OrderedDict([("z", 1), ("y", torch.arange(3))])
+    out = policy.cast_tree({"dd": dd, "od": od}, "f16")
+    assert type(out["dd"]) is collections.defaultdict and out["dd"].default_factory is list
+    assert type(out["od"]) is collections.OrderedDict and list(out["od"]) == ["z", "y"]
+    assert out["dd"]["a"] is dd["a"] and out["od"]["y"] is od["y"]
+
+
 def test_leaves_already_in_the_target_type_are_not_copied():
     # host tensors are fine as long as nothing has to be cast
     a = torch.ones(3, dtype=torch.bfloat16)
