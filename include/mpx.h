@@ -307,7 +307,8 @@ int mpx_layernorm_fwd_cast(const float* X, int64_t ldx, const void* gamma, const
  * half(column sums); their partial sums use `workspace` (float32,
  * mpx_layernorm_bwd_workspace bytes).  dX (NULL: skipped) and the pair
  * dgamma / dbeta (both NULL: skipped, no workspace needed) may be requested
- * in separate calls, e.g. on two streams; at least one must be given.
+ * in separate calls, e.g. on two streams; at least one must be given; the
+ * split calls give the same bits as one call computing both.
  * d_nonfinite (nullable) counts non-finite dgamma / dbeta elements. */
 int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, const void* dY,
                       const void* Rgrad, void* dX, int64_t ldo, void* dgamma, void* dbeta,
@@ -362,7 +363,10 @@ size_t mpx_classifier_head_workspace(int64_t B, int64_t d);
  * X: B rows of width d with row stride ldx (e.g. the CLS rows of a
  * [B, T, d] activation: ldx = T d); labels: int32 [B]; 1 <= C <= 32,
  * 1 <= d <= 2048, C * d <= 16384 (W is staged in on-chip memory), B <= 2048.  Every result is the same bits as the separate
- * calls give (same arithmetic, summation orders and roundings).  The weight
+ * calls give (same arithmetic, summation orders and roundings), except
+ * dgamma and dbeta when mpx_layernorm_bwd works in row groups (d = 384 or
+ * 768 with 16-byte aligned rows): it adds the same float32 terms over the
+ * rows in another grouping, so those two can differ in the last place.  The weight
  * and bias gradients of the linear layer are left to mpx_linear_bwd (from Z
  * and dlogits).  d_nonfinite (nullable) counts non-finite dgamma / dbeta
  * elements.  A label outside [0, C) makes the loss NaN.  Errors:
