@@ -146,10 +146,11 @@ def test_layernorm_row_groups_match_one_wave_rows(fmt, rows, d):
 
 
 @pytest.mark.parametrize("fmt", FMTS)
-def test_layernorm_bwd_subsets_match_full_call(fmt):
+@pytest.mark.parametrize("rows,d", [(8321, 384), (12608, 768), (37, 768), (1000, 256)])
+def test_layernorm_bwd_subsets_match_full_call(fmt, rows, d):
     """dX alone (no workspace) and dgamma / dbeta alone, as the two-stream
-    backward issues them, give the bits of the full call."""
-    rows, d = 8321, 384
+    backward issues them, give the bits of the full call (row groups at
+    d = 384 and 768, one wave per row at d = 256)."""
     x = _rand((rows, d), fmt, 11, 2.0, 0.5)
     g = _rand((d,), fmt, 12, 0.2, 1.0)
     dy, rg = _rand((rows, d), fmt, 13), _rand((rows, d), fmt, 14)
