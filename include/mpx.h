@@ -30,8 +30,7 @@
  *    mpx_softmax_fwd/bwd, mpx_cross_entropy, mpx_mse, mpx_patchify_cast and
  *    mpx_embed_assemble(_bwd) also accept dt == MPX_F32: every tensor named
  *    "half" in their description is then float32 and half() is the identity
- *    (the float32 LayerNorm backward takes d <= 1024; d_nonfinite must be
- *    NULL).
+ *    (d_nonfinite must be NULL).
  *  - Return value: MPX_OK (0) or a negative code; mpx_last_error() gives a
  *    message (per host thread).  Invalid arguments are detected before
  *    anything is launched.  Non-finite DATA is never an error: it is reported

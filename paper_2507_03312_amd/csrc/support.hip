@@ -1469,7 +1469,6 @@ extern "C" int mpx_layernorm_bwd(const void* X, int64_t ldx, const void* gamma, 
   MPX_REQUIRE(dX || dgamma, "nothing to compute: dX, dgamma and dbeta are all NULL");
   MPX_REQUIRE(rows >= 1 && d >= 1 && d <= 2048 && ldx >= d && ldo >= d, "bad sizes");
   MPX_REQUIRE(is_half(dt) || dt == MPX_F32, "dt must be MPX_F16, MPX_BF16 or MPX_F32");
-  MPX_REQUIRE(dt != MPX_F32 || d <= kLnF32MaxD, "MPX_F32 LayerNorm backward needs d <= 1024");
   MPX_REQUIRE(dt != MPX_F32 || !d_nonfinite, "d_nonfinite is counted for half gradients only");
   float* part = nullptr;
   if (dgamma) {  // only the gamma / beta gradients use the workspace

@@ -10,9 +10,9 @@
 
 namespace mpx {
 
-// LayerNorm limits of the float32 backward: the gamma / beta partials of a
-// workgroup's four waves are combined in LDS
-constexpr int64_t kLnF32MaxD = 1024;
+// LayerNorm limit of the float32 backward (the half one's): the gamma / beta
+// partials of a workgroup's four waves are combined in LDS
+constexpr int64_t kLnF32MaxD = 2048;
 
 hipError_t launch_layernorm_fwd_f32(const float* X, int64_t ldx, const float* gamma,
                                     const float* beta, float* Y, float* mean_rstd, int64_t rows,

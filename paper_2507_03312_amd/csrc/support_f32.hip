@@ -54,13 +54,16 @@ __global__ __launch_bounds__(256) void layernorm_fwd_f32_kernel(const float* __r
 // the gamma / beta column sums (dY xhat, dY) of the rows a workgroup's four
 // waves visit go to part[block][0:d] and part[block][d:2d], the waves'
 // register sums combined in LDS in wave order.
-constexpr int kCpl = kLnF32MaxD / 64;  // columns per lane
 
+// CPL columns per lane (16 up to d = 1024, 32 up to 2048), one running
+// gamma / beta sum per column
+template <int CPL>
 __global__ __launch_bounds__(256) void layernorm_bwd_f32_kernel(
     const float* __restrict__ X, int64_t ldx, const float* __restrict__ gamma,
     const float* __restrict__ dY, const float* __restrict__ Rg, float* __restrict__ dX, int64_t ldo,
     int64_t rows, int64_t d, float* __restrict__ part) {
-  __shared__ float red[4][2 * kLnF32MaxD];
+  constexpr int kCpl = CPL;
+  __shared__ float red[4][2 * 64 * CPL];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   float pg[kCpl], pb[kCpl];
 #pragma unroll
@@ -242,8 +245,11 @@ hipError_t launch_layernorm_bwd_f32(const float* X, int64_t ldx, const float* ga
                                     float* part, hipStream_t s) {
   if (d > kLnF32MaxD) return hipErrorInvalidValue;
   const int64_t nb = ln_bwd_f32_blocks(rows);
-  layernorm_bwd_f32_kernel<<<(unsigned)nb, 256, 0, s>>>(X, ldx, gamma, dY, Rgrad, dX, ldo, rows, d,
-                                                        dgamma ? part : nullptr);
+  float* pt = dgamma ? part : nullptr;
+  if (d <= 1024)
+    layernorm_bwd_f32_kernel<16><<<(unsigned)nb, 256, 0, s>>>(X, ldx, gamma, dY, Rgrad, dX, ldo, rows, d, pt);
+  else
+    layernorm_bwd_f32_kernel<32><<<(unsigned)nb, 256, 0, s>>>(X, ldx, gamma, dY, Rgrad, dX, ldo, rows, d, pt);
   if (dgamma)
     ln_partials_final_f32_kernel<<<(unsigned)((2 * d + 255) / 256), 256, 0, s>>>(part, nb, d, dgamma, dbeta);
   return hipGetLastError();

@@ -51,8 +51,8 @@ def test_argument_checks_of_the_float32_and_fused_paths():
     dereferenced or launched (the pointers here are placeholders)."""
     from paper_2507_03312_amd import binding as mx
     p = 256  # never dereferenced: every call below fails its checks first
-    with pytest.raises(mx.MPXError, match="d <= 1024"):
-        mx.mpx_layernorm_bwd(p, 2048, p, p, None, p, 2048, None, None, 4, 2048, mx.MPX_F32, None, 0,
+    with pytest.raises(mx.MPXError, match="bad sizes"):
+        mx.mpx_layernorm_bwd(p, 2049, p, p, None, p, 2049, None, None, 4, 2049, mx.MPX_F32, None, 0,
                              None, 0)
     with pytest.raises(mx.MPXError, match="half gradients only"):
         mx.mpx_linear_bwd(p, None, p, None, 0, None, p, None, 8, 8, 8, mx.MPX_F32, p, 1 << 20, p, 0)

@@ -482,7 +482,7 @@ def _close32(got, ref, scale, rel=2e-6, what=""):
     assert np.all(err <= bnd), f"{what}: worst {err.max():.3g} (bound {bnd[np.argmax(err - bnd)]:.3g})"
 
 
-@pytest.mark.parametrize("rows,d", [(130, 384), (7, 768), (65, 100)])
+@pytest.mark.parametrize("rows,d", [(130, 384), (7, 768), (65, 100), (33, 1500), (9, 2048)])
 def test_layernorm_f32(rows, d):
     pol = Policy("f32")
     rng = np.random.default_rng(rows + d)
